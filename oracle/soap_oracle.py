@@ -1,0 +1,186 @@
+"""fp64 oracle of one SOAP optimizer step (TEST INFRASTRUCTURE ONLY).
+
+Only tests/, the smoke check and the bench's CPU-baseline leg may import this
+module.  Every input is the exact fp32 array handed to the GPU, promoted to fp64.
+
+The step follows the paper's KL-SOAP listing (Algorithm 2, "KL-SOAP used in
+experiments") with the plain-EMA Kronecker factors of the Shampoo primer
+(Section 2), refresh frequency F = 1 (hyperparameter table of Section 5.4) and
+the real-time refresh of Section 5.4.2 (the current gradient enters the factors
+before the eigenbasis is recomputed).  Readings where the paper is silent or
+inconsistent:
+
+  * EMA coefficients multiply the OLD state (Section 2 primer, Muon Algorithm 1,
+    the hyperparameter table's "EMA coefficient" wording); Algorithm 2's
+    placement of beta on the new term is read as a notation slip.
+  * The first moment is kept in weight space and rotated every step,
+    M' = Q_L^T M Q_R (Eq. 1).  With F = 1 and orthogonal Q this equals Algorithm
+    2's rotate-back / rotate-in of an eigenbasis-resident m (pinned in tests).
+  * V lives in the eigenbasis and is not re-rotated at a refresh (Algorithm 2
+    touches only m there).
+  * Adam bias correction is on by default (c1 = 1 - beta1^t, c2 = 1 - beta2^t),
+    eps is added to sqrt(V / c2); with the flag off the step is Algorithm 2
+    literally.  Identity eigenbases then reproduce AdamW (Section 2).
+  * One beta2 serves the factor EMA and V (the table gives both 0.95).
+  * QR(.).Q means the Q factor with non-negative diagonal R (unique for
+    nonsingular input).
+  * Initial state: L = R = Q_L = Q_R = I, M = V = 0.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+from . import build as _build
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        path = _build.build()
+        lib = ctypes.CDLL(path)
+        lib.oracle_householder_qr.restype = ctypes.c_int
+        lib.oracle_householder_qr.argtypes = [
+            ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int]
+        _LIB = lib
+    return _LIB
+
+
+def _threads() -> int:
+    return int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+
+
+@dataclasses.dataclass
+class OracleState:
+    """Per-matrix SOAP state (Algorithm 2 "Optimizer States"), fp64.
+
+    W, M, V: m x n (M in weight space, V in the eigenbasis); L, Q_L: m x m;
+    R, Q_R: n x n.
+    """
+    W: np.ndarray
+    L: np.ndarray
+    R: np.ndarray
+    QL: np.ndarray
+    QR: np.ndarray
+    M: np.ndarray
+    V: np.ndarray
+
+    def copy(self) -> "OracleState":
+        return OracleState(*(np.array(getattr(self, f.name), copy=True)
+                             for f in dataclasses.fields(self)))
+
+
+def init_state(W: np.ndarray) -> OracleState:
+    """L = R = Q_L = Q_R = I and M = V = 0 (initial state; the paper gives none)."""
+    m, n = W.shape
+    return OracleState(np.array(W, dtype=np.float64), np.eye(m), np.eye(n), np.eye(m),
+                       np.eye(n), np.zeros((m, n)), np.zeros((m, n)))
+
+
+def factor_ema(F: np.ndarray, X: np.ndarray, beta: float) -> np.ndarray:
+    """Kronecker-factor EMA of the Shampoo primer (Section 2):
+    F <- beta F + (1 - beta) X X^T.  For L pass X = G, for R pass X = G^T.
+
+    The result is symmetric by definition; it is formed from its lower triangle
+    (the old F is read only there) and mirrored."""
+    S = beta * np.asarray(F, dtype=np.float64) + (1.0 - beta) * (X @ X.T)
+    low = np.tril(S)
+    return low + np.tril(low, -1).T
+
+
+def householder_qr(A: np.ndarray, with_r: bool = False):
+    """Q of A = QR with non-negative diag(R), by textbook unblocked Householder
+    (see householder.c).  Algorithm 2's eigenbasis refresh applies this to
+    L_t Q_L and R_t Q_R."""
+    A = np.ascontiguousarray(A, dtype=np.float64)
+    n = A.shape[0]
+    if A.shape != (n, n):
+        raise ValueError("square matrices only")
+    Q = np.empty((n, n))
+    R = np.empty((n, n)) if with_r else None
+    rc = _lib().oracle_householder_qr(n, A.ctypes.data, Q.ctypes.data,
+                                      R.ctypes.data if with_r else None, _threads())
+    if rc != 0:
+        raise RuntimeError("oracle QR failed")
+    return (Q, R) if with_r else Q
+
+
+def momentum_ema(M: np.ndarray, G: np.ndarray, beta1: float) -> np.ndarray:
+    """First-moment EMA in weight space (Section 2 primer; Eq. 1 rotates m_t):
+    M <- beta1 M + (1 - beta1) G."""
+    return beta1 * M + (1.0 - beta1) * G
+
+
+def rotate_in(QL: np.ndarray, X: np.ndarray, QR: np.ndarray) -> np.ndarray:
+    """Rotation into the eigenbasis, Q_L^T X Q_R (Algorithm 2, "Rotate gradient
+    into eigenbasis"; Eq. 1 for the first moment).  Evaluated as (Q_L^T X) Q_R."""
+    return (QL.T @ X) @ QR
+
+
+def bias_corrections(beta1: float, beta2: float, t: int, enabled: bool) -> Tuple[float, float]:
+    """Adam bias corrections c1 = 1 - beta1^t, c2 = 1 - beta2^t (1, 1 when off)."""
+    if not enabled:
+        return 1.0, 1.0
+    return 1.0 - beta1 ** t, 1.0 - beta2 ** t
+
+
+def adam_eigenbasis(Gp: np.ndarray, Mp: np.ndarray, V: np.ndarray, beta2: float,
+                    eps: float, c1: float, c2: float) -> Tuple[np.ndarray, np.ndarray]:
+    """Adam in the eigenbasis (Algorithm 2, "Calculate Adam update"):
+    V <- beta2 V + (1 - beta2) G' * G';  N = (M'/c1) / (sqrt(V/c2) + eps)."""
+    V = beta2 * V + (1.0 - beta2) * Gp * Gp
+    N = (Mp / c1) / (np.sqrt(V / c2) + eps)
+    return V, N
+
+
+def rotate_out(QL: np.ndarray, N: np.ndarray, QR: np.ndarray) -> np.ndarray:
+    """Rotation back, Delta W = Q_L N Q_R^T (Algorithm 2, "Rotate update out of
+    eigenbasis").  Evaluated as (Q_L N) Q_R^T."""
+    return (QL @ N) @ QR.T
+
+
+def weight_update(W: np.ndarray, dW: np.ndarray, lr: float, wd: float) -> np.ndarray:
+    """Decoupled weight decay and update (Algorithm 2, last step):
+    W <- (1 - lr wd) W - lr Delta W."""
+    return (1.0 - lr * wd) * W - lr * dW
+
+
+def soap_step(state: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
+              eps: float, lr: float, weight_decay: float, bias_correction: bool = True,
+              diagnostics: bool = False):
+    """One SOAP step on one matrix (Algorithm 2 with F = 1, real-time refresh).
+
+    Order: factor EMA with the current G, power product and QR refresh, first
+    moment EMA, rotation in, Adam, rotation out, weight update.  Returns the new
+    state (and a dict of intermediates when ``diagnostics``)."""
+    if t < 1:
+        raise ValueError("step t is 1-based")
+    G = np.asarray(G, dtype=np.float64)
+    s = state.copy()
+    s.L = factor_ema(s.L, G, beta2)
+    s.R = factor_ema(s.R, G.T, beta2)
+    AL = s.L @ s.QL
+    AR = s.R @ s.QR
+    s.QL = householder_qr(AL)
+    s.QR = householder_qr(AR)
+    s.M = momentum_ema(s.M, G, beta1)
+    Gp = rotate_in(s.QL, G, s.QR)
+    Mp = rotate_in(s.QL, s.M, s.QR)
+    c1, c2 = bias_corrections(beta1, beta2, t, bias_correction)
+    s.V, N = adam_eigenbasis(Gp, Mp, s.V, beta2, eps, c1, c2)
+    dW = rotate_out(s.QL, N, s.QR)
+    s.W = weight_update(s.W, dW, lr, weight_decay)
+    if diagnostics:
+        return s, {"AL": AL, "AR": AR, "Gp": Gp, "Mp": Mp, "N": N, "dW": dW}
+    return s
+
+
+def soap_step_batched(states, Gs, t: int, **hp):
+    """The batched entry point is B independent single-matrix steps."""
+    return [soap_step(st, G, t, **hp) for st, G in zip(states, Gs)]
