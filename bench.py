@@ -1,0 +1,159 @@
+"""SOAP optimizer-step throughput on one MI355X.
+
+Workload: one 4096 x 14336 fp32 weight (MLP up-projection shape), low-rank
+(rank 128) plus 10%-noise synthetic gradients, every step a full SOAP update
+with per-step QR refresh of both eigenbases (R is 14336 x 14336).  Gradients
+are generated and copied to HBM before the timed region.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+Prints ONE JSON line.  `value` is steps/s of the whole step; `roofline`
+describes the dominant kernel (timed with HIP events on the library's stream
+through the soap_timing_* API); `cpu_baseline` times the fp64 oracle on a
+bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak (256 CU x 256 flop/clk x 2.4 GHz)
+PEAK_HBM_GBS = 8000.0
+HP = dict(beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3, weight_decay=0.1)
+
+
+def step_flops(m: int, n: int) -> float:
+    """Algorithmic flops of one SOAP step on an m x n weight: one triangle of
+    each factor EMA, the two power products, Householder QR with explicit Q of
+    both factors, and three rotation pairs (the Adam/momentum terms are O(mn))."""
+    syrk = m * (m + 1) * n + n * (n + 1) * m
+    power = 2.0 * (m ** 3 + n ** 3)
+    qr = (8.0 / 3.0) * (m ** 3 + n ** 3)
+    rot = 6.0 * m * n * (m + n)
+    return syrk + power + qr + rot
+
+
+def cpu_baseline(m: int, n: int, rank: int, scale: int = 4):
+    """Times one fp64 oracle step on the workload shrunk by `scale` per side
+    (same aspect ratio, rank and noise recipe) and scales the time by
+    step_flops(m, n) / step_flops(m/scale, n/scale) (= scale^3: the step's work
+    is a homogeneous cubic in the dimensions)."""
+    import oracle
+    from synth import gradients as sg
+    ms, ns = m // scale, n // scale
+    spec = sg.MatrixSpec("cpu_sample", ms, ns, max(1, rank // scale), "rel", 0.10)
+    G = next(sg.make_matrix_stream(spec, 2, 1)).astype(np.float64)
+    st = oracle.init_state(sg.initial_weight(spec, 2).astype(np.float64))
+    t0 = time.perf_counter()
+    oracle.soap_step(st, G, 1, **HP)
+    dt = time.perf_counter() - t0
+    ratio = step_flops(m, n) / step_flops(ms, ns)
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
+    return {
+        "value": 1.0 / (dt * ratio), "unit": "steps/s", "cores": threads, "kind": "oracle",
+        "sample": (f"one fp64 oracle step on a {ms}x{ns} matrix (the {m}x{n} workload at 1/{scale} "
+                   f"per side, rank {spec.rank}, 10% noise) took {dt:.2f} s; scaled by the exact "
+                   f"flop ratio {ratio:.1f}"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the SOAP step of a "
+              "matrix is independent of every other matrix and this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2607_20548_amd as soap
+    from synth import gradients as sg
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    wl = sg.workload(2)
+    spec = wl.matrices[0]
+    m, n = spec.m, spec.n
+    total = args.warmup + args.steps
+    print(f"[bench] generating {total} gradients {m}x{n}", file=sys.stderr, flush=True)
+    grads = [torch.from_numpy(G).cuda() for G in sg.make_matrix_stream(spec, 2, total)]
+    W = torch.from_numpy(sg.initial_weight(spec, 2)).cuda()
+    state = soap.SoapState(m, n)
+    stream = torch.cuda.current_stream()
+
+    for t in range(1, args.warmup + 1):
+        state.step(W, grads[t - 1], t, **HP)
+    torch.cuda.synchronize()
+    soap.soap_init_state(1, m, n, state.L, state.R, state.Q_L, state.Q_R, state.M, state.V)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
+
+    soap.soap_timing_reset()
+    soap.soap_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(1, args.steps + 1):
+        state.step(W, grads[args.warmup + t - 1], t, stream=stream, **HP)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    soap.soap_timing_enable(False)
+    soap.soap_timing_collect()
+
+    stages = {}
+    for i in range(soap.soap_timing_num_stages()):
+        ms, launches, fl = soap.soap_timing_get(i)
+        stages[soap.soap_timing_stage_name(i)] = (ms, launches, fl)
+    # dominant single-kernel stage among the MFMA GEMMs (the QR stages are
+    # sequences of kernels and are reported separately)
+    single = {k: v for k, v in stages.items() if k.startswith(("power", "factor", "rotate"))
+              and v[1] > 0 and not k.startswith("rotate_in_QLt")}
+    dom = max(single, key=lambda k: single[k][0])
+    d_ms, d_n, d_fl = single[dom]
+    achieved = d_fl / (d_ms / d_n * 1e-3) / d_n / 1e12
+
+    F = step_flops(m, n)
+    value = args.steps / elapsed
+    out = {
+        "metric": "SOAP steps/s per weight shape + achieved MFMA TFLOPS fraction (1 GPU)",
+        "value": value,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded low-rank + noise gradients, rank 128, 10% noise)",
+        "config": {"workload": f"soap_step on one {m}x{n} fp32 weight (MLP up-projection), "
+                               f"QR refresh of both factors every step",
+                   "m": m, "n": n, "rank": spec.rank, "global_batch": 1, "seq_len": None,
+                   "parallelism": "none (1 GPU)"},
+        "step_tflops": F * value / 1e12,
+        "step_frac_of_fp32_mfma_peak": F * value / 1e12 / PEAK_FP32_MFMA_TFLOPS,
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
+                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
+                     "avg_launch_ms": d_ms / d_n},
+        "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(m, n, spec.rank)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

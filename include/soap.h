@@ -1,0 +1,152 @@
+/*
+ * soap.h — C ABI of the MI355X (gfx950) SOAP optimizer-step library.
+ *
+ * The library performs the per-weight-matrix SOAP update of "SOAP, Muon, and
+ * Beyond: Pushing LLM Pretraining Scales" (Algorithm 2, KL-SOAP listing, with
+ * the plain-EMA Kronecker factors of the Section 2 Shampoo primer, eigenbasis
+ * refresh every step (F = 1, hyperparameter table of Section 5.4) and the
+ * real-time refresh of Section 5.4.2).  One call of soap_step does, in order:
+ *
+ *   1. L <- b2 L + (1-b2) G G^T,   R <- b2 R + (1-b2) G^T G          (factor EMA)
+ *   2. Q_L <- QR(L Q_L).Q,  Q_R <- QR(R Q_R).Q, diag(R-factor) >= 0  (refresh)
+ *   3. M <- b1 M + (1-b1) G;  G' = Q_L^T G Q_R;  M' = Q_L^T M Q_R    (rotate in)
+ *   4. V <- b2 V + (1-b2) G'^2;  N = (M'/c1) / (sqrt(V/c2) + eps)    (Adam)
+ *   5. W <- (1 - lr wd) W - lr Q_L N Q_R^T                            (rotate out)
+ *
+ * with c1 = 1 - b1^t and c2 = 1 - b2^t (c1 = c2 = 1 under
+ * SOAP_FLAG_NO_BIAS_CORRECTION).  M is the first moment in weight space; by
+ * linearity and orthogonality of the Q this equals Algorithm 2's
+ * eigenbasis-resident m when the basis is refreshed every step.  V is indexed
+ * by (column of Q_L, column of Q_R).
+ *
+ * Conventions for every entry point:
+ *  - All matrices are fp32, row-major and dense: the leading dimension is the
+ *    number of columns.  A weight is m x n ("in" x "out" in Algorithm 2):
+ *    param, grad, M, V are m x n; L, Q_L are m x m; R, Q_R are n x n.
+ *    Batched tensors are contiguous [batch][rows][cols].
+ *  - Matrix pointers are DEVICE pointers (hipMalloc or torch device memory),
+ *    16-byte aligned.  The caller owns every buffer, including the workspace;
+ *    the library never allocates or frees device memory and keeps no state
+ *    between calls except the thread-local error string (and, only while
+ *    soap_timing_enable(1) is in force, a pool of HIP events).
+ *  - Work is enqueued on `stream` (0 = the null stream) and the call returns
+ *    without synchronising.  Validation happens on the host before anything is
+ *    enqueued: on failure nothing is enqueued, a negative soap_status is
+ *    returned and soap_last_error() describes it.  A HIP launch error is
+ *    reported as SOAP_ERR_HIP; a device fault surfaces at the caller's next
+ *    synchronisation.  NaN/Inf in the inputs propagate and are not checked.
+ *  - Calls on different streams are safe when their buffers and workspaces are
+ *    disjoint.  No C++ exception crosses this boundary.
+ *  - Every dimension must be in [1, SOAP_MAX_DIM].
+ */
+#ifndef SOAP_MI355X_H
+#define SOAP_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SOAP_OK = 0,
+  SOAP_ERR_NULL = -1,       /* a required pointer is NULL                       */
+  SOAP_ERR_SHAPE = -2,      /* batch/m/n outside [1, SOAP_MAX_DIM] or overflow   */
+  SOAP_ERR_HPARAM = -3,     /* beta outside [0,1), eps/lr/wd negative or not finite,
+                               step < 1, unknown flag bits                       */
+  SOAP_ERR_WORKSPACE = -4,  /* workspace smaller than the *_workspace_bytes value */
+  SOAP_ERR_ALIGN = -5,      /* a pointer is not 16-byte aligned                  */
+  SOAP_ERR_ALIAS = -6,      /* grad overlaps a buffer the call writes, or two
+                               written buffers overlap                           */
+  SOAP_ERR_HIP = -7         /* a HIP runtime call failed                         */
+} soap_status;
+
+enum { SOAP_FLAG_NO_BIAS_CORRECTION = 1u << 0 };
+
+#define SOAP_MAX_DIM 16384
+
+/* Bytes of device workspace soap_step / soap_step_batched need for `batch`
+ * matrices of shape m x n (batch = 1 for soap_step).  Returns 0 for an invalid
+ * shape.  The workspace holds the power products L Q_L and R Q_R, the QR
+ * block reflectors and the rotation intermediates; its contents need not be
+ * initialised and are garbage after the call. */
+size_t soap_workspace_bytes(int64_t batch, int64_t m, int64_t n);
+
+/* Initial optimizer state (the paper gives none; identity bases keep the
+ * first power product nonsingular): L = R = Q_L = Q_R = I, M = V = 0, for
+ * `batch` contiguous matrices.  Any of the six pointers may be NULL to skip
+ * that tensor. */
+int soap_init_state(int64_t batch, int64_t m, int64_t n, float *L, float *R, float *Q_L,
+                    float *Q_R, float *M, float *V, hipStream_t stream);
+
+/* One SOAP step on one m x n weight (Algorithm 2, F = 1).  `param`, L, R,
+ * Q_L, Q_R, M, V are updated in place; `grad` is read only.  L and R are read
+ * from their lower triangle and written fully symmetric.  `step` is the
+ * 1-based t of this update.  beta1, beta2 in [0,1); eps, lr, weight_decay
+ * finite and >= 0; flags is 0 or SOAP_FLAG_NO_BIAS_CORRECTION. */
+int soap_step(float *param, const float *grad, float *L, float *R, float *Q_L, float *Q_R,
+              float *M, float *V, int64_t m, int64_t n, float beta1, float beta2, float eps,
+              float lr, float weight_decay, int64_t step, uint32_t flags, void *workspace,
+              size_t workspace_bytes, hipStream_t stream);
+
+/* soap_step on `batch` same-shape matrices in one call (e.g. the experts of an
+ * MoE layer).  Every tensor is contiguous [batch][..][..] in the layout of
+ * soap_step; the matrices are independent and share the hyperparameters. */
+int soap_step_batched(int64_t batch, float *param, const float *grad, float *L, float *R,
+                      float *Q_L, float *Q_R, float *M, float *V, int64_t m, int64_t n,
+                      float beta1, float beta2, float eps, float lr, float weight_decay,
+                      int64_t step, uint32_t flags, void *workspace, size_t workspace_bytes,
+                      hipStream_t stream);
+
+/* Description of the last failure on the calling thread ("" after success).
+ * Valid until the next call on the same thread. */
+const char *soap_last_error(void);
+
+/* ---- stage entry points (used by the tests to check each kernel alone) ---- */
+
+/* Eigenbasis refresh QR (Algorithm 2, "QR(.).Q"): A = Q Rf for one n x n
+ * matrix, with diag(Rf) >= 0, by blocked Householder.  A is read only; Q (n x n)
+ * receives the Q factor; Rf (n x n, may be NULL) the triangular factor with its
+ * strict lower part zeroed. */
+size_t soap_qr_workspace_bytes(int64_t n);
+int soap_qr_f32(int64_t n, const float *A, float *Q, float *Rf, void *workspace,
+                size_t workspace_bytes, hipStream_t stream);
+
+/* The MFMA GEMM used for every product of the step:
+ * C = alpha * op(A) op(B) + beta * C, op(X) = X or X^T (trans != 0),
+ * op(A) M x K, op(B) K x N, row-major with leading dimensions lda, ldb, ldc.
+ * When beta == 0, C is not read. */
+int soap_gemm_f32(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, float alpha,
+                  const float *A, int64_t lda, const float *B, int64_t ldb, float beta,
+                  float *C, int64_t ldc, hipStream_t stream);
+
+/* Factor EMA (Section 2 primer): F <- beta F + (1 - beta) X X^T for X = G
+ * (trans = 0, F is m x m) or X = G^T (trans = 1, F is n x n), G m x n.  Only
+ * the lower triangle of X X^T is computed; F is written fully symmetric. */
+int soap_factor_ema_f32(int trans, int64_t m, int64_t n, const float *G, float *F, float beta,
+                        hipStream_t stream);
+
+/* ---- measurement ---- */
+
+/* When enabled, every stage of soap_step / soap_step_batched records a pair
+ * of HIP events on the call's stream.  soap_timing_collect synchronises on
+ * them and adds their durations to per-stage totals; soap_timing_reset clears
+ * the totals.  Stage ids are 0 .. soap_timing_num_stages()-1. */
+int soap_timing_enable(int enable);
+int soap_timing_num_stages(void);
+const char *soap_timing_stage_name(int stage);
+int soap_timing_collect(void);
+int soap_timing_reset(void);
+/* Totals since the last reset: milliseconds, launches, and the algorithmic
+ * flops of those launches (one triangle for the factor EMA, 2 m n k for a
+ * product, (4/3) n^3 + (4/3) n^3 for a QR with its explicit Q). */
+int soap_timing_get(int stage, double *total_ms, int64_t *launches, double *flops);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOAP_MI355X_H */

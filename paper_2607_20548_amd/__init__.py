@@ -1,0 +1,230 @@
+"""Python binding of the MI355X SOAP optimizer-step library (libsoap_mi355x.so).
+
+Argument marshalling only: every function forwards to the C entry point of the
+same name in ``include/soap.h``; all arithmetic runs in the HIP kernels.
+Matrix arguments may be torch tensors (fp32, contiguous, on the GPU) or raw
+integer device pointers; ``None`` passes NULL.  The stream defaults to torch's
+current stream.  A nonzero status raises ``SoapError`` carrying
+``soap_last_error()``.  There is no fallback: if the library is not built,
+``lib()`` raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsoap_mi355x.so")
+
+SOAP_OK = 0
+SOAP_ERR_NULL = -1
+SOAP_ERR_SHAPE = -2
+SOAP_ERR_HPARAM = -3
+SOAP_ERR_WORKSPACE = -4
+SOAP_ERR_ALIGN = -5
+SOAP_ERR_ALIAS = -6
+SOAP_ERR_HIP = -7
+SOAP_FLAG_NO_BIAS_CORRECTION = 1
+SOAP_MAX_DIM = 16384
+
+EXPORTED = [
+    "soap_workspace_bytes", "soap_init_state", "soap_step", "soap_step_batched",
+    "soap_last_error", "soap_qr_workspace_bytes", "soap_qr_f32", "soap_gemm_f32",
+    "soap_factor_ema_f32", "soap_timing_enable", "soap_timing_num_stages",
+    "soap_timing_stage_name", "soap_timing_collect", "soap_timing_reset", "soap_timing_get",
+]
+
+
+class SoapError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"soap status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_F = ctypes.c_float
+_U32 = ctypes.c_uint32
+_SZ = ctypes.c_size_t
+_INT = ctypes.c_int
+
+
+def lib() -> ctypes.CDLL:
+    """Load the built library (build it with paper_2607_20548_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(LIB_PATH)
+    sig = {
+        "soap_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
+        "soap_init_state": (_INT, [_I64, _I64, _I64, _P, _P, _P, _P, _P, _P, _P]),
+        "soap_step": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _F, _F,
+                             _I64, _U32, _P, _SZ, _P]),
+        "soap_step_batched": (_INT, [_I64, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F,
+                                     _F, _F, _F, _I64, _U32, _P, _SZ, _P]),
+        "soap_last_error": (ctypes.c_char_p, []),
+        "soap_qr_workspace_bytes": (_SZ, [_I64]),
+        "soap_qr_f32": (_INT, [_I64, _P, _P, _P, _P, _SZ, _P]),
+        "soap_gemm_f32": (_INT, [_INT, _INT, _I64, _I64, _I64, _F, _P, _I64, _P, _I64, _F, _P,
+                                 _I64, _P]),
+        "soap_factor_ema_f32": (_INT, [_INT, _I64, _I64, _P, _P, _F, _P]),
+        "soap_timing_enable": (_INT, [_INT]),
+        "soap_timing_num_stages": (_INT, []),
+        "soap_timing_stage_name": (ctypes.c_char_p, [_INT]),
+        "soap_timing_collect": (_INT, []),
+        "soap_timing_reset": (_INT, []),
+        "soap_timing_get": (_INT, [_INT, ctypes.POINTER(ctypes.c_double),
+                                   ctypes.POINTER(ctypes.c_int64),
+                                   ctypes.POINTER(ctypes.c_double)]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    import torch
+    if not isinstance(x, torch.Tensor):
+        raise TypeError(f"expected a torch tensor or an int pointer, got {type(x)}")
+    if x.dtype != torch.float32 and x.dtype != torch.uint8:
+        raise TypeError(f"tensors must be float32 (workspaces may be uint8), got {x.dtype}")
+    if not x.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not x.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        if not torch.cuda.is_available():
+            return None
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int) -> None:
+    if status != SOAP_OK:
+        raise SoapError(status, soap_last_error())
+
+
+def soap_last_error() -> str:
+    return lib().soap_last_error().decode()
+
+
+def soap_workspace_bytes(batch: int, m: int, n: int) -> int:
+    return lib().soap_workspace_bytes(batch, m, n)
+
+
+def soap_qr_workspace_bytes(n: int) -> int:
+    return lib().soap_qr_workspace_bytes(n)
+
+
+def soap_init_state(batch, m, n, L, R, Q_L, Q_R, M, V, stream=None) -> None:
+    _check(lib().soap_init_state(batch, m, n, _ptr(L), _ptr(R), _ptr(Q_L), _ptr(Q_R), _ptr(M),
+                                 _ptr(V), _stream(stream)))
+
+
+def soap_step(param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr, weight_decay,
+              step, flags, workspace, workspace_bytes, stream=None) -> None:
+    _check(lib().soap_step(_ptr(param), _ptr(grad), _ptr(L), _ptr(R), _ptr(Q_L), _ptr(Q_R),
+                           _ptr(M), _ptr(V), m, n, beta1, beta2, eps, lr, weight_decay, step,
+                           flags, _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def soap_step_batched(batch, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
+                      weight_decay, step, flags, workspace, workspace_bytes, stream=None) -> None:
+    _check(lib().soap_step_batched(batch, _ptr(param), _ptr(grad), _ptr(L), _ptr(R), _ptr(Q_L),
+                                   _ptr(Q_R), _ptr(M), _ptr(V), m, n, beta1, beta2, eps, lr,
+                                   weight_decay, step, flags, _ptr(workspace), workspace_bytes,
+                                   _stream(stream)))
+
+
+def soap_qr_f32(n, A, Q, Rf, workspace, workspace_bytes, stream=None) -> None:
+    _check(lib().soap_qr_f32(n, _ptr(A), _ptr(Q), _ptr(Rf), _ptr(workspace), workspace_bytes,
+                             _stream(stream)))
+
+
+def soap_gemm_f32(trans_a, trans_b, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc,
+                  stream=None) -> None:
+    _check(lib().soap_gemm_f32(int(trans_a), int(trans_b), M, N, K, alpha, _ptr(A), lda, _ptr(B),
+                               ldb, beta, _ptr(C), ldc, _stream(stream)))
+
+
+def soap_factor_ema_f32(trans, m, n, G, F, beta, stream=None) -> None:
+    _check(lib().soap_factor_ema_f32(int(trans), m, n, _ptr(G), _ptr(F), beta, _stream(stream)))
+
+
+def soap_timing_enable(enable: bool) -> None:
+    _check(lib().soap_timing_enable(int(bool(enable))))
+
+
+def soap_timing_num_stages() -> int:
+    return lib().soap_timing_num_stages()
+
+
+def soap_timing_stage_name(stage: int) -> str:
+    return lib().soap_timing_stage_name(stage).decode()
+
+
+def soap_timing_collect() -> None:
+    _check(lib().soap_timing_collect())
+
+
+def soap_timing_reset() -> None:
+    _check(lib().soap_timing_reset())
+
+
+def soap_timing_get(stage: int):
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    fl = ctypes.c_double()
+    _check(lib().soap_timing_get(stage, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(fl)))
+    return ms.value, n.value, fl.value
+
+
+# ---------------------------------------------------------------- helpers
+class SoapState:
+    """Device-resident SOAP state for `batch` m x n matrices (fp32, contiguous),
+    allocated with torch and initialised by soap_init_state."""
+
+    def __init__(self, m: int, n: int, batch: int = 1, device: str = "cuda"):
+        import torch
+        self.m, self.n, self.batch = m, n, batch
+        shp = (lambda r, c: (batch, r, c)) if batch > 1 else (lambda r, c: (r, c))
+        kw = dict(dtype=torch.float32, device=device)
+        self.L = torch.empty(shp(m, m), **kw)
+        self.R = torch.empty(shp(n, n), **kw)
+        self.Q_L = torch.empty(shp(m, m), **kw)
+        self.Q_R = torch.empty(shp(n, n), **kw)
+        self.M = torch.empty(shp(m, n), **kw)
+        self.V = torch.empty(shp(m, n), **kw)
+        self.ws_bytes = soap_workspace_bytes(batch, m, n)
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        soap_init_state(batch, m, n, self.L, self.R, self.Q_L, self.Q_R, self.M, self.V)
+
+    def step(self, param, grad, t: int, beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3,
+             weight_decay=0.1, flags=0, stream=None) -> None:
+        if self.batch == 1:
+            soap_step(param, grad, self.L, self.R, self.Q_L, self.Q_R, self.M, self.V, self.m,
+                      self.n, beta1, beta2, eps, lr, weight_decay, t, flags, self.workspace,
+                      self.ws_bytes, stream)
+        else:
+            soap_step_batched(self.batch, param, grad, self.L, self.R, self.Q_L, self.Q_R, self.M,
+                              self.V, self.m, self.n, beta1, beta2, eps, lr, weight_decay, t,
+                              flags, self.workspace, self.ws_bytes, stream)

@@ -1,0 +1,373 @@
+// fp32 GEMM on the CDNA4 matrix cores (v_mfma_f32_32x32x2_f32), used for every
+// dense product of the SOAP step: the factor EMAs (one triangle), the power
+// products L Q_L and R Q_R, the rotations and the compact-WY updates of the QR.
+//
+// Tiling: a 256-thread workgroup (4 wave64s in a 2 x 2 arrangement) computes a
+// 128 x 128 tile of C; each wave owns a 64 x 64 sub-tile held as 2 x 2 MFMA
+// 32x32 accumulators (64 accumulation registers per lane).  K advances in slabs
+// of 16 staged through double-buffered LDS.  Both operands are kept in LDS as
+// [x][k] rows (x = output row or column, k contiguous, padded to 20 floats so
+// that 16-byte reads of 16 consecutive lanes fall in distinct banks); a lane
+// then fetches the 8 k-values it feeds to 8 consecutive MFMAs with two
+// ds_read_b128.  Within a 16-slab, lane half h of the MFMA operand carries
+// k = 8h + s at MFMA step s; A and B use the same assignment, so the sum over
+// k is complete.
+//
+// Tile order: the 8 XCDs receive workgroups round-robin, so the linear tile
+// index is remapped to give each XCD a contiguous run of tiles, and that run is
+// walked in groups of 8 tile-rows so that neighbouring tiles share A rows and B
+// columns in the XCD's L2.
+#include "internal.h"
+
+namespace soap {
+namespace {
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128;
+constexpr int BN = 128;
+constexpr int BK = 16;
+constexpr int LDSK = BK + 4;            // padded LDS row stride in floats
+constexpr int TILE_FLOATS = 128 * LDSK;  // one operand tile in LDS
+constexpr int NTHREADS = 256;
+constexpr int GROUP_M = 8;
+
+enum { MODE_GENERAL = 0, MODE_SYRK = 1, MODE_ADAM = 2 };
+
+struct KParams {
+  int M, N, K;
+  const float *A;
+  int64_t lda, sA;
+  const float *A2;
+  const float *B;
+  int64_t ldb, sB;
+  float *C;
+  int64_t ldc, sC;
+  float alpha, beta;
+  float *V;
+  float *Nout;
+  float b2, c1, c2, eps;
+  int tiles_m, tiles_n, ntiles;
+  int kslice;       // K extent of one split-K slice (multiple of BK); = K when not split
+  float *part;      // split-K partials, or nullptr
+};
+
+// Loads one operand slab of 128 x-rows by BK k-values into registers.
+//   KCONTIG = true : global element (x, k) at base[x*ld + k]
+//   KCONTIG = false: global element (x, k) at base[k*ld + x]
+// Work split: 512 (x, k-quad) items over 256 threads, two per thread.
+template <bool KCONTIG, int VEC>
+struct SlabLoader {
+  float r[8];
+
+  __device__ __forceinline__ void load(const float *__restrict__ base, int64_t ld, int x0,
+                                       int k0, int X, int K, int tid) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int idx = tid + NTHREADS * s;
+      if (KCONTIG) {
+        const int x = x0 + (idx >> 2);
+        const int k = k0 + 4 * (idx & 3);
+        if (VEC == 4) {
+          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+          if (x < X && k < K) v = *reinterpret_cast<const float4 *>(base + (int64_t)x * ld + k);
+          r[4 * s + 0] = v.x; r[4 * s + 1] = v.y; r[4 * s + 2] = v.z; r[4 * s + 3] = v.w;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            r[4 * s + e] = (x < X && k + e < K) ? base[(int64_t)x * ld + k + e] : 0.f;
+        }
+      } else {
+        const int x = x0 + (idx & 127);
+        const int k = k0 + 4 * (idx >> 7);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          r[4 * s + e] = (x < X && k + e < K) ? base[(int64_t)(k + e) * ld + x] : 0.f;
+      }
+    }
+  }
+
+  __device__ __forceinline__ void store(float *lds, int tid) const {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int idx = tid + NTHREADS * s;
+      const int x = KCONTIG ? (idx >> 2) : (idx & 127);
+      const int kq = KCONTIG ? (idx & 3) : (idx >> 7);
+      *reinterpret_cast<float4 *>(lds + x * LDSK + 4 * kq) =
+          make_float4(r[4 * s + 0], r[4 * s + 1], r[4 * s + 2], r[4 * s + 3]);
+    }
+  }
+};
+
+__device__ __forceinline__ void read_frag(const float *lds, int x, int h, float (&f)[8]) {
+  const float4 lo = *reinterpret_cast<const float4 *>(lds + x * LDSK + 8 * h);
+  const float4 hi = *reinterpret_cast<const float4 *>(lds + x * LDSK + 8 * h + 4);
+  f[0] = lo.x; f[1] = lo.y; f[2] = lo.z; f[3] = lo.w;
+  f[4] = hi.x; f[5] = hi.y; f[6] = hi.z; f[7] = hi.w;
+}
+
+// Maps the linear workgroup id to a (tile-row, tile-column) pair.
+template <int MODE>
+__device__ __forceinline__ void tile_coords(const KParams &p, int &tm, int &tn) {
+  int t = blockIdx.x;
+  const int nt = p.ntiles;
+  if ((nt & 7) == 0) t = (t & 7) * (nt >> 3) + (t >> 3);  // contiguous run per XCD
+  if (MODE == MODE_SYRK) {
+    // lower-triangle tiles (tm >= tn), enumerated row by row
+    int r = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
+    while ((r + 1) * (r + 2) / 2 <= t) ++r;
+    while (r * (r + 1) / 2 > t) --r;
+    tm = r;
+    tn = t - r * (r + 1) / 2;
+  } else {
+    const int per_group = GROUP_M * p.tiles_n;
+    const int group = t / per_group;
+    const int first_m = group * GROUP_M;
+    const int gsz = min(p.tiles_m - first_m, GROUP_M);
+    const int in_group = t - group * per_group;
+    tm = first_m + in_group % gsz;
+    tn = in_group / gsz;
+  }
+}
+
+template <int TA, int TB, int VEC, int MODE, int TAG>
+__global__ __launch_bounds__(NTHREADS) void gemm_f32_mfma(KParams p) {
+  constexpr int NA = (MODE == MODE_ADAM) ? 2 : 1;
+  __shared__ __attribute__((aligned(16))) float lds[2 * (NA + 1) * TILE_FLOATS];
+
+  int tm, tn;
+  tile_coords<MODE>(p, tm, tn);
+  const int64_t bz = blockIdx.z;
+  const float *A = p.A + bz * p.sA;
+  const float *A2 = (MODE == MODE_ADAM) ? p.A2 + bz * p.sA : nullptr;
+  const float *B = p.B + bz * p.sB;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int xl = lane & 31, h = lane >> 5;
+
+  // op(A) rows are x = i: k-contiguous when TA == 0.  op(B) columns are x = j:
+  // k-contiguous when TB == 1.
+  SlabLoader<TA == 0, VEC> la, la2;
+  SlabLoader<TB == 1, VEC> lb;
+
+  v16f acc[NA][2][2];
+#pragma unroll
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[a][i][j][r] = 0.f;
+
+  auto buf = [&](int stage, int which) { return lds + (stage * (NA + 1) + which) * TILE_FLOATS; };
+
+  const int kbeg = blockIdx.y * p.kslice;
+  const int kend = min(p.K, kbeg + p.kslice);
+  const int nk = (kend - kbeg + BK - 1) / BK;
+  la.load(A, p.lda, m0, kbeg, p.M, kend, tid);
+  if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, kbeg, p.M, kend, tid);
+  lb.load(B, p.ldb, n0, kbeg, p.N, kend, tid);
+  la.store(buf(0, 0), tid);
+  if (MODE == MODE_ADAM) la2.store(buf(0, 1), tid);
+  lb.store(buf(0, NA), tid);
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      const int k0 = kbeg + (kt + 1) * BK;
+      la.load(A, p.lda, m0, k0, p.M, kend, tid);
+      if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, k0, p.M, kend, tid);
+      lb.load(B, p.ldb, n0, k0, p.N, kend, tid);
+    }
+    float fb[2][8];
+    read_frag(buf(cur, NA), wn * 64 + xl, h, fb[0]);
+    read_frag(buf(cur, NA), wn * 64 + 32 + xl, h, fb[1]);
+#pragma unroll
+    for (int a = 0; a < NA; ++a) {
+      float fa[2][8];
+      read_frag(buf(cur, a), wm * 64 + xl, h, fa[0]);
+      read_frag(buf(cur, a), wm * 64 + 32 + xl, h, fa[1]);
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[a][i][j] =
+                __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[a][i][j], 0, 0, 0);
+    }
+    if (more) {
+      la.store(buf(cur ^ 1, 0), tid);
+      if (MODE == MODE_ADAM) la2.store(buf(cur ^ 1, 1), tid);
+      lb.store(buf(cur ^ 1, NA), tid);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue.  Accumulator register r of block (i, j) holds
+  // C[row0 + 8*(r/4) + 4*h + r%4][col0 + xl].
+  float *C = p.C + bz * p.sC;
+  float *P = p.part ? p.part + (bz * gridDim.y + blockIdx.y) * (int64_t)p.M * p.N : nullptr;
+  float *V = (MODE == MODE_ADAM) ? p.V + bz * p.sC : nullptr;
+  float *Nout = (MODE == MODE_ADAM) ? p.Nout + bz * p.sC : nullptr;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wn * 64 + j * 32 + xl;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+        if (row >= p.M || col >= p.N) continue;
+        const int64_t off = (int64_t)row * p.ldc + col;
+        if (MODE == MODE_GENERAL && P) {
+          P[(int64_t)row * p.N + col] = acc[0][i][j][r];
+        } else if (MODE == MODE_GENERAL) {
+          float v = p.alpha * acc[0][i][j][r];
+          if (p.beta != 0.f) v += p.beta * C[off];
+          C[off] = v;
+        } else if (MODE == MODE_SYRK) {
+          if (row < col) continue;  // the mirror of (col,row) is written by its owner
+          const float v = p.beta * C[off] + p.alpha * acc[0][i][j][r];
+          C[off] = v;
+          if (row != col) C[(int64_t)col * p.ldc + row] = v;
+        } else {
+          const float g = acc[0][i][j][r];
+          const float mm = acc[1][i][j][r];
+          const float v = p.b2 * V[off] + (1.f - p.b2) * g * g;
+          V[off] = v;
+          Nout[off] = (mm / p.c1) / (sqrtf(v / p.c2) + p.eps);
+        }
+      }
+    }
+}
+
+// C = alpha * sum_s part[s] + beta * C, slices summed in index order.
+__global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ part, int S,
+                                                     int M, int N, float *C, int64_t ldc,
+                                                     int64_t sC, float alpha, float beta) {
+  const int64_t bz = blockIdx.y;
+  const int64_t mn = (int64_t)M * N;
+  const float *pb = part + bz * S * mn;
+  float *Cb = C + bz * sC;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < mn; e += (int64_t)gridDim.x * 256) {
+    float acc = 0.f;
+    for (int s = 0; s < S; ++s) acc += pb[s * mn + e];
+    const int64_t row = e / N, col = e - row * N;
+    float v = alpha * acc;
+    if (beta != 0.f) v += beta * Cb[row * ldc + col];
+    Cb[row * ldc + col] = v;
+  }
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+template <int MODE>
+hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) {
+  dim3 block(NTHREADS);
+  const int S = (MODE == MODE_GENERAL && d.splitk > 1 && d.part) ? d.splitk : 1;
+  dim3 grid(kp.ntiles, S, (unsigned)d.batch);
+#define SOAP_LAUNCH(TA, TB, VEC, TAG) \
+  hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE, TAG>), grid, block, 0, s, kp)
+  const int code = d.trans_a * 2 + d.trans_b;
+  if (MODE == MODE_GENERAL && d.tag != 0 && code == 2) {
+    // the power products (transposed-A layout) under their own symbols
+    if (d.tag == 1) { if (vec_ok) SOAP_LAUNCH(1, 0, 4, 1); else SOAP_LAUNCH(1, 0, 1, 1); }
+    else { if (vec_ok) SOAP_LAUNCH(1, 0, 4, 2); else SOAP_LAUNCH(1, 0, 1, 2); }
+  } else if (vec_ok) {
+    switch (code) {
+      case 0: SOAP_LAUNCH(0, 0, 4, 0); break;
+      case 1: SOAP_LAUNCH(0, 1, 4, 0); break;
+      case 2: SOAP_LAUNCH(1, 0, 4, 0); break;
+      default: SOAP_LAUNCH(1, 1, 4, 0); break;
+    }
+  } else {
+    switch (code) {
+      case 0: SOAP_LAUNCH(0, 0, 1, 0); break;
+      case 1: SOAP_LAUNCH(0, 1, 1, 0); break;
+      case 2: SOAP_LAUNCH(1, 0, 1, 0); break;
+      default: SOAP_LAUNCH(1, 1, 1, 0); break;
+    }
+  }
+#undef SOAP_LAUNCH
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess || S == 1) return err;
+  int64_t mn = d.M * d.N;
+  unsigned gx = (unsigned)std::min<int64_t>((mn + 255) / 256, 2048);
+  hipLaunchKernelGGL(splitk_reduce, dim3(gx, (unsigned)d.batch), dim3(256), 0, s, kp.part, S,
+                     kp.M, kp.N, d.C, d.ldc, d.sC, d.alpha, d.beta);
+  return hipGetLastError();
+}
+
+KParams make_params(const GemmDesc &d) {
+  KParams kp{};
+  kp.M = (int)d.M; kp.N = (int)d.N; kp.K = (int)d.K;
+  kp.A = d.A; kp.lda = d.lda; kp.sA = d.sA;
+  kp.A2 = nullptr;
+  kp.B = d.B; kp.ldb = d.ldb; kp.sB = d.sB;
+  kp.C = d.C; kp.ldc = d.ldc; kp.sC = d.sC;
+  kp.alpha = d.alpha; kp.beta = d.beta;
+  kp.tiles_m = (int)((d.M + BM - 1) / BM);
+  kp.tiles_n = (int)((d.N + BN - 1) / BN);
+  kp.ntiles = kp.tiles_m * kp.tiles_n;
+  kp.kslice = (int)d.K;
+  kp.part = nullptr;
+  if (d.splitk > 1 && d.part) {
+    const int64_t per = (d.K + d.splitk - 1) / d.splitk;
+    kp.kslice = (int)(((per + BK - 1) / BK) * BK);
+    kp.part = d.part;
+  }
+  return kp;
+}
+
+// 16-byte vector loads are used only on k-contiguous operands; they need the
+// k extent, the leading dimension, the batch stride and the base to be
+// multiples of 4 floats.
+bool vec_ok_for(const GemmDesc &d, const float *A2) {
+  bool ok = (d.K % 4 == 0);
+  if (d.trans_a == 0) ok = ok && d.lda % 4 == 0 && d.sA % 4 == 0 && aligned16(d.A) && (!A2 || aligned16(A2));
+  if (d.trans_b == 1) ok = ok && d.ldb % 4 == 0 && d.sB % 4 == 0 && aligned16(d.B);
+  return ok;
+}
+
+}  // namespace
+
+int choose_splitk(int64_t M, int64_t N, int64_t K, int64_t batch, int max_split) {
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN) * batch;
+  int64_t s = (512 + tiles - 1) / tiles;
+  const int64_t kcap = K / 512;     // keep at least 512 of K per slice
+  if (s > kcap) s = kcap;
+  if (s > max_split) s = max_split;
+  if (s < 1) s = 1;
+  return (int)s;
+}
+
+hipError_t launch_gemm(const GemmDesc &d, hipStream_t s) {
+  if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
+  KParams kp = make_params(d);
+  return dispatch<MODE_GENERAL>(d, kp, s, vec_ok_for(d, nullptr));
+}
+
+hipError_t launch_syrk_ema(const GemmDesc &d, hipStream_t s) {
+  if (d.M <= 0 || d.batch <= 0) return hipSuccess;
+  KParams kp = make_params(d);
+  kp.ntiles = kp.tiles_m * (kp.tiles_m + 1) / 2;
+  return dispatch<MODE_SYRK>(d, kp, s, vec_ok_for(d, nullptr));
+}
+
+hipError_t launch_gemm_adam(const GemmDesc &d, const AdamEpi &e, hipStream_t s) {
+  if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
+  KParams kp = make_params(d);
+  kp.A2 = e.A2;
+  kp.V = e.V;
+  kp.Nout = e.Nout;
+  kp.b2 = e.b2; kp.c1 = e.c1; kp.c2 = e.c2; kp.eps = e.eps;
+  return dispatch<MODE_ADAM>(d, kp, s, vec_ok_for(d, e.A2));
+}
+
+}  // namespace soap

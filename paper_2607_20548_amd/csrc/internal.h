@@ -1,0 +1,87 @@
+// Internal declarations shared by the host orchestration and the kernel files
+// of the SOAP library.  Nothing here is part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace soap {
+
+// ----------------------------------------------------------------- GEMM
+// op(A) is M x K, op(B) is K x N, C is M x N; all row-major.
+//   trans_a = 0: op(A)[i][k] = A[i*lda + k]      trans_a = 1: op(A)[i][k] = A[k*lda + i]
+//   trans_b = 0: op(B)[k][j] = B[k*ldb + j]      trans_b = 1: op(B)[k][j] = B[j*ldb + k]
+// A batch of independent products is laid out with element strides sA, sB, sC.
+struct GemmDesc {
+  int trans_a = 0, trans_b = 0;
+  int64_t M = 0, N = 0, K = 0;
+  const float *A = nullptr;
+  int64_t lda = 0, sA = 0;
+  const float *B = nullptr;
+  int64_t ldb = 0, sB = 0;
+  float *C = nullptr;
+  int64_t ldc = 0, sC = 0;
+  float alpha = 1.f, beta = 0.f;
+  int64_t batch = 1;
+  // Split-K: when splitk > 1 the K range is cut into `splitk` slices whose
+  // partial products go to `part` (batch * splitk * M * N floats) and are then
+  // summed in a fixed order by a second kernel.
+  int splitk = 1;
+  float *part = nullptr;
+  // Distinct kernel symbol for profiling (0 = shared GEMM; 1, 2 = the power
+  // products L Q_L and R Q_R), so that a trace can attribute time per stage.
+  int tag = 0;
+};
+
+// A split-K factor that gives at least ~2 workgroups per CU for a product with
+// the given tile count and K, capped by the partial buffer `max_split`.
+int choose_splitk(int64_t M, int64_t N, int64_t K, int64_t batch, int max_split);
+
+// C = alpha op(A) op(B) + beta C (C not read when beta == 0).
+hipError_t launch_gemm(const GemmDesc &d, hipStream_t s);
+
+// Symmetric rank-k EMA on one triangle:  C <- beta C + alpha op(A) op(B) where
+// op(B) = op(A)^T, only tiles on or below the diagonal are computed and each
+// result is stored at (i,j) and (j,i).  C is read from its lower triangle.
+hipError_t launch_syrk_ema(const GemmDesc &d, hipStream_t s);
+
+// Fused second rotation + Adam in the eigenbasis.  With op(A) = T_G and
+// op(A2) = T_M (same layout/strides), op(B) = Q_R:
+//   G' = T_G Q_R,  M' = T_M Q_R,  V <- b2 V + (1-b2) G'^2,
+//   Nout = (M'/c1) / (sqrt(V/c2) + eps).
+// V and Nout use the leading dimension / stride of C in the descriptor.
+struct AdamEpi {
+  const float *A2 = nullptr;
+  float *V = nullptr;
+  float *Nout = nullptr;
+  float b2 = 0.f, c1 = 1.f, c2 = 1.f, eps = 0.f;
+};
+hipError_t launch_gemm_adam(const GemmDesc &d, const AdamEpi &e, hipStream_t s);
+
+// ------------------------------------------------------- elementwise
+// M <- b1 M + (1-b1) G over `count` floats.
+hipError_t launch_momentum(float *M, const float *G, int64_t count, float b1, hipStream_t s);
+// Fill `batch` row-major r x c matrices (element stride sbatch between them)
+// with diag_value on the diagonal and 0 elsewhere.
+hipError_t launch_fill_diag(float *X, int64_t batch, int64_t r, int64_t c, int64_t sbatch,
+                            float diag_value, hipStream_t s);
+// Zero `count` 32-bit words.
+hipError_t launch_zero_u32(uint32_t *p, int64_t count, hipStream_t s);
+// Copy `count` floats.
+hipError_t launch_copy(float *dst, const float *src, int64_t count, hipStream_t s);
+
+// ----------------------------------------------------------------- QR
+// Blocked Householder QR of `batch` n x n matrices A, each given TRANSPOSED:
+// At = A^T row-major (element stride n*n between matrices).  At is overwritten
+// by the factorization; the Q factor with non-negative diag(R) is written
+// row-major to Q.  If Rf is non-null the triangular factor is written there
+// (row-major, strict lower part zero).
+size_t qr_workspace_bytes(int64_t batch, int64_t n);
+hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
+                                void *ws, size_t ws_bytes, hipStream_t s);
+// dst = src^T for one n x n row-major matrix.
+hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t s);
+
+}  // namespace soap

@@ -1,0 +1,703 @@
+// Blocked Householder QR with explicit Q, for the SOAP eigenbasis refresh
+// (the paper's Algorithm 2 takes QR(L_t Q_L).Q and QR(R_t Q_R).Q every step).
+//
+// Structure (two-level blocking):
+//  * Outer blocks of NB = 128 columns.  After an outer block is factored, its
+//    reflectors act on the trailing matrix through the compact-WY form
+//    H_1 ... H_nb = I - Y T Y^T:  A_trail -= Y (T^T (Y^T A_trail)), three fp32
+//    MFMA GEMMs (the first one split over K).
+//  * Inside an outer block, inner panels of width b in {16, 8, 4} are each
+//    factored by ONE 512-thread workgroup that holds the whole panel
+//    (rows ci..n-1, b columns) in registers; the column loop uses wave64
+//    butterfly reductions and two workgroup barriers per column.  b is chosen
+//    so that b * rows-per-thread <= 128 registers.
+//  * After each inner panel a row-split reduction forms Y_p^T over the outer
+//    block (the panel's Gram matrix for its T block, Y_prev^T Y_p for the T
+//    column, Y_p^T A_rest for the update); its last workgroup finishes the
+//    small triangular products, and a row-parallel apply updates the rest of
+//    the outer block.
+//  * Q is formed backwards, Q[c:, c:] -= Y (T (Y^T Q[c:, c:])), starting from I.
+//
+// Reflector convention (as in LAPACK's larfg): for x = A[j:, j] with
+// s = ||x[1:]||^2 and sigma = ||x||, v0 = x0 + sgn(x0) sigma (sgn(0) = +1),
+// v = x / v0 (so v[0] = 1), beta = 2 v0^2 / (s + v0^2), and H x = -sgn(x0) sigma e_1.
+// |v0| >= |x0| keeps every |v_i| <= 1 and beta in [1, 2], which keeps the
+// compact-WY products well scaled in fp32.  (The opposite choice, which makes
+// R's diagonal positive directly, produces Householder vectors of size
+// 1e4..1e5 on the near-identity matrices L Q of SOAP and loses about two
+// digits in the blocked form.)  s == 0 means the column is already
+// triangular: H = I.  The diagonal of R then has signs d_j; the unique Q with
+// non-negative diag(R) is Q_house diag(d), obtained by starting the backward
+// accumulation of Q from diag(d) instead of I.
+//
+// Storage: the matrix is factored in transposed form, At = A^T row-major (so
+// At[col * n + row] = A[row][col]).  A panel's columns are then contiguous
+// rows of At and every panel load and store is coalesced; the compact-WY
+// GEMMs take the transposition through their operand flags.  After factoring,
+// At holds R above the outer-block diagonal blocks (transposed) and, inside
+// every outer block, the explicit unit lower-trapezoidal Y (zeros above its
+// diagonal, ones on it), which the GEMMs read directly.
+#include "internal.h"
+
+#include <algorithm>
+
+namespace soap {
+namespace {
+
+constexpr int NB = 128;            // outer block width
+constexpr int PANEL_THREADS = 512;
+constexpr int PANEL_WAVES = PANEL_THREADS / 64;
+constexpr int RCH = 256;           // rows per workgroup in the inner reduction
+constexpr int RED_THREADS = 1024;  // threads of the inner reduction
+constexpr int APPLY_ROWS = 8;      // rows per workgroup in the inner apply
+constexpr int MAX_B = 32;
+constexpr int PART_STRIDE = MAX_B * NB;   // floats per partial block
+
+// --------------------------------------------------------------- reductions
+// Transposed butterfly over a wave64: NV values per lane (NV a power of two,
+// <= 64) are summed across the wave with NV - 1 + log2(64/NV) shuffles.  On
+// return lane l holds the wave total of value index l / (64 / NV).
+template <int NV>
+__device__ __forceinline__ float wave_reduce_transposed(float (&v)[NV], int lane) {
+#pragma unroll
+  for (int half = NV / 2, mask = 32; half >= 1; half >>= 1, mask >>= 1) {
+    const bool up = (lane & mask) != 0;
+#pragma unroll
+    for (int i = 0; i < half; ++i) {
+      const float keep = up ? v[i + half] : v[i];
+      const float send = up ? v[i] : v[i + half];
+      v[i] = keep + __shfl_xor(send, mask);
+    }
+  }
+  float x = v[0];
+#pragma unroll
+  for (int mask = 32 / NV; mask >= 1; mask >>= 1) x += __shfl_xor(x, mask);
+  return x;
+}
+
+// Sum of NV values over the panel workgroup; the NV totals are left in
+// tot (LDS) for every thread to read.  red: [PANEL_WAVES][NV] in LDS.
+template <int NV>
+__device__ __forceinline__ void block_allreduce(float (&v)[NV], float *red, float *tot) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int G = 64 / NV;
+  const float x = wave_reduce_transposed<NV>(v, lane);
+  if ((lane % G) == 0) red[wave * NV + lane / G] = x;
+  __syncthreads();
+  if (threadIdx.x < NV) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < PANEL_WAVES; ++w) s += red[w * NV + threadIdx.x];
+    tot[threadIdx.x] = s;
+  }
+  __syncthreads();
+}
+
+// Copies a rows x cols block (row strides sld, dld) from global memory to LDS
+// with NT threads, keeping 8 loads in flight per thread.
+template <int NT>
+__device__ __forceinline__ void stage_block(float *dst, int dld, const float *src, int sld,
+                                            int rows, int cols) {
+  const int total = rows * cols;
+  for (int base = threadIdx.x; base < total; base += 8 * NT) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = base + u * NT;
+      v[u] = (e < total) ? src[(e / cols) * sld + e % cols] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = base + u * NT;
+      if (e < total) dst[(e / cols) * dld + e % cols] = v[u];
+    }
+  }
+}
+
+struct PanelParams {
+  float *At;         // batch of transposed n x n matrices (At[col*n + row])
+  int64_t sA;
+  int n;
+  int c;             // first column of the outer block
+  int ci;            // first column of this panel
+  int beff;          // panel width actually used (<= B)
+  float *T;          // T of this outer block: NB x NB row-major, batch stride sT
+  int64_t sT;
+  float *Rf;         // optional triangular-factor output, row-major (batch stride sA)
+  float *dsign;      // sign of each R diagonal entry, n per matrix
+  float *beta;       // reflector coefficient of each column, n per matrix
+};
+
+// Factors A[ci:n, ci:ci+beff] in registers; writes Y back (zeros above the
+// diagonal inside the outer block, ones on it), the reflector coefficients,
+// the R-diagonal signs and, if requested, the R entries of these columns for
+// rows c .. ci+beff-1.  Thread t owns rows ci + t + PANEL_THREADS*s.  (The
+// panel's block of T is formed by the row-parallel reduction that follows.)
+template <int B, int RPT>
+__global__ __launch_bounds__(PANEL_THREADS) void qr_panel_kernel(PanelParams p) {
+  static_assert(B * RPT <= 128, "panel must fit in 128 registers per thread");
+  __shared__ float red[PANEL_WAVES * B];
+  __shared__ float tot[B];
+  __shared__ float piv[2][B];
+
+  const int64_t bz = blockIdx.x;
+  float *At = p.At + bz * p.sA;
+  float *Rf = p.Rf ? p.Rf + bz * p.sA : nullptr;
+  const int n = p.n, ci = p.ci, c = p.c, beff = p.beff;
+  const int N = n - ci;
+  const int t = threadIdx.x;
+  const unsigned un = (unsigned)n;   // n*n < 2^31: 32-bit offsets within a matrix
+
+  // R entries above this panel inside the outer block: rows c..ci-1.
+  for (int e = t; e < (ci - c) * beff; e += PANEL_THREADS) {
+    const int j = e / (ci - c), r = c + e % (ci - c);
+    const unsigned off = (unsigned)(ci + j) * un + r;
+    if (Rf) Rf[(unsigned)r * un + ci + j] = At[off];
+    At[off] = 0.f;
+  }
+
+  float a[RPT][B];
+#pragma unroll
+  for (int s = 0; s < RPT; ++s) {
+    const int lr = t + PANEL_THREADS * s;
+#pragma unroll
+    for (int j = 0; j < B; ++j)
+      a[s][j] = (lr < N && j < beff) ? At[(unsigned)(ci + j) * un + ci + lr] : 0.f;
+  }
+  // Column loop, fully unrolled: j is a compile-time index, so every register
+  // access is static and finished columns cost nothing.  The guard j < beff
+  // is uniform across the workgroup.
+#pragma unroll
+  for (int j = 0; j < B; ++j) {
+    if (j < beff) {
+      float *pv = piv[j & 1];
+      if (t == j) {
+#pragma unroll
+        for (int cc = 0; cc < B; ++cc)
+          if (cc >= j) pv[cc] = a[0][cc];
+      }
+      float v[B];
+#pragma unroll
+      for (int cc = 0; cc < B; ++cc) v[cc] = 0.f;
+#pragma unroll
+      for (int s = 0; s < RPT; ++s) {
+        const int lr = t + PANEL_THREADS * s;
+        float x = 0.f;
+#pragma unroll
+        for (int cc = 0; cc < B; ++cc)
+          if (cc == j) x = a[s][cc];
+        const float y = (lr > j && lr < N) ? x : 0.f;
+#pragma unroll
+        for (int cc = 0; cc < B; ++cc)
+          if (cc >= j) v[cc] += y * a[s][cc];
+      }
+      block_allreduce<B>(v, red, tot);
+      const float x0 = pv[j];
+      const float st = tot[j];
+      float beta, inv_v0, rjj;
+      if (st == 0.f) {          // already triangular: H = I
+        inv_v0 = 0.f;
+        beta = 0.f;
+        rjj = x0;
+      } else {
+        const float sigma = sqrtf(x0 * x0 + st);
+        const float v0 = (x0 >= 0.f) ? (x0 + sigma) : (x0 - sigma);
+        beta = 2.f * v0 * v0 / (st + v0 * v0);
+        inv_v0 = 1.f / v0;
+        rjj = (x0 >= 0.f) ? -sigma : sigma;
+      }
+      float f[B];   // beta * v^T a_cc for the columns right of j
+#pragma unroll
+      for (int cc = 0; cc < B; ++cc)
+        f[cc] = (cc > j) ? beta * (pv[cc] + tot[cc] * inv_v0) : 0.f;
+#pragma unroll
+      for (int s = 0; s < RPT; ++s) {
+        const int lr = t + PANEL_THREADS * s;
+        const bool live = (lr > j) && (lr < N);
+        float x = 0.f;
+#pragma unroll
+        for (int cc = 0; cc < B; ++cc)
+          if (cc == j) x = a[s][cc];
+        const float y = live ? x * inv_v0 : 0.f;   // Householder vector entry
+#pragma unroll
+        for (int cc = 0; cc < B; ++cc) {
+          if (cc > j) a[s][cc] -= f[cc] * y;
+          if (cc == j) a[s][cc] = live ? y : a[s][cc];
+        }
+      }
+      if (t == j) {
+#pragma unroll
+        for (int cc = 0; cc < B; ++cc) {
+          if (cc > j) a[0][cc] -= f[cc];
+          if (cc == j) a[0][cc] = rjj;
+        }
+      }
+      if (t == 0) {
+        p.beta[bz * n + ci + j] = beta;
+        p.dsign[bz * n + ci + j] = (rjj < 0.f) ? -1.f : 1.f;
+      }
+    }
+  }
+
+  // Write Y (explicit zeros above its diagonal, ones on it) and the R entries.
+#pragma unroll
+  for (int s = 0; s < RPT; ++s) {
+    const int lr = t + PANEL_THREADS * s;
+    if (lr >= N) continue;
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      if (j < beff) {
+        if (lr <= j && Rf) Rf[(unsigned)(ci + lr) * un + ci + j] = a[s][j];
+        At[(unsigned)(ci + j) * un + ci + lr] = (lr > j) ? a[s][j] : (lr == j ? 1.f : 0.f);
+      }
+    }
+  }
+}
+
+struct InnerParams {
+  float *At;
+  int64_t sA;
+  int n, c, ci, b, cend;
+  float *T;           // outer-block T, batch stride sT
+  int64_t sT;
+  const float *beta;  // reflector coefficients, n per matrix
+  float *Wi;          // b x w output (T_p^T Y_p^T A_rest), batch stride sW
+  int64_t sW;
+  float *part;        // partial products, batch stride sP (P * PART_STRIDE)
+  int64_t sP;
+  unsigned *cnt;      // one arrival counter per matrix (zero between uses)
+  int P;              // workgroups per matrix
+};
+
+constexpr int TS = RCH + 1;   // LDS column stride of the reduction tile (bank spread)
+
+// One workgroup per RCH rows computes O = Y_p^T [Y_prev | Y_p | A_rest] over
+// its rows (Y_p = this panel's reflectors, Y_prev = the earlier panels of the
+// outer block, A_rest = the outer block's columns right of the panel).  The
+// last workgroup to arrive (per matrix) sums the partials in workgroup order
+// and forms, from G = Y_p^T Y_p, X = Y_prev^T Y_p and W = Y_p^T A_rest:
+//   T_p (upper triangular):  T_p[j][j] = beta_j,
+//                            T_p[0:j, j] = -beta_j T_p[0:j, 0:j] G[0:j, j]
+//   the T column block:      T[0:off, off:off+b] = -T[0:off, 0:off] X T_p
+//   the update coefficients: Wi = T_p^T W.
+__global__ __launch_bounds__(RED_THREADS) void qr_inner_reduce_kernel(InnerParams p) {
+  // Column-major tile of the outer block's rows r0..r0+RCH-1.  Once the
+  // partials are written the last workgroup reuses it for the summed partials
+  // (Os: b x NB), the Z block (Zs: NB x MAX_B) and T (Ts: NB x NB).
+  __shared__ float tile[NB * TS];
+  __shared__ int last;
+  float *Os = tile;
+  float *Zs = tile + MAX_B * NB;
+  float *Ts = tile + 2 * MAX_B * NB;
+  const int64_t bz = blockIdx.y;
+  const int g = blockIdx.x;
+  const float *At = p.At + bz * p.sA;
+  const int n = p.n, c = p.c, ci = p.ci, b = p.b;
+  const int ncol = p.cend - c;
+  const int off = ci - c;
+  const int w = p.cend - (ci + b);
+  const int r0 = ci + g * RCH;
+  const int rows = min(RCH, n - r0);
+  const int t = threadIdx.x;
+
+  // tile load: thread -> (row, group of 32 columns); 32 coalesced loads in flight
+  {
+    const int rr = t & (RCH - 1), cg = t / RCH;    // 4 column groups
+    if (rr < rows) {
+      const float *src = At + (int64_t)(c + 32 * cg) * n + r0 + rr;
+      float v[32];
+#pragma unroll
+      for (int u = 0; u < 32; ++u) v[u] = (32 * cg + u < ncol) ? src[(int64_t)u * n] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 32; ++u)
+        if (32 * cg + u < ncol) tile[(32 * cg + u) * TS + rr] = v[u];
+    }
+  }
+  __syncthreads();
+
+  // thread -> (outer-block column q, one of 8 slices of the panel columns)
+  constexpr int JG = RED_THREADS / 128;
+  const int q = t & 127;
+  const int jg = t >> 7;
+  const int hb = (b + JG - 1) / JG;
+  float o[MAX_B / JG];
+#pragma unroll
+  for (int u = 0; u < MAX_B / JG; ++u) o[u] = 0.f;
+  if (q < ncol) {
+    const float *xc = tile + q * TS;
+    const float *yc = tile + (off + jg * hb) * TS;
+    for (int rr = 0; rr < rows; ++rr) {
+      const float x = xc[rr];
+#pragma unroll
+      for (int u = 0; u < MAX_B / JG; ++u)
+        if (u < hb && jg * hb + u < b) o[u] += yc[u * TS + rr] * x;
+    }
+  }
+  float *part = p.part + bz * p.sP + (int64_t)g * PART_STRIDE;
+  if (q < ncol) {
+#pragma unroll
+    for (int u = 0; u < MAX_B / JG; ++u) {
+      const int jj = jg * hb + u;
+      if (u < hb && jj < b) part[jj * NB + q] = o[u];
+    }
+  }
+  __threadfence();
+  __syncthreads();
+  if (t == 0) {
+    const unsigned prev = atomicAdd(p.cnt + bz, 1u);
+    last = (prev == (unsigned)(p.P - 1));
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+
+  float *T = p.T + bz * p.sT;
+  const float *beta = p.beta + bz * p.n + ci;
+  stage_block<RED_THREADS>(Ts, NB, T, NB, off, off);
+  const float *pb = p.part + bz * p.sP;
+  for (int e = t; e < b * ncol; e += RED_THREADS) {
+    const int jj = e / ncol, qq = e - jj * ncol;
+    const float *src = pb + jj * NB + qq;
+    float s[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) s[u] = 0.f;
+    for (int gg = 0; gg < p.P; gg += 16) {
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (gg + u < p.P) s[u] += src[(int64_t)(gg + u) * PART_STRIDE];
+    }
+    float tot16 = 0.f;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) tot16 += s[u];
+    Os[jj * NB + qq] = tot16;
+  }
+  __syncthreads();
+  // T_p, one column at a time (thread i < j computes T_p[i][j]); stored at
+  // Ts[off+i][off+j].  G[l][j] = Os[l][off + j].
+  for (int j = 0; j < b; ++j) {
+    if (t <= j) {
+      float val = beta[j];
+      if (t < j) {
+        float acc = 0.f;
+        for (int l = t; l < j; ++l) acc += Ts[(off + t) * NB + off + l] * Os[l * NB + off + j];
+        val = -beta[j] * acc;
+      }
+      Ts[(off + t) * NB + off + j] = val;
+    }
+    if (t > j && t < b) Ts[(off + t) * NB + off + j] = 0.f;
+    __syncthreads();
+  }
+  // rows off..off+b of T: zeros left of the diagonal block, then T_p
+  for (int e = t; e < b * (off + b); e += RED_THREADS) {
+    const int i = e / (off + b), jc = e % (off + b);
+    T[(off + i) * NB + jc] = (jc < off) ? 0.f : Ts[(off + i) * NB + jc];
+  }
+  // Wi[jj][q] = sum_{l <= jj} T_p[l][jj] * W[l][q],  W[l][q] = Os[l][off + b + q]
+  float *Wi = p.Wi + bz * p.sW;
+  for (int e = t; e < b * w; e += RED_THREADS) {
+    const int jj = e / w, qq = e - jj * w;
+    float s = 0.f;
+    for (int l = 0; l <= jj; ++l) s += Ts[(off + l) * NB + off + jj] * Os[l * NB + off + b + qq];
+    Wi[jj * w + qq] = s;
+  }
+  if (off > 0) {
+    // Z[i][jj] = sum_{l <= jj} X[i][l] T_p[l][jj],  X[i][l] = Os[l][i]
+    for (int e = t; e < off * b; e += RED_THREADS) {
+      const int i = e / b, jj = e - i * b;
+      float s = 0.f;
+      for (int l = 0; l <= jj; ++l) s += Os[l * NB + i] * Ts[(off + l) * NB + off + jj];
+      Zs[i * MAX_B + jj] = s;
+    }
+    __syncthreads();
+    // T[i][off + jj] = -sum_{l = i}^{off-1} T[i][l] Z[l][jj]
+    for (int e = t; e < off * b; e += RED_THREADS) {
+      const int i = e / b, jj = e - i * b;
+      float s = 0.f;
+      for (int l = i; l < off; ++l) s += Ts[i * NB + l] * Zs[l * MAX_B + jj];
+      T[i * NB + off + jj] = -s;
+    }
+  }
+  if (t == 0) p.cnt[bz] = 0u;
+}
+
+struct ApplyParams {
+  float *At;
+  int64_t sA;
+  int n, ci, b, w;
+  const float *Wi;
+  int64_t sW;
+};
+
+// A[r][ci+b+q] -= sum_l Y[r][l] Wi[l][q] for rows r >= ci; one thread per row
+// so that every access to At (column-major A) is coalesced.
+__global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
+  __shared__ float Ws[MAX_B * NB];
+  const int64_t bz = blockIdx.y;
+  float *At = p.At + bz * p.sA;
+  const float *Wi = p.Wi + bz * p.sW;
+  const int n = p.n, ci = p.ci, b = p.b, w = p.w;
+  const int t = threadIdx.x;
+  stage_block<256>(Ws, NB, Wi, w, b, w);
+  __syncthreads();
+  const int r = ci + blockIdx.x * 256 + t;
+  if (r >= n) return;
+  float y[MAX_B];
+#pragma unroll
+  for (int l = 0; l < MAX_B; ++l) y[l] = (l < b) ? At[(int64_t)(ci + l) * n + r] : 0.f;
+  float *dst = At + (int64_t)(ci + b) * n + r;
+  int q = 0;
+  for (; q + 8 <= w; q += 8) {
+    float cur[8], s[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) { cur[u] = dst[(int64_t)(q + u) * n]; s[u] = 0.f; }
+#pragma unroll
+    for (int l = 0; l < MAX_B; ++l)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s[u] += y[l] * Ws[l * NB + q + u];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) dst[(int64_t)(q + u) * n] = cur[u] - s[u];
+  }
+  for (; q < w; ++q) {
+    float s = 0.f;
+#pragma unroll
+    for (int l = 0; l < MAX_B; ++l) s += y[l] * Ws[l * NB + q];
+    dst[(int64_t)q * n] -= s;
+  }
+}
+
+// Final triangular factor: entries of an earlier outer block than their column
+// come from At, entries inside an outer block were stored by the panels; every
+// row i is then scaled by d_i so that diag(R) >= 0.  Strict lower part = 0.
+__global__ __launch_bounds__(256) void qr_extract_r_kernel(const float *At, float *Rf,
+                                                           const float *dsign, int n,
+                                                           int64_t sA) {
+  const int64_t bz = blockIdx.y;
+  const float *Ab = At + bz * sA;
+  float *Rb = Rf + bz * sA;
+  const float *d = dsign + bz * n;
+  const int64_t nn = (int64_t)n * n;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += (int64_t)gridDim.x * 256) {
+    const int i = (int)(e / n), j = (int)(e % n);
+    if (i > j) Rb[e] = 0.f;
+    else Rb[e] = d[i] * ((i / NB < j / NB) ? Ab[(int64_t)j * n + i] : Rb[e]);
+  }
+}
+
+// Q <- diag(d) for each matrix of the batch.
+__global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *dsign, int n,
+                                                        int64_t sA) {
+  const int64_t bz = blockIdx.y;
+  float *Qb = Q + bz * sA;
+  const float *d = dsign + bz * n;
+  const int64_t nn = (int64_t)n * n;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += (int64_t)gridDim.x * 256) {
+    const int i = (int)(e / n), j = (int)(e % n);
+    Qb[e] = (i == j) ? d[i] : 0.f;
+  }
+}
+
+// dst = src^T for one n x n matrix, through 32 x 32 LDS tiles.
+__global__ __launch_bounds__(256) void transpose_kernel(float *dst, const float *src, int n) {
+  __shared__ float tile[32][33];
+  const int bx = blockIdx.x * 32, by = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  for (int k = ty; k < 32; k += 8) {
+    const int r = by + k, cc = bx + tx;
+    if (r < n && cc < n) tile[k][tx] = src[(int64_t)r * n + cc];
+  }
+  __syncthreads();
+  for (int k = ty; k < 32; k += 8) {
+    const int r = bx + k, cc = by + tx;
+    if (r < n && cc < n) dst[(int64_t)r * n + cc] = tile[tx][k];
+  }
+}
+
+// ------------------------------------------------------------ host driver
+struct QrLayout {
+  int64_t n, nob;
+  size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, total;
+  int64_t sT, sWbuf, sSk, sPart, sWi;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+constexpr int MAX_SPLIT = 8;
+
+QrLayout qr_layout(int64_t batch, int64_t n) {
+  QrLayout L{};
+  L.n = n;
+  L.nob = (n + NB - 1) / NB;
+  const int64_t P = (n + RCH - 1) / RCH;
+  L.sT = L.nob * NB * NB;
+  L.sWbuf = (int64_t)NB * n;
+  L.sSk = (int64_t)MAX_SPLIT * NB * n;
+  L.sPart = P * PART_STRIDE;
+  L.sWi = (int64_t)MAX_B * NB;
+  size_t o = 0;
+  L.t_off = o;    o = align256(o + sizeof(float) * batch * L.sT);
+  L.w_off = o;    o = align256(o + sizeof(float) * batch * L.sWbuf);
+  L.w2_off = o;   o = align256(o + sizeof(float) * batch * L.sWbuf);
+  L.sk_off = o;   o = align256(o + sizeof(float) * batch * L.sSk);
+  L.part_off = o; o = align256(o + sizeof(float) * batch * L.sPart);
+  L.wi_off = o;   o = align256(o + sizeof(float) * batch * L.sWi);
+  L.d_off = o;    o = align256(o + sizeof(float) * batch * n);
+  L.b_off = o;    o = align256(o + sizeof(float) * batch * n);
+  L.cnt_off = o;  o = align256(o + sizeof(unsigned) * batch);
+  L.total = o;
+  return L;
+}
+
+template <int B, int RPT>
+hipError_t launch_panel(const PanelParams &pp, int64_t batch, hipStream_t s) {
+  hipLaunchKernelGGL((qr_panel_kernel<B, RPT>), dim3((unsigned)batch), dim3(PANEL_THREADS), 0, s,
+                     pp);
+  return hipGetLastError();
+}
+
+// Panel width for `rows` remaining rows: the widest b with b * ceil(rows/512) <= 128.
+int panel_width(int64_t rows) {
+  if (rows <= 4096) return 16;
+  if (rows <= 8192) return 8;
+  return 4;
+}
+
+}  // namespace
+
+size_t qr_workspace_bytes(int64_t batch, int64_t n) { return qr_layout(batch, n).total; }
+
+hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t s) {
+  const unsigned g = (unsigned)((n + 31) / 32);
+  hipLaunchKernelGGL(transpose_kernel, dim3(g, g), dim3(256), 0, s, dst, src, (int)n);
+  return hipGetLastError();
+}
+
+#define SOAP_TRY(x)                         \
+  do {                                      \
+    hipError_t e_ = (x);                    \
+    if (e_ != hipSuccess) return e_;        \
+  } while (0)
+
+hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
+                                void *ws, size_t ws_bytes, hipStream_t s) {
+  const QrLayout L = qr_layout(batch, n);
+  if (ws_bytes < L.total) return hipErrorInvalidValue;
+  char *base = static_cast<char *>(ws);
+  float *Tb = reinterpret_cast<float *>(base + L.t_off);
+  float *Wb = reinterpret_cast<float *>(base + L.w_off);
+  float *W2 = reinterpret_cast<float *>(base + L.w2_off);
+  float *Sk = reinterpret_cast<float *>(base + L.sk_off);
+  float *Pt = reinterpret_cast<float *>(base + L.part_off);
+  float *Wi = reinterpret_cast<float *>(base + L.wi_off);
+  float *dsign = reinterpret_cast<float *>(base + L.d_off);
+  float *betas = reinterpret_cast<float *>(base + L.b_off);
+  unsigned *cnt = reinterpret_cast<unsigned *>(base + L.cnt_off);
+  const int64_t sA = n * n;
+  const int ni = (int)n;
+
+  SOAP_TRY(launch_zero_u32(cnt, batch, s));
+
+  for (int64_t ob = 0; ob < L.nob; ++ob) {
+    const int c = (int)(ob * NB);
+    const int cend = (int)std::min<int64_t>(n, c + NB);
+    float *Tob = Tb + ob * NB * NB;
+    for (int ci = c; ci < cend;) {
+      const int64_t rows = n - ci;
+      const int B = panel_width(rows);
+      const int beff = std::min(B, cend - ci);
+      PanelParams pp{At, sA, ni, c, ci, beff, Tob, L.sT, Rf, dsign, betas};
+      switch (B) {
+        case 16: SOAP_TRY((launch_panel<16, 8>(pp, batch, s))); break;
+        case 8: SOAP_TRY((launch_panel<8, 16>(pp, batch, s))); break;
+        default: SOAP_TRY((launch_panel<4, 32>(pp, batch, s))); break;
+      }
+      const int w = cend - (ci + beff);
+      {
+        const int P = (int)((rows + RCH - 1) / RCH);
+        InnerParams ip{At, sA, ni, c, ci, beff, cend, Tob, L.sT, betas, Wi, L.sWi, Pt, L.sPart,
+                       cnt, P};
+        hipLaunchKernelGGL(qr_inner_reduce_kernel, dim3(P, (unsigned)batch), dim3(RED_THREADS), 0,
+                           s, ip);
+        SOAP_TRY(hipGetLastError());
+      }
+      if (w > 0) {
+        ApplyParams ap{At, sA, ni, ci, beff, w, Wi, L.sWi};
+        const unsigned gx = (unsigned)((rows + 255) / 256);
+        hipLaunchKernelGGL(qr_inner_apply_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, ap);
+        SOAP_TRY(hipGetLastError());
+      }
+      ci += beff;
+    }
+    if (cend < n) {
+      const int64_t nb = cend - c, Nt = n - cend, Kr = n - c;
+      // W = Y^T A[c:n, cend:n]:  W[i][j] = sum_k At[c+i][c+k] At[cend+j][c+k]
+      GemmDesc g1;
+      g1.trans_a = 0; g1.trans_b = 1; g1.M = nb; g1.N = Nt; g1.K = Kr;
+      g1.A = At + (int64_t)c * n + c; g1.lda = n; g1.sA = sA;
+      g1.B = At + (int64_t)cend * n + c; g1.ldb = n; g1.sB = sA;
+      g1.C = Wb; g1.ldc = Nt; g1.sC = L.sWbuf; g1.batch = batch;
+      g1.splitk = choose_splitk(nb, Nt, Kr, batch, MAX_SPLIT);
+      g1.part = Sk;
+      SOAP_TRY(launch_gemm(g1, s));
+      // W2 = T^T W
+      GemmDesc g2;
+      g2.trans_a = 1; g2.trans_b = 0; g2.M = nb; g2.N = Nt; g2.K = nb;
+      g2.A = Tob; g2.lda = NB; g2.sA = L.sT;
+      g2.B = Wb; g2.ldb = Nt; g2.sB = L.sWbuf;
+      g2.C = W2; g2.ldc = Nt; g2.sC = L.sWbuf; g2.batch = batch;
+      SOAP_TRY(launch_gemm(g2, s));
+      // A[c:n, cend:n] -= Y W2, i.e.  At[cend+j][c+k] -= sum_i W2[i][j] Y[k][i]
+      GemmDesc g3;
+      g3.trans_a = 1; g3.trans_b = 0; g3.M = Nt; g3.N = Kr; g3.K = nb;
+      g3.A = W2; g3.lda = Nt; g3.sA = L.sWbuf;
+      g3.B = At + (int64_t)c * n + c; g3.ldb = n; g3.sB = sA;
+      g3.C = At + (int64_t)cend * n + c; g3.ldc = n; g3.sC = sA;
+      g3.alpha = -1.f; g3.beta = 1.f; g3.batch = batch;
+      SOAP_TRY(launch_gemm(g3, s));
+    }
+  }
+
+  // Explicit Q (row-major), accumulated backwards from diag(d).
+  {
+    const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
+    hipLaunchKernelGGL(qr_init_q_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, Q, dsign,
+                       ni, sA);
+    SOAP_TRY(hipGetLastError());
+  }
+  for (int64_t ob = L.nob - 1; ob >= 0; --ob) {
+    const int c = (int)(ob * NB);
+    const int64_t nb = std::min<int64_t>(n, c + NB) - c, Kr = n - c;
+    float *Tob = Tb + ob * NB * NB;
+    GemmDesc g1;  // W = Y^T Q[c:n, c:n]:  op(A)[i][k] = Y[k][i] = At[c+i][c+k]
+    g1.trans_a = 0; g1.trans_b = 0; g1.M = nb; g1.N = Kr; g1.K = Kr;
+    g1.A = At + (int64_t)c * n + c; g1.lda = n; g1.sA = sA;
+    g1.B = Q + (int64_t)c * n + c; g1.ldb = n; g1.sB = sA;
+    g1.C = Wb; g1.ldc = Kr; g1.sC = L.sWbuf; g1.batch = batch;
+    g1.splitk = choose_splitk(nb, Kr, Kr, batch, MAX_SPLIT);
+    g1.part = Sk;
+    SOAP_TRY(launch_gemm(g1, s));
+    GemmDesc g2;  // W2 = T W
+    g2.trans_a = 0; g2.trans_b = 0; g2.M = nb; g2.N = Kr; g2.K = nb;
+    g2.A = Tob; g2.lda = NB; g2.sA = L.sT;
+    g2.B = Wb; g2.ldb = Kr; g2.sB = L.sWbuf;
+    g2.C = W2; g2.ldc = Kr; g2.sC = L.sWbuf; g2.batch = batch;
+    SOAP_TRY(launch_gemm(g2, s));
+    GemmDesc g3;  // Q[c:n, c:n] -= Y W2:  op(A)[k][i] = Y[k][i] = At[c+i][c+k]
+    g3.trans_a = 1; g3.trans_b = 0; g3.M = Kr; g3.N = Kr; g3.K = nb;
+    g3.A = At + (int64_t)c * n + c; g3.lda = n; g3.sA = sA;
+    g3.B = W2; g3.ldb = Kr; g3.sB = L.sWbuf;
+    g3.C = Q + (int64_t)c * n + c; g3.ldc = n; g3.sC = sA;
+    g3.alpha = -1.f; g3.beta = 1.f; g3.batch = batch;
+    SOAP_TRY(launch_gemm(g3, s));
+  }
+
+  if (Rf) {
+    const int64_t nn = n * n;
+    const unsigned gx = (unsigned)std::min<int64_t>((nn + 255) / 256, 2048);
+    hipLaunchKernelGGL(qr_extract_r_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, At, Rf,
+                       dsign, ni, sA);
+    SOAP_TRY(hipGetLastError());
+  }
+  return hipSuccess;
+}
+
+}  // namespace soap

@@ -1,0 +1,464 @@
+// Host side of the SOAP C ABI: argument validation, workspace carving, the
+// ordered sequence of kernel launches for one step, stage timing and the
+// thread-local error string.  Everything is enqueued on the caller's stream;
+// nothing here allocates device memory.
+#include "soap.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+int fail(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return SOAP_OK;
+}
+
+int hip_fail(hipError_t e, const char *where) {
+  return fail(SOAP_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool dim_ok(int64_t d) { return d >= 1 && d <= SOAP_MAX_DIM; }
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// ---------------------------------------------------------------- timing
+enum Stage {
+  ST_MOMENTUM = 0,
+  ST_FACTOR_L,
+  ST_FACTOR_R,
+  ST_POWER_L,
+  ST_POWER_R,
+  ST_QR_L,
+  ST_QR_R,
+  ST_ROT_IN_L,
+  ST_ROT_IN_R_ADAM,
+  ST_ROT_OUT_L,
+  ST_ROT_OUT_R_UPDATE,
+  ST_COUNT
+};
+
+const char *kStageNames[ST_COUNT] = {
+    "momentum_ema",     "factor_ema_L",    "factor_ema_R",  "power_L",
+    "power_R",          "qr_L",            "qr_R",          "rotate_in_QLt",
+    "rotate_in_QR_adam", "rotate_out_QL",  "rotate_out_QRt_update"};
+
+struct Pending {
+  int stage;
+  hipEvent_t a, b;
+  double flops;
+};
+
+struct Timing {
+  std::mutex mu;
+  bool enabled = false;
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> free_events;
+  double ms[ST_COUNT] = {};
+  int64_t launches[ST_COUNT] = {};
+  double flops[ST_COUNT] = {};
+};
+
+Timing &timing() {
+  static Timing t;
+  return t;
+}
+
+hipEvent_t take_event(Timing &t) {
+  if (!t.free_events.empty()) {
+    hipEvent_t e = t.free_events.back();
+    t.free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Records a pair of events around one stage when timing is enabled.
+class StageScope {
+ public:
+  StageScope(int stage, double flops, hipStream_t s) : stage_(stage), flops_(flops), s_(s) {
+    Timing &t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    if (!t.enabled) return;
+    a_ = take_event(t);
+    b_ = take_event(t);
+    if (a_ && b_ && hipEventRecord(a_, s_) == hipSuccess) active_ = true;
+  }
+  ~StageScope() {
+    if (!active_) return;
+    Timing &t = timing();
+    std::lock_guard<std::mutex> g(t.mu);
+    if (hipEventRecord(b_, s_) == hipSuccess) t.pending.push_back({stage_, a_, b_, flops_});
+  }
+
+ private:
+  int stage_;
+  double flops_;
+  hipStream_t s_;
+  hipEvent_t a_ = nullptr, b_ = nullptr;
+  bool active_ = false;
+};
+
+// ------------------------------------------------------------- workspace
+struct StepLayout {
+  size_t al, ar, tg, tm, nb, qr, total;
+};
+
+StepLayout step_layout(int64_t batch, int64_t m, int64_t n) {
+  StepLayout L{};
+  const size_t f = sizeof(float);
+  size_t o = 0;
+  L.al = o; o = align256(o + f * batch * m * m);
+  L.ar = o; o = align256(o + f * batch * n * n);
+  L.tg = o; o = align256(o + f * batch * m * n);
+  L.tm = o; o = align256(o + f * batch * m * n);
+  L.nb = o; o = align256(o + f * batch * m * n);
+  L.qr = o; o = align256(o + soap::qr_workspace_bytes(batch, std::max(m, n)));
+  L.total = o;
+  return L;
+}
+
+struct Range {
+  const void *p;
+  size_t bytes;
+  const char *name;
+};
+
+bool overlap(const Range &x, const Range &y) {
+  const char *a = static_cast<const char *>(x.p), *b = static_cast<const char *>(y.p);
+  return a < b + y.bytes && b < a + x.bytes;
+}
+
+int check_hparams(float beta1, float beta2, float eps, float lr, float wd, int64_t step,
+                  uint32_t flags) {
+  if (!std::isfinite(beta1) || beta1 < 0.f || beta1 >= 1.f)
+    return fail(SOAP_ERR_HPARAM, "beta1 = %g is outside [0, 1)", (double)beta1);
+  if (!std::isfinite(beta2) || beta2 < 0.f || beta2 >= 1.f)
+    return fail(SOAP_ERR_HPARAM, "beta2 = %g is outside [0, 1)", (double)beta2);
+  if (!std::isfinite(eps) || eps < 0.f)
+    return fail(SOAP_ERR_HPARAM, "eps = %g must be finite and >= 0", (double)eps);
+  if (!std::isfinite(lr) || lr < 0.f)
+    return fail(SOAP_ERR_HPARAM, "lr = %g must be finite and >= 0", (double)lr);
+  if (!std::isfinite(wd) || wd < 0.f)
+    return fail(SOAP_ERR_HPARAM, "weight_decay = %g must be finite and >= 0", (double)wd);
+  if (step < 1) return fail(SOAP_ERR_HPARAM, "step = %lld must be >= 1", (long long)step);
+  if (flags & ~uint32_t(SOAP_FLAG_NO_BIAS_CORRECTION))
+    return fail(SOAP_ERR_HPARAM, "unknown flag bits 0x%x", flags);
+  return SOAP_OK;
+}
+
+int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R, float *QL,
+              float *QR, float *M, float *V, int64_t m, int64_t n, float beta1, float beta2,
+              float eps, float lr, float wd, int64_t step, uint32_t flags, void *ws,
+              size_t ws_bytes, hipStream_t s) {
+  if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n))
+    return fail(SOAP_ERR_SHAPE, "batch=%lld m=%lld n=%lld: each must be in [1, %d]",
+                (long long)batch, (long long)m, (long long)n, SOAP_MAX_DIM);
+  const Range bufs[] = {
+      {param, sizeof(float) * batch * m * n, "param"}, {grad, sizeof(float) * batch * m * n, "grad"},
+      {L, sizeof(float) * batch * m * m, "L"},         {R, sizeof(float) * batch * n * n, "R"},
+      {QL, sizeof(float) * batch * m * m, "Q_L"},      {QR, sizeof(float) * batch * n * n, "Q_R"},
+      {M, sizeof(float) * batch * m * n, "M"},         {V, sizeof(float) * batch * m * n, "V"},
+      {ws, ws_bytes, "workspace"}};
+  for (const Range &b : bufs)
+    if (!b.p) return fail(SOAP_ERR_NULL, "%s is NULL", b.name);
+  int rc = check_hparams(beta1, beta2, eps, lr, wd, step, flags);
+  if (rc != SOAP_OK) return rc;
+  const StepLayout lay = step_layout(batch, m, n);
+  if (ws_bytes < lay.total)
+    return fail(SOAP_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
+  for (const Range &b : bufs)
+    if (!aligned16(b.p)) return fail(SOAP_ERR_ALIGN, "%s is not 16-byte aligned", b.name);
+  const int nb = sizeof(bufs) / sizeof(bufs[0]);
+  for (int i = 0; i < nb; ++i)
+    for (int j = i + 1; j < nb; ++j)
+      if (overlap(bufs[i], bufs[j]))
+        return fail(SOAP_ERR_ALIAS, "%s overlaps %s", bufs[i].name, bufs[j].name);
+
+  const bool bc = !(flags & SOAP_FLAG_NO_BIAS_CORRECTION);
+  const float c1 = bc ? (float)(1.0 - std::pow((double)beta1, (double)step)) : 1.f;
+  const float c2 = bc ? (float)(1.0 - std::pow((double)beta2, (double)step)) : 1.f;
+
+  char *w = static_cast<char *>(ws);
+  float *AL = reinterpret_cast<float *>(w + lay.al);
+  float *AR = reinterpret_cast<float *>(w + lay.ar);
+  float *TG = reinterpret_cast<float *>(w + lay.tg);
+  float *TM = reinterpret_cast<float *>(w + lay.tm);
+  float *NN = reinterpret_cast<float *>(w + lay.nb);
+  void *qws = w + lay.qr;
+  const size_t qws_bytes = ws_bytes - lay.qr;
+  const int64_t mn = m * n, mm = m * m, nn = n * n;
+  const double B = (double)batch, md = (double)m, nd = (double)n;
+  hipError_t e;
+
+  {  // M <- b1 M + (1-b1) G (weight space)
+    StageScope sc(ST_MOMENTUM, 0.0, s);
+    if ((e = soap::launch_momentum(M, grad, batch * mn, beta1, s)) != hipSuccess)
+      return hip_fail(e, "momentum");
+  }
+  {  // L <- b2 L + (1-b2) G G^T
+    StageScope sc(ST_FACTOR_L, B * md * (md + 1) * nd, s);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
+    d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
+    d.C = L; d.ldc = m; d.sC = mm; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
+    if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return hip_fail(e, "factor EMA L");
+  }
+  {  // R <- b2 R + (1-b2) G^T G
+    StageScope sc(ST_FACTOR_R, B * nd * (nd + 1) * md, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
+    d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
+    d.C = R; d.ldc = n; d.sC = nn; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
+    if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return hip_fail(e, "factor EMA R");
+  }
+  // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L since
+  // L is symmetric (both triangles are stored).
+  {  // A_L^T = Q_L^T L
+    StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0;
+    d.M = m; d.N = m; d.K = m; d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
+    d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power L");
+  }
+  {  // A_R^T = Q_R^T R
+    StageScope sc(ST_POWER_R, B * 2.0 * nd * nd * nd, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0;
+    d.M = n; d.N = n; d.K = n; d.A = QR; d.lda = n; d.sA = nn; d.B = R; d.ldb = n; d.sB = nn;
+    d.C = AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power R");
+  }
+  {  // Q_L = QR(A_L).Q
+    StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, s);
+    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws, qws_bytes, s)) != hipSuccess)
+      return hip_fail(e, "QR L");
+  }
+  {  // Q_R = QR(A_R).Q
+    StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
+    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws, qws_bytes, s)) != hipSuccess)
+      return hip_fail(e, "QR R");
+  }
+  {  // T_G = Q_L^T G,  T_M = Q_L^T M
+    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
+    d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in G");
+    d.B = M; d.C = TM;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in M");
+  }
+  {  // G' = T_G Q_R, M' = T_M Q_R, then Adam in the eigenbasis
+    StageScope sc(ST_ROT_IN_R_ADAM, B * 4.0 * md * nd * nd, s);
+    soap::GemmDesc d;
+    d.M = m; d.N = n; d.K = n; d.A = TG; d.lda = n; d.sA = mn; d.B = QR; d.ldb = n; d.sB = nn;
+    d.C = nullptr; d.ldc = n; d.sC = mn; d.batch = batch;
+    soap::AdamEpi ae;
+    ae.A2 = TM; ae.V = V; ae.Nout = NN; ae.b2 = beta2; ae.c1 = c1; ae.c2 = c2; ae.eps = eps;
+    if ((e = soap::launch_gemm_adam(d, ae, s)) != hipSuccess) return hip_fail(e, "rotate in + Adam");
+  }
+  {  // T2 = Q_L N (into T_G, which is dead now)
+    StageScope sc(ST_ROT_OUT_L, B * 2.0 * md * md * nd, s);
+    soap::GemmDesc d;
+    d.M = m; d.N = n; d.K = m; d.A = QL; d.lda = m; d.sA = mm; d.B = NN; d.ldb = n; d.sB = mn;
+    d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate out L");
+  }
+  {  // W <- (1 - lr wd) W - lr T2 Q_R^T
+    StageScope sc(ST_ROT_OUT_R_UPDATE, B * 2.0 * md * nd * nd, s);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = n; d.K = n;
+    d.A = TG; d.lda = n; d.sA = mn; d.B = QR; d.ldb = n; d.sB = nn;
+    d.C = param; d.ldc = n; d.sC = mn; d.alpha = -lr; d.beta = 1.f - lr * wd; d.batch = batch;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate out R + update");
+  }
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t soap_workspace_bytes(int64_t batch, int64_t m, int64_t n) {
+  if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n)) return 0;
+  return step_layout(batch, m, n).total;
+}
+
+int soap_init_state(int64_t batch, int64_t m, int64_t n, float *L, float *R, float *Q_L,
+                    float *Q_R, float *M, float *V, hipStream_t stream) {
+  if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n))
+    return fail(SOAP_ERR_SHAPE, "batch=%lld m=%lld n=%lld: each must be in [1, %d]",
+                (long long)batch, (long long)m, (long long)n, SOAP_MAX_DIM);
+  struct T { float *p; int64_t r, c; float d; const char *name; } ts[] = {
+      {L, m, m, 1.f, "L"}, {R, n, n, 1.f, "R"}, {Q_L, m, m, 1.f, "Q_L"},
+      {Q_R, n, n, 1.f, "Q_R"}, {M, m, n, 0.f, "M"}, {V, m, n, 0.f, "V"}};
+  for (const T &t : ts)
+    if (t.p && !aligned16(t.p)) return fail(SOAP_ERR_ALIGN, "%s is not 16-byte aligned", t.name);
+  for (const T &t : ts) {
+    if (!t.p) continue;
+    hipError_t e = soap::launch_fill_diag(t.p, batch, t.r, t.c, t.r * t.c, t.d, stream);
+    if (e != hipSuccess) return hip_fail(e, "init state");
+  }
+  return ok();
+}
+
+int soap_step(float *param, const float *grad, float *L, float *R, float *Q_L, float *Q_R,
+              float *M, float *V, int64_t m, int64_t n, float beta1, float beta2, float eps,
+              float lr, float weight_decay, int64_t step, uint32_t flags, void *workspace,
+              size_t workspace_bytes, hipStream_t stream) {
+  return step_impl(1, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
+                   weight_decay, step, flags, workspace, workspace_bytes, stream);
+}
+
+int soap_step_batched(int64_t batch, float *param, const float *grad, float *L, float *R,
+                      float *Q_L, float *Q_R, float *M, float *V, int64_t m, int64_t n,
+                      float beta1, float beta2, float eps, float lr, float weight_decay,
+                      int64_t step, uint32_t flags, void *workspace, size_t workspace_bytes,
+                      hipStream_t stream) {
+  return step_impl(batch, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
+                   weight_decay, step, flags, workspace, workspace_bytes, stream);
+}
+
+const char *soap_last_error(void) { return g_err; }
+
+size_t soap_qr_workspace_bytes(int64_t n) {
+  if (!dim_ok(n)) return 0;
+  return align256(sizeof(float) * n * n) + soap::qr_workspace_bytes(1, n);
+}
+
+int soap_qr_f32(int64_t n, const float *A, float *Q, float *Rf, void *workspace,
+                size_t workspace_bytes, hipStream_t stream) {
+  if (!dim_ok(n)) return fail(SOAP_ERR_SHAPE, "n=%lld must be in [1, %d]", (long long)n, SOAP_MAX_DIM);
+  if (!A || !Q || !workspace) return fail(SOAP_ERR_NULL, "A, Q and workspace must be non-NULL");
+  const size_t need = soap_qr_workspace_bytes(n);
+  if (workspace_bytes < need)
+    return fail(SOAP_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, need);
+  if (!aligned16(A) || !aligned16(Q) || (Rf && !aligned16(Rf)) || !aligned16(workspace))
+    return fail(SOAP_ERR_ALIGN, "pointers must be 16-byte aligned");
+  const Range rs[] = {{A, sizeof(float) * n * n, "A"}, {Q, sizeof(float) * n * n, "Q"},
+                      {Rf ? Rf : Q, Rf ? sizeof(float) * n * n : 0, "Rf"},
+                      {workspace, workspace_bytes, "workspace"}};
+  for (int i = 0; i < 4; ++i)
+    for (int j = i + 1; j < 4; ++j)
+      if (rs[i].bytes && rs[j].bytes && overlap(rs[i], rs[j]))
+        return fail(SOAP_ERR_ALIAS, "%s overlaps %s", rs[i].name, rs[j].name);
+  float *Aw = static_cast<float *>(workspace);
+  char *rest = static_cast<char *>(workspace) + align256(sizeof(float) * n * n);
+  hipError_t e = soap::launch_transpose(Aw, A, n, stream);   // the QR factors A^T
+  if (e == hipSuccess)
+    e = soap::qr_factor_and_form_q(Aw, Q, Rf, 1, n, rest, workspace_bytes - align256(sizeof(float) * n * n),
+                                   stream);
+  if (e != hipSuccess) return hip_fail(e, "QR");
+  return ok();
+}
+
+int soap_gemm_f32(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, float alpha,
+                  const float *A, int64_t lda, const float *B, int64_t ldb, float beta, float *C,
+                  int64_t ldc, hipStream_t stream) {
+  if (M < 1 || N < 1 || K < 0 || M > (1 << 24) || N > (1 << 24) || K > (1 << 24))
+    return fail(SOAP_ERR_SHAPE, "bad GEMM shape M=%lld N=%lld K=%lld", (long long)M,
+                (long long)N, (long long)K);
+  if (!A || !B || !C) return fail(SOAP_ERR_NULL, "A, B and C must be non-NULL");
+  const int64_t ra = trans_a ? K : M, ca = trans_a ? M : K;
+  const int64_t rb = trans_b ? N : K, cb = trans_b ? K : N;
+  if (lda < std::max<int64_t>(1, ca) || ldb < std::max<int64_t>(1, cb) || ldc < N)
+    return fail(SOAP_ERR_SHAPE, "leading dimension too small");
+  (void)ra; (void)rb;
+  soap::GemmDesc d;
+  d.trans_a = trans_a ? 1 : 0; d.trans_b = trans_b ? 1 : 0;
+  d.M = M; d.N = N; d.K = K; d.A = A; d.lda = lda; d.B = B; d.ldb = ldb;
+  d.C = C; d.ldc = ldc; d.alpha = alpha; d.beta = beta;
+  hipError_t e = soap::launch_gemm(d, stream);
+  if (e != hipSuccess) return hip_fail(e, "GEMM");
+  return ok();
+}
+
+int soap_factor_ema_f32(int trans, int64_t m, int64_t n, const float *G, float *F, float beta,
+                        hipStream_t stream) {
+  if (!dim_ok(m) || !dim_ok(n)) return fail(SOAP_ERR_SHAPE, "bad shape m=%lld n=%lld", (long long)m, (long long)n);
+  if (!G || !F) return fail(SOAP_ERR_NULL, "G and F must be non-NULL");
+  if (!std::isfinite(beta) || beta < 0.f || beta >= 1.f)
+    return fail(SOAP_ERR_HPARAM, "beta = %g is outside [0, 1)", (double)beta);
+  const int64_t d = trans ? n : m;
+  const Range rg{G, sizeof(float) * m * n, "G"}, rf{F, sizeof(float) * d * d, "F"};
+  if (overlap(rg, rf)) return fail(SOAP_ERR_ALIAS, "G overlaps F");
+  soap::GemmDesc g;
+  g.trans_a = trans ? 1 : 0; g.trans_b = trans ? 0 : 1;
+  g.M = d; g.N = d; g.K = trans ? m : n;
+  g.A = G; g.lda = n; g.B = G; g.ldb = n;
+  g.C = F; g.ldc = d; g.alpha = 1.f - beta; g.beta = beta;
+  hipError_t e = soap::launch_syrk_ema(g, stream);
+  if (e != hipSuccess) return hip_fail(e, "factor EMA");
+  return ok();
+}
+
+int soap_timing_enable(int enable) {
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.enabled = enable != 0;
+  return SOAP_OK;
+}
+
+int soap_timing_num_stages(void) { return ST_COUNT; }
+
+const char *soap_timing_stage_name(int stage) {
+  return (stage >= 0 && stage < ST_COUNT) ? kStageNames[stage] : "";
+}
+
+int soap_timing_collect(void) {
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  for (Pending &p : t.pending) {
+    hipError_t e = hipEventSynchronize(p.b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, p.a, p.b);
+    if (e != hipSuccess) return hip_fail(e, "timing collect");
+    t.ms[p.stage] += ms;
+    t.launches[p.stage] += 1;
+    t.flops[p.stage] += p.flops;
+    t.free_events.push_back(p.a);
+    t.free_events.push_back(p.b);
+  }
+  t.pending.clear();
+  return ok();
+}
+
+int soap_timing_reset(void) {
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  for (int i = 0; i < ST_COUNT; ++i) { t.ms[i] = 0; t.launches[i] = 0; t.flops[i] = 0; }
+  return SOAP_OK;
+}
+
+int soap_timing_get(int stage, double *total_ms, int64_t *launches, double *flops) {
+  if (stage < 0 || stage >= ST_COUNT) return fail(SOAP_ERR_SHAPE, "no stage %d", stage);
+  Timing &t = timing();
+  std::lock_guard<std::mutex> g(t.mu);
+  if (total_ms) *total_ms = t.ms[stage];
+  if (launches) *launches = t.launches[stage];
+  if (flops) *flops = t.flops[stage];
+  return SOAP_OK;
+}
+
+}  // extern "C"

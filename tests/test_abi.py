@@ -1,0 +1,119 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry
+point soap.h declares, and its host-side validation returns the documented
+status codes before anything is enqueued (only fake pointers are passed, and
+only to calls that must fail validation)."""
+import os
+import re
+
+import pytest
+
+import paper_2607_20548_amd as soap
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2607_20548_amd import build
+    build.build(force=False)
+    return soap.lib()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "soap.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(soap_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(L, name), name
+    assert sorted(names) == sorted(soap.EXPORTED)
+
+
+BASE = 0x7f0000000000
+MB = 1 << 24
+
+
+def fake_args(m=8, n=12, ws=None, **over):
+    p = {k: BASE + i * MB for i, k in enumerate(
+        ["param", "grad", "L", "R", "Q_L", "Q_R", "M", "V", "workspace"])}
+    args = dict(p, m=m, n=n, beta1=0.9, beta2=0.95, eps=1e-8, lr=1e-3, weight_decay=0.1, step=1,
+                flags=0, workspace_bytes=soap.soap_workspace_bytes(1, m, n) if ws is None else ws)
+    args.update(over)
+    return args
+
+
+def call_step(L, a):
+    return L.soap_step(a["param"], a["grad"], a["L"], a["R"], a["Q_L"], a["Q_R"], a["M"], a["V"],
+                       a["m"], a["n"], a["beta1"], a["beta2"], a["eps"], a["lr"],
+                       a["weight_decay"], a["step"], a["flags"], a["workspace"],
+                       a["workspace_bytes"], None)
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(param=None), soap.SOAP_ERR_NULL),
+    (dict(V=None), soap.SOAP_ERR_NULL),
+    (dict(m=0), soap.SOAP_ERR_SHAPE),
+    (dict(n=soap.SOAP_MAX_DIM + 1), soap.SOAP_ERR_SHAPE),
+    (dict(beta1=1.0), soap.SOAP_ERR_HPARAM),
+    (dict(beta2=-0.1), soap.SOAP_ERR_HPARAM),
+    (dict(eps=float("nan")), soap.SOAP_ERR_HPARAM),
+    (dict(lr=float("inf")), soap.SOAP_ERR_HPARAM),
+    (dict(weight_decay=-1.0), soap.SOAP_ERR_HPARAM),
+    (dict(step=0), soap.SOAP_ERR_HPARAM),
+    (dict(flags=2), soap.SOAP_ERR_HPARAM),
+    (dict(grad=BASE + 1 * MB + 4), soap.SOAP_ERR_ALIGN),
+    (dict(grad=BASE), soap.SOAP_ERR_ALIAS),                 # grad == param
+    (dict(R=BASE + 2 * MB + 64), soap.SOAP_ERR_ALIAS),      # R inside L
+])
+def test_step_validation(L, over, code):
+    assert call_step(L, fake_args(**over)) == code
+    assert soap.soap_last_error() != ""
+
+
+def test_workspace_too_small(L):
+    need = soap.soap_workspace_bytes(1, 8, 12)
+    assert need > 0
+    assert call_step(L, fake_args(ws=need - 1)) == soap.SOAP_ERR_WORKSPACE
+    assert "needed" in soap.soap_last_error()
+
+
+def test_workspace_bytes_shapes(L):
+    assert soap.soap_workspace_bytes(1, 0, 5) == 0
+    assert soap.soap_workspace_bytes(0, 4, 5) == 0
+    small = soap.soap_workspace_bytes(1, 256, 512)
+    assert soap.soap_workspace_bytes(4, 256, 512) > 3 * small
+    # the power products alone need (m^2 + n^2) floats
+    assert soap.soap_workspace_bytes(1, 4096, 14336) > 4 * (4096 ** 2 + 14336 ** 2)
+
+
+def test_batched_and_other_entry_points_validate(L):
+    a = fake_args()
+    rc = L.soap_step_batched(0, a["param"], a["grad"], a["L"], a["R"], a["Q_L"], a["Q_R"], a["M"],
+                             a["V"], 8, 12, 0.9, 0.95, 1e-8, 1e-3, 0.1, 1, 0, a["workspace"],
+                             a["workspace_bytes"], None)
+    assert rc == soap.SOAP_ERR_SHAPE
+    assert L.soap_qr_f32(0, BASE, BASE + MB, None, BASE + 2 * MB, 1 << 20, None) == soap.SOAP_ERR_SHAPE
+    assert L.soap_qr_f32(64, BASE, BASE + MB, None, BASE + 2 * MB, 16, None) == soap.SOAP_ERR_WORKSPACE
+    assert L.soap_init_state(1, 0, 4, None, None, None, None, None, None, None) == soap.SOAP_ERR_SHAPE
+    assert L.soap_init_state(1, 4, 4, BASE + 8, None, None, None, None, None, None) == soap.SOAP_ERR_ALIGN
+    assert L.soap_factor_ema_f32(0, 4, 4, BASE, BASE + MB, 1.5, None) == soap.SOAP_ERR_HPARAM
+    assert L.soap_gemm_f32(0, 0, 0, 4, 4, 1.0, BASE, 4, BASE, 4, 0.0, BASE, 4, None) == soap.SOAP_ERR_SHAPE
+
+
+def test_timing_api_without_gpu(L):
+    n = soap.soap_timing_num_stages()
+    names = [soap.soap_timing_stage_name(i) for i in range(n)]
+    assert "qr_R" in names and "power_R" in names and len(set(names)) == n
+    soap.soap_timing_reset()
+    assert soap.soap_timing_get(0) == (0.0, 0, 0.0)
+
+
+def test_success_clears_error(L):
+    call_step(L, fake_args(m=0))
+    assert soap.soap_last_error() != ""
+    soap.soap_timing_reset()   # a call that succeeds without touching the GPU
+    assert L.soap_workspace_bytes(1, 4, 4) > 0
