@@ -51,38 +51,27 @@ constexpr int RCH = 256;           // rows per workgroup in the inner reduction
 constexpr int RED_THREADS = 1024;  // threads of the inner reduction
 constexpr int APPLY_ROWS = 8;      // rows per workgroup in the inner apply
 constexpr int MAX_B = 32;
+constexpr int MAX_PANEL = 16;      // widest inner panel
 constexpr int PART_STRIDE = MAX_B * NB;   // floats per partial block
 
 // --------------------------------------------------------------- reductions
-// Transposed butterfly over a wave64: NV values per lane (NV a power of two,
-// <= 64) are summed across the wave with NV - 1 + log2(64/NV) shuffles.  On
-// return lane l holds the wave total of value index l / (64 / NV).
-template <int NV>
-__device__ __forceinline__ float wave_reduce_transposed(float (&v)[NV], int lane) {
-#pragma unroll
-  for (int half = NV / 2, mask = 32; half >= 1; half >>= 1, mask >>= 1) {
-    const bool up = (lane & mask) != 0;
-#pragma unroll
-    for (int i = 0; i < half; ++i) {
-      const float keep = up ? v[i + half] : v[i];
-      const float send = up ? v[i] : v[i + half];
-      v[i] = keep + __shfl_xor(send, mask);
-    }
-  }
-  float x = v[0];
-#pragma unroll
-  for (int mask = 32 / NV; mask >= 1; mask >>= 1) x += __shfl_xor(x, mask);
-  return x;
-}
-
-// Sum of NV values over the panel workgroup; the NV totals are left in
-// tot (LDS) for every thread to read.  red: [PANEL_WAVES][NV] in LDS.
+// Sum of NV values over the panel workgroup; the NV totals are left in tot
+// (LDS) for every thread to read.  Each value is summed over the wave with
+// xor shuffles (no lane-dependent selects: a transposed butterfly would need
+// per-lane choices of which half to keep, which the compiler lowers to
+// compare/select chains over the whole array), then across waves in LDS.
+// red: [PANEL_WAVES][NV] in LDS.
 template <int NV>
 __device__ __forceinline__ void block_allreduce(float (&v)[NV], float *red, float *tot) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  constexpr int G = 64 / NV;
-  const float x = wave_reduce_transposed<NV>(v, lane);
-  if ((lane % G) == 0) red[wave * NV + lane / G] = x;
+#pragma unroll
+  for (int mask = 32; mask >= 1; mask >>= 1)
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] += __shfl_xor(v[i], mask);
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) red[wave * NV + i] = v[i];
+  }
   __syncthreads();
   if (threadIdx.x < NV) {
     float s = 0.f;
@@ -300,45 +289,49 @@ __global__ __launch_bounds__(RED_THREADS) void qr_inner_reduce_kernel(InnerParam
   const int rows = min(RCH, n - r0);
   const int t = threadIdx.x;
 
-  // tile load: thread -> (row, group of 32 columns); 32 coalesced loads in flight
+  // tile load: thread -> (row, group of 32 columns); 32 coalesced loads in
+  // flight.  Rows past the end are zero-filled (they enter the contraction).
   {
     const int rr = t & (RCH - 1), cg = t / RCH;    // 4 column groups
-    if (rr < rows) {
-      const float *src = At + (int64_t)(c + 32 * cg) * n + r0 + rr;
-      float v[32];
+    const float *src = At + (int64_t)(c + 32 * cg) * n + r0 + rr;
+    float v[32];
 #pragma unroll
-      for (int u = 0; u < 32; ++u) v[u] = (32 * cg + u < ncol) ? src[(int64_t)u * n] : 0.f;
+    for (int u = 0; u < 32; ++u)
+      v[u] = (rr < rows && 32 * cg + u < ncol) ? src[(int64_t)u * n] : 0.f;
 #pragma unroll
-      for (int u = 0; u < 32; ++u)
-        if (32 * cg + u < ncol) tile[(32 * cg + u) * TS + rr] = v[u];
-    }
+    for (int u = 0; u < 32; ++u) tile[(32 * cg + u) * TS + rr] = v[u];
   }
   __syncthreads();
 
-  // thread -> (outer-block column q, one of 8 slices of the panel columns)
-  constexpr int JG = RED_THREADS / 128;
-  const int q = t & 127;
-  const int jg = t >> 7;
-  const int hb = (b + JG - 1) / JG;
-  float o[MAX_B / JG];
-#pragma unroll
-  for (int u = 0; u < MAX_B / JG; ++u) o[u] = 0.f;
-  if (q < ncol) {
-    const float *xc = tile + q * TS;
-    const float *yc = tile + (off + jg * hb) * TS;
-    for (int rr = 0; rr < rows; ++rr) {
-      const float x = xc[rr];
-#pragma unroll
-      for (int u = 0; u < MAX_B / JG; ++u)
-        if (u < hb && jg * hb + u < b) o[u] += yc[u * TS + rr] * x;
-    }
-  }
+  // O[i][q] = sum_rows Y_p[row][i] * X[row][q] on the matrix cores: wave w < 8
+  // owns the 16 x 16 block q in [16w, 16w+16) (i < 16 covers any panel width),
+  // v_mfma_f32_16x16x4_f32 over the 256 rows.  The K order is permuted: at
+  // step s, lane group g = lane/16 takes row 64 g + s, so each lane reads four
+  // consecutive rows of its tile column with one 16-byte LDS read.
+  const int lane = t & 63, wave = t >> 6;
   float *part = p.part + bz * p.sP + (int64_t)g * PART_STRIDE;
-  if (q < ncol) {
+  if (wave < 8) {
+    typedef float v4f __attribute__((ext_vector_type(4)));
+    const int i = lane & 15, grp = lane >> 4;
+    const int q = 16 * wave + i;
+    // A operand: Y_p column i (zero beyond the panel width); B operand: column q
+    const float *acol = tile + (off + (i < b ? i : 0)) * TS + 64 * grp;
+    const float *bcol = tile + q * TS + 64 * grp;
+    const float amask = (i < b) ? 1.f : 0.f;
+    v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int s4 = 0; s4 < 64; s4 += 4) {
+      float a4[4], b4[4];
 #pragma unroll
-    for (int u = 0; u < MAX_B / JG; ++u) {
-      const int jj = jg * hb + u;
-      if (u < hb && jj < b) part[jj * NB + q] = o[u];
+      for (int u = 0; u < 4; ++u) { a4[u] = acol[s4 + u] * amask; b4[u] = bcol[s4 + u]; }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[u], b4[u], acc, 0, 0, 0);
+    }
+    // accumulator r of lane l holds O[4*(l/16) + r][16*wave + l%16]
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int ii = 4 * grp + r;
+      if (ii < b && q < ncol) part[ii * NB + q] = acc[r];
     }
   }
   __threadfence();
@@ -372,21 +365,34 @@ __global__ __launch_bounds__(RED_THREADS) void qr_inner_reduce_kernel(InnerParam
     Os[jj * NB + qq] = tot16;
   }
   __syncthreads();
-  // T_p, one column at a time (thread i < j computes T_p[i][j]); stored at
-  // Ts[off+i][off+j].  G[l][j] = Os[l][off + j].
-  for (int j = 0; j < b; ++j) {
-    if (t <= j) {
-      float val = beta[j];
-      if (t < j) {
+  // T_p by wave 0: lane i keeps row i of T_p in registers; everything is
+  // unrolled over the (at most 16) panel columns, so there is no barrier and
+  // no dependent LDS round trip inside the recurrence.
+  //   T_p[j][j] = beta_j,  T_p[i][j] = -beta_j sum_{l=i}^{j-1} T_p[i][l] G[l][j],
+  // with G[l][j] = Os[l][off + j] (the panel's Gram matrix).
+  if (t < 64) {
+    const int i = t;
+    float trow[MAX_PANEL];
+#pragma unroll
+    for (int j = 0; j < MAX_PANEL; ++j) {
+      float val = 0.f;
+      if (j < b) {
+        const float bj = beta[j];
         float acc = 0.f;
-        for (int l = t; l < j; ++l) acc += Ts[(off + t) * NB + off + l] * Os[l * NB + off + j];
-        val = -beta[j] * acc;
+#pragma unroll
+        for (int l = 0; l < j; ++l)
+          if (l >= i) acc += trow[l] * Os[l * NB + off + j];
+        val = (i == j) ? bj : (i < j ? -bj * acc : 0.f);
       }
-      Ts[(off + t) * NB + off + j] = val;
+      trow[j] = val;
     }
-    if (t > j && t < b) Ts[(off + t) * NB + off + j] = 0.f;
-    __syncthreads();
+    if (i < b) {
+#pragma unroll
+      for (int j = 0; j < MAX_PANEL; ++j)
+        if (j < b) Ts[(off + i) * NB + off + j] = trow[j];
+    }
   }
+  __syncthreads();
   // rows off..off+b of T: zeros left of the diagonal block, then T_p
   for (int e = t; e < b * (off + b); e += RED_THREADS) {
     const int i = e / (off + b), jc = e % (off + b);
@@ -397,7 +403,9 @@ __global__ __launch_bounds__(RED_THREADS) void qr_inner_reduce_kernel(InnerParam
   for (int e = t; e < b * w; e += RED_THREADS) {
     const int jj = e / w, qq = e - jj * w;
     float s = 0.f;
-    for (int l = 0; l <= jj; ++l) s += Ts[(off + l) * NB + off + jj] * Os[l * NB + off + b + qq];
+#pragma unroll
+    for (int l = 0; l < MAX_PANEL; ++l)
+      if (l <= jj) s += Ts[(off + l) * NB + off + jj] * Os[l * NB + off + b + qq];
     Wi[jj * w + qq] = s;
   }
   if (off > 0) {
@@ -405,16 +413,25 @@ __global__ __launch_bounds__(RED_THREADS) void qr_inner_reduce_kernel(InnerParam
     for (int e = t; e < off * b; e += RED_THREADS) {
       const int i = e / b, jj = e - i * b;
       float s = 0.f;
-      for (int l = 0; l <= jj; ++l) s += Os[l * NB + i] * Ts[(off + l) * NB + off + jj];
+#pragma unroll
+      for (int l = 0; l < MAX_PANEL; ++l)
+        if (l <= jj) s += Os[l * NB + i] * Ts[(off + l) * NB + off + jj];
       Zs[i * MAX_B + jj] = s;
     }
     __syncthreads();
     // T[i][off + jj] = -sum_{l = i}^{off-1} T[i][l] Z[l][jj]
     for (int e = t; e < off * b; e += RED_THREADS) {
       const int i = e / b, jj = e - i * b;
-      float s = 0.f;
-      for (int l = i; l < off; ++l) s += Ts[i * NB + l] * Zs[l * MAX_B + jj];
-      T[i * NB + off + jj] = -s;
+      float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+      int l = i;
+      for (; l + 4 <= off; l += 4) {
+        s0 += Ts[i * NB + l + 0] * Zs[(l + 0) * MAX_B + jj];
+        s1 += Ts[i * NB + l + 1] * Zs[(l + 1) * MAX_B + jj];
+        s2 += Ts[i * NB + l + 2] * Zs[(l + 2) * MAX_B + jj];
+        s3 += Ts[i * NB + l + 3] * Zs[(l + 3) * MAX_B + jj];
+      }
+      for (; l < off; ++l) s0 += Ts[i * NB + l] * Zs[l * MAX_B + jj];
+      T[i * NB + off + jj] = -((s0 + s1) + (s2 + s3));
     }
   }
   if (t == 0) p.cnt[bz] = 0u;

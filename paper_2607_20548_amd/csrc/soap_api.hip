@@ -118,9 +118,31 @@ class StageScope {
   bool active_ = false;
 };
 
+// ------------------------------------------------------ auxiliary stream
+// The L-side chain (factor EMA L, power product, QR of m x m) and the R-side
+// chain are independent until the rotations; the L side runs on one
+// auxiliary stream per device (default priority, created on first use) and is
+// joined back with events, so its latency-bound QR panels overlap the R side.
+std::mutex g_aux_mu;
+hipStream_t g_aux[64] = {};
+
+hipError_t aux_stream(hipStream_t *out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_aux_mu);
+  if (!g_aux[dev]) {
+    e = hipStreamCreateWithFlags(&g_aux[dev], hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+  }
+  *out = g_aux[dev];
+  return hipSuccess;
+}
+
 // ------------------------------------------------------------- workspace
 struct StepLayout {
-  size_t al, ar, tg, tm, nb, qr, total;
+  size_t al, ar, tg, tm, nb, qrl, qrr, total;
 };
 
 StepLayout step_layout(int64_t batch, int64_t m, int64_t n) {
@@ -132,7 +154,8 @@ StepLayout step_layout(int64_t batch, int64_t m, int64_t n) {
   L.tg = o; o = align256(o + f * batch * m * n);
   L.tm = o; o = align256(o + f * batch * m * n);
   L.nb = o; o = align256(o + f * batch * m * n);
-  L.qr = o; o = align256(o + soap::qr_workspace_bytes(batch, std::max(m, n)));
+  L.qrl = o; o = align256(o + soap::qr_workspace_bytes(batch, m));
+  L.qrr = o; o = align256(o + soap::qr_workspace_bytes(batch, n));
   L.total = o;
   return L;
 }
@@ -204,8 +227,10 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   float *TG = reinterpret_cast<float *>(w + lay.tg);
   float *TM = reinterpret_cast<float *>(w + lay.tm);
   float *NN = reinterpret_cast<float *>(w + lay.nb);
-  void *qws = w + lay.qr;
-  const size_t qws_bytes = ws_bytes - lay.qr;
+  void *qws_l = w + lay.qrl;
+  const size_t qws_l_bytes = lay.qrr - lay.qrl;
+  void *qws_r = w + lay.qrr;
+  const size_t qws_r_bytes = ws_bytes - lay.qrr;
   const int64_t mn = m * n, mm = m * m, nn = n * n;
   const double B = (double)batch, md = (double)m, nd = (double)n;
   hipError_t e;
@@ -215,14 +240,45 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if ((e = soap::launch_momentum(M, grad, batch * mn, beta1, s)) != hipSuccess)
       return hip_fail(e, "momentum");
   }
+  // Fork: the L side on the auxiliary stream, the R side on the caller's.
+  hipStream_t sl = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  if ((e = aux_stream(&sl)) != hipSuccess) return hip_fail(e, "auxiliary stream");
+  if ((e = hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming)) != hipSuccess)
+    return hip_fail(e, "event");
+  if ((e = hipEventCreateWithFlags(&ev_join, hipEventDisableTiming)) != hipSuccess) {
+    hipEventDestroy(ev_fork);
+    return hip_fail(e, "event");
+  }
+  struct EventGuard {
+    hipEvent_t a, b;
+    ~EventGuard() { hipEventDestroy(a); hipEventDestroy(b); }
+  } guard{ev_fork, ev_join};
+  if ((e = hipEventRecord(ev_fork, s)) != hipSuccess) return hip_fail(e, "fork record");
+  if ((e = hipStreamWaitEvent(sl, ev_fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
   {  // L <- b2 L + (1-b2) G G^T
-    StageScope sc(ST_FACTOR_L, B * md * (md + 1) * nd, s);
+    StageScope sc(ST_FACTOR_L, B * md * (md + 1) * nd, sl);
     soap::GemmDesc d;
     d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
     d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
     d.C = L; d.ldc = m; d.sC = mm; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
-    if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return hip_fail(e, "factor EMA L");
+    if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "factor EMA L");
+  }  // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L since
+  // L is symmetric (both triangles are stored).
+  {  // A_L^T = Q_L^T L
+    StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0;
+    d.M = m; d.N = m; d.K = m; d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
+    d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "power L");
   }
+  {  // Q_L = QR(A_L).Q
+    StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
+    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl)) != hipSuccess)
+      return hip_fail(e, "QR L");
+  }
+  if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
   {  // R <- b2 R + (1-b2) G^T G
     StageScope sc(ST_FACTOR_R, B * nd * (nd + 1) * md, s);
     soap::GemmDesc d;
@@ -230,16 +286,6 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
     d.C = R; d.ldc = n; d.sC = nn; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
     if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return hip_fail(e, "factor EMA R");
-  }
-  // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L since
-  // L is symmetric (both triangles are stored).
-  {  // A_L^T = Q_L^T L
-    StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, s);
-    soap::GemmDesc d;
-    d.trans_a = 1; d.trans_b = 0;
-    d.M = m; d.N = m; d.K = m; d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
-    d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
-    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power L");
   }
   {  // A_R^T = Q_R^T R
     StageScope sc(ST_POWER_R, B * 2.0 * nd * nd * nd, s);
@@ -249,16 +295,11 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     d.C = AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
     if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power R");
   }
-  {  // Q_L = QR(A_L).Q
-    StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, s);
-    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws, qws_bytes, s)) != hipSuccess)
-      return hip_fail(e, "QR L");
-  }
   {  // Q_R = QR(A_R).Q
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
-    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws, qws_bytes, s)) != hipSuccess)
+    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s)) != hipSuccess)
       return hip_fail(e, "QR R");
-  }
+  }  if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
   {  // T_G = Q_L^T G,  T_M = Q_L^T M
     StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, s);
     soap::GemmDesc d;
