@@ -55,7 +55,9 @@ struct KParams {
 // Loads one operand slab of 128 x-rows by BK k-values into registers.
 //   KCONTIG = true : global element (x, k) at base[x*ld + k]
 //   KCONTIG = false: global element (x, k) at base[k*ld + x]
-// Work split: 512 (x, k-quad) items over 256 threads, two per thread.
+// Work split: 512 (x, k-quad) items over 256 threads, two per thread; with
+// VEC == 4 an x-contiguous slab is instead read as 4 x 2 blocks (k-quad, x
+// pair), one per thread.
 template <bool KCONTIG, int VEC>
 struct SlabLoader {
   float r[8];
@@ -77,6 +79,21 @@ struct SlabLoader {
           for (int e = 0; e < 4; ++e)
             r[4 * s + e] = (x < X && k + e < K) ? base[(int64_t)x * ld + k + e] : 0.f;
         }
+      } else if (VEC == 4) {
+        // x-contiguous with 8-byte loads: thread -> (k-quad, x pair); the
+        // 4 x 2 block is transposed in registers (r[0..3] = column x,
+        // r[4..7] = column x+1).  Needs an even x extent and leading dimension.
+        if (s == 0) {
+          const int x = x0 + 2 * (tid & 63);
+          const int k = k0 + 4 * (tid >> 6);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float2 v = make_float2(0.f, 0.f);
+            if (x < X && k + e < K) v = *reinterpret_cast<const float2 *>(base + (int64_t)(k + e) * ld + x);
+            r[e] = v.x;
+            r[4 + e] = v.y;
+          }
+        }
       } else {
         const int x = x0 + (idx & 127);
         const int k = k0 + 4 * (idx >> 7);
@@ -88,6 +105,13 @@ struct SlabLoader {
   }
 
   __device__ __forceinline__ void store(float *lds, int tid) const {
+    if (!KCONTIG && VEC == 4) {
+      const int xl = 2 * (tid & 63), kq = tid >> 6;
+      *reinterpret_cast<float4 *>(lds + xl * LDSK + 4 * kq) = make_float4(r[0], r[1], r[2], r[3]);
+      *reinterpret_cast<float4 *>(lds + (xl + 1) * LDSK + 4 * kq) =
+          make_float4(r[4], r[5], r[6], r[7]);
+      return;
+    }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int idx = tid + NTHREADS * s;
@@ -325,13 +349,22 @@ KParams make_params(const GemmDesc &d) {
   return kp;
 }
 
-// 16-byte vector loads are used only on k-contiguous operands; they need the
-// k extent, the leading dimension, the batch stride and the base to be
-// multiples of 4 floats.
+// Vector loads: a k-contiguous operand uses 16-byte loads along k (k extent,
+// leading dimension, batch stride multiples of 4 floats, 16-byte aligned
+// base); an x-contiguous operand uses 8-byte loads along x (even x extent,
+// leading dimension and batch stride, 8-byte aligned base).
+bool aligned8(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
+
 bool vec_ok_for(const GemmDesc &d, const float *A2) {
-  bool ok = (d.K % 4 == 0);
-  if (d.trans_a == 0) ok = ok && d.lda % 4 == 0 && d.sA % 4 == 0 && aligned16(d.A) && (!A2 || aligned16(A2));
-  if (d.trans_b == 1) ok = ok && d.ldb % 4 == 0 && d.sB % 4 == 0 && aligned16(d.B);
+  bool ok = true;
+  if (d.trans_a == 0)
+    ok = ok && d.K % 4 == 0 && d.lda % 4 == 0 && d.sA % 4 == 0 && aligned16(d.A) && (!A2 || aligned16(A2));
+  else
+    ok = ok && d.M % 2 == 0 && d.lda % 2 == 0 && d.sA % 2 == 0 && aligned8(d.A) && (!A2 || aligned8(A2));
+  if (d.trans_b == 1)
+    ok = ok && d.K % 4 == 0 && d.ldb % 4 == 0 && d.sB % 4 == 0 && aligned16(d.B);
+  else
+    ok = ok && d.N % 2 == 0 && d.ldb % 2 == 0 && d.sB % 2 == 0 && aligned8(d.B);
   return ok;
 }
 
