@@ -77,10 +77,11 @@ hipError_t launch_copy(float *dst, const float *src, int64_t count, hipStream_t 
 // At = A^T row-major (element stride n*n between matrices).  At is overwritten
 // by the factorization; the Q factor with non-negative diag(R) is written
 // row-major to Q.  If Rf is non-null the triangular factor is written there
-// (row-major, strict lower part zero).
+// (row-major, strict lower part zero).  Work is ordered on stream s; the
+// panel factorizations run on stream sp (joined back into s with events).
 size_t qr_workspace_bytes(int64_t batch, int64_t n);
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
-                                void *ws, size_t ws_bytes, hipStream_t s);
+                                void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp);
 // dst = src^T for one n x n row-major matrix.
 hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t s);
 

@@ -40,6 +40,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <vector>
 
 namespace soap {
 namespace {
@@ -482,6 +483,359 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
   }
 }
 
+// ------------------------------------------------ resident-block factorization
+// One launch factors a whole outer block (rows c..n-1, nb <= NB columns) with
+// the same reflectors as the panel path.  Workgroup g keeps rows
+// c + g*BK_ROWS .. c + (g+1)*BK_ROWS - 1 of the block in registers: thread t
+// owns column k = t/4 and, with part = t%4, the local rows 16 i + 4 part + e
+// (i < BK_R/4, e < 4).  Per column j:
+//   * the pivot column is broadcast through LDS and every thread forms the
+//     partial dot of its column with the pivot below the diagonal row;
+//   * the partials are summed grid-wide in two hops through global memory.
+//     Every value travels as a 64-bit item (value bits | generation << 32)
+//     written and read with agent-scope atomics, so a reader recognises a
+//     fresh value by its generation (global column index + 1) and needs no
+//     barrier or flag: each workgroup posts its partial of every column; the
+//     owner of column k (workgroup 1 + k mod (P-1)) sums the P partials in
+//     workgroup order, reads the diagonal-row value from workgroup 0, and
+//     forwards both into a private copy for every workgroup (so that no
+//     cache line is polled by more than one workgroup); every workgroup reads
+//     the totals it needs from its copy, so all of them apply bit-identical
+//     reflectors.  Items are double-buffered by column parity: no workgroup
+//     can get two columns ahead of a reader;
+//   * every thread updates its own column.
+// Workgroup 0 holds the block's diagonal rows: its pivot broadcast is zero at
+// and above the diagonal row (so its dot products need no masks), it posts
+// the diagonal-row values, and it keeps S = strict upper part of Y^T Y,
+//   S[l][j] = y_l^T v_j = A_l + D_l / v0_j  (from the same dot products),
+// from which it forms T after the column loop:
+//   T[0:j, j] = -beta_j T[0:j, 0:j] S[0:j, j],  T[j][j] = beta_j.
+// The launch needs all of its workgroups resident at once; the host limits it
+// to BK_MAX_WG workgroups.  Waits are bounded: one that exceeds BK_SPIN_LIMIT
+// polls raises a per-matrix abort flag, after which every wait returns at
+// once and the block is written as NaN, so the kernel always ends.
+constexpr int BK_THREADS = 512;
+constexpr int BK_PARTS = 4;                     // threads per column
+constexpr int BK_R = 64;                        // rows per thread
+constexpr int BK_ROWS = BK_PARTS * BK_R;        // rows per workgroup
+constexpr int BK_MAX_ITEMS = 16;                // partials summed per owner thread
+constexpr int BK_MAX_P = BK_PARTS * BK_MAX_ITEMS;   // workgroups per matrix (n <= 16384)
+constexpr int BK_MAX_WG = 96;                   // workgroups per launch
+constexpr unsigned BK_SPIN_LIMIT = 1u << 22;
+constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (spreads banks)
+// exchange area per matrix, in 64-bit items: partials [2][NB][BK_MAX_P],
+// diagonal-row values of workgroup 0 [2][NB], per-reader copies of
+// (total, diagonal-row value) [BK_MAX_P][2][NB][2] (4 KiB per reader), abort flag
+constexpr int64_t BK_XD = 0;
+constexpr int64_t BK_XA = 2 * NB * BK_MAX_P;
+constexpr int64_t BK_XC = BK_XA + 2 * NB;
+constexpr int64_t BK_XABORT = BK_XC + (int64_t)BK_MAX_P * 2 * NB * 2;
+constexpr int64_t BK_XSTRIDE = BK_XABORT + 32;
+
+struct BlockParams {
+  float *At;
+  int64_t sA;
+  int n, c, nb;
+  float *T;                  // this block's T (NB x NB row-major), batch stride sT
+  int64_t sT;
+  float *Rf;                 // optional triangular-factor output (batch stride sA)
+  float *dsign, *beta;       // n per matrix
+  unsigned long long *xch;   // exchange area, BK_XSTRIDE items per matrix (zeroed per call)
+  int P;                     // workgroups per matrix
+};
+
+__device__ __forceinline__ void bk_put(unsigned long long *p, float v, unsigned gen) {
+  const unsigned long long item = ((unsigned long long)gen << 32) | __float_as_uint(v);
+  __hip_atomic_store(p, item, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ unsigned long long bk_get(const unsigned long long *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One failed poll: counts it, raises the abort flag past the limit, and
+// reports whether the wait must end (limit reached or abort seen).  Polls
+// back off (s_sleep grows to about 0.2 us) so that waiting workgroups do not
+// crowd out the stores they wait for.
+__device__ __forceinline__ bool bk_give_up(unsigned &spins, unsigned *abort_flag) {
+  ++spins;
+  if (spins >= BK_SPIN_LIMIT) {
+    __hip_atomic_store(abort_flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return true;
+  }
+  if ((spins & 63u) == 0u &&
+      __hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+    return true;
+  if (spins < 4) __builtin_amdgcn_s_sleep(1);
+  else if (spins < 16) __builtin_amdgcn_s_sleep(2);
+  else __builtin_amdgcn_s_sleep(4);
+  return false;
+}
+
+// Owner hop: waits for generation `gen` of the partials p[0], p[4], ...,
+// p[4 (cnt-1)] (re-reading only those not yet current) and returns their sum
+// in order.  false: aborted.
+__device__ __forceinline__ bool bk_sum_partials(const unsigned long long *p, int cnt, unsigned gen,
+                                                unsigned *abort_flag, float &sum) {
+  float v[BK_MAX_ITEMS];
+  unsigned pending = (cnt >= 32) ? ~0u : ((1u << cnt) - 1u);
+  unsigned spins = 0;
+  for (;;) {
+#pragma unroll
+    for (int u = 0; u < BK_MAX_ITEMS; ++u)
+      if (pending & (1u << u)) {
+        const unsigned long long it = bk_get(p + BK_PARTS * u);
+        v[u] = __uint_as_float((unsigned)it);
+        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << u);
+      }
+    if (pending == 0u) break;
+    if (bk_give_up(spins, abort_flag)) return false;
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < BK_MAX_ITEMS; ++u)
+    if (u < cnt) s += v[u];
+  sum = s;
+  return true;
+}
+
+// Reader hop: waits for generation `gen` of the items at p and (if q is not
+// null) q.  false: aborted.
+__device__ __forceinline__ bool bk_read2(const unsigned long long *p, const unsigned long long *q,
+                                         unsigned gen, unsigned *abort_flag, float &vp,
+                                         float &vq) {
+  unsigned spins = 0;
+  bool hp = false, hq = (q == nullptr);
+  for (;;) {
+    if (!hp) {
+      const unsigned long long a = bk_get(p);
+      vp = __uint_as_float((unsigned)a);
+      hp = (unsigned)(a >> 32) == gen;
+    }
+    if (!hq) {
+      const unsigned long long b = bk_get(q);
+      vq = __uint_as_float((unsigned)b);
+      hq = (unsigned)(b >> 32) == gen;
+    }
+    if (hp && hq) return true;
+    if (bk_give_up(spins, abort_flag)) return false;
+  }
+}
+
+template <int R>
+__global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
+  constexpr int NI = R / 4;
+  constexpr int RS = BK_PARTS * R;
+  // register groups i that can hold one of the diagonal rows 0..NB-1 of
+  // workgroup 0 (local row 16 i + 4 part + e < NB); only these need masks
+  constexpr int NIM = (NB / 16 < NI) ? NB / 16 : NI;
+  __shared__ float px[2][RS];            // pivot column, by column parity
+  __shared__ float pv[2][2];             // pivot tail sum of squares and diagonal value
+  __shared__ float bs[NB];               // beta_j (workgroup 0)
+  __shared__ float Ss[NB * BK_TSTR];     // S (workgroup 0), row-major
+  __shared__ float Ts[NB * BK_TSTR];     // T (workgroup 0), row-major
+
+  const int g = blockIdx.x;
+  const int64_t bz = blockIdx.y;
+  const int t = threadIdx.x, k = t >> 2, part = t & 3;
+  const int n = p.n, c = p.c, nb = p.nb, P = p.P;
+  const unsigned un = (unsigned)n;     // n*n < 2^31
+  float *At = p.At + bz * p.sA;
+  const int r0 = c + g * RS;
+  const bool w0 = (g == 0);
+  const bool col = k < nb;
+  const bool owner = P > 1 && col && 1 + k % (P - 1) == g;
+  unsigned long long *X = p.xch + bz * BK_XSTRIDE;
+  unsigned *abort_flag = reinterpret_cast<unsigned *>(X + BK_XABORT);
+
+  float a[NI][4];
+  {
+    const float *src = At + (unsigned)(c + (col ? k : 0)) * un;
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = r0 + 16 * i + 4 * part + e;
+        a[i][e] = (col && row < n) ? src[row] : 0.f;
+      }
+  }
+  bool alive = true;
+
+  for (int j = 0; j < nb; ++j) {
+    const int par = j & 1;
+    const unsigned gen = (unsigned)(c + j + 1);
+    if (k == j) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int lr = 16 * i + 4 * part + e;
+          px[par][lr] = (w0 && i < NIM && lr <= j) ? 0.f : a[i][e];
+        }
+    }
+    __syncthreads();
+    const float *x = px[par];
+    float d = 0.f, av = 0.f;
+    if (col) {
+      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[e] += a[i][e] * x[16 * i + 4 * part + e];
+      d = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+      if (w0) {   // value of the diagonal row j
+#pragma unroll
+        for (int i = 0; i < NIM; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) av = (16 * i + 4 * part + e == j) ? a[i][e] : av;
+      }
+    }
+    d += __shfl_xor(d, 1);
+    d += __shfl_xor(d, 2);
+    av += __shfl_xor(av, 1);
+    av += __shfl_xor(av, 2);
+    float D = d, A = av;
+    if (P > 1) {
+      unsigned long long *xd = X + BK_XD + ((int64_t)par * NB + k) * BK_MAX_P;
+      unsigned long long *xa = X + BK_XA + par * NB + k;
+      const int lead = (t & 63) & ~3;          // lane of part 0 of this column
+      if (col && part == 0) bk_put(xd + g, d, gen);
+      if (w0 && col && part == 1) bk_put(xa, av, gen);
+      if (owner) {                             // owner hop
+        float s = 0.f, aval = 0.f, unused = 0.f;
+        const int cnt = (P - part + BK_PARTS - 1) / BK_PARTS;
+        if (alive) alive = bk_sum_partials(xd + part, cnt, gen, abort_flag, s);
+        s += __shfl_xor(s, 1);
+        s += __shfl_xor(s, 2);
+        if (part == 0 && alive) alive = bk_read2(xa, nullptr, gen, abort_flag, aval, unused);
+        aval = __shfl(aval, lead);
+        for (int r = part; r < P; r += BK_PARTS) {
+          unsigned long long *cp = X + BK_XC + (((int64_t)r * 2 + par) * NB + k) * 2;
+          bk_put(cp, s, gen);
+          bk_put(cp + 1, aval, gen);
+        }
+      }
+      if (col && (w0 || k >= j)) {             // reader hop (one lane per column)
+        const unsigned long long *cp = X + BK_XC + (((int64_t)g * 2 + par) * NB + k) * 2;
+        float tot = 0.f, aa = 0.f;
+        if (part == 0 && alive) alive = bk_read2(cp, w0 ? nullptr : cp + 1, gen, abort_flag, tot, aa);
+        D = __shfl(tot, lead);
+        aa = __shfl(aa, lead);
+        if (!w0) A = aa;
+      }
+    }
+    if (k == j && part == 0) {
+      pv[par][0] = D;
+      pv[par][1] = A;
+    }
+    __syncthreads();
+    const float st = pv[par][0], x0 = pv[par][1];
+    float bet, inv_v0, rjj;
+    if (st == 0.f) {          // already triangular: H = I
+      bet = 0.f;
+      inv_v0 = 0.f;
+      rjj = x0;
+    } else {
+      const float sigma = sqrtf(x0 * x0 + st);
+      const float v0 = (x0 >= 0.f) ? (x0 + sigma) : (x0 - sigma);
+      bet = 2.f * v0 * v0 / (st + v0 * v0);
+      inv_v0 = 1.f / v0;
+      rjj = (x0 >= 0.f) ? -sigma : sigma;
+    }
+    if (col && k > j) {
+      // a -= f v with v = [1 at the diagonal row; x / v0 below it]; in
+      // workgroup 0 the broadcast x is zero at and above the diagonal row
+      const float f = bet * (A + D * inv_v0);
+      const float fs = f * inv_v0;
+      if (w0) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int lr = 16 * i + 4 * part + e;
+            a[i][e] = fmaf(-fs, x[lr], a[i][e]);
+            if (i < NIM) a[i][e] -= (lr == j) ? f : 0.f;
+          }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[16 * i + 4 * part + e], a[i][e]);
+      }
+    } else if (k == j) {
+      if (w0) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int lr = 16 * i + 4 * part + e;
+            if (i < NIM)
+              a[i][e] = (lr > j) ? a[i][e] * inv_v0 : ((lr == j) ? rjj : a[i][e]);
+            else
+              a[i][e] *= inv_v0;
+          }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) a[i][e] *= inv_v0;
+      }
+    }
+    if (w0) {
+      if (col && k < j && part == 0) Ss[k * BK_TSTR + j] = A + D * inv_v0;
+      if (t == 0) {
+        bs[j] = bet;
+        p.beta[bz * n + c + j] = bet;
+        p.dsign[bz * n + c + j] = (rjj < 0.f) ? -1.f : 1.f;
+      }
+    }
+  }
+
+  // Write Y (zeros above its diagonal, ones on it) and the R entries of the
+  // block's diagonal rows.  An aborted exchange poisons the block.
+  const bool bad =
+      P > 1 && __hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+  const float nan = __builtin_nanf("");
+  if (col) {
+    float *dst = At + (unsigned)(c + k) * un;
+    float *Rf = p.Rf ? p.Rf + bz * p.sA : nullptr;
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int lr = 16 * i + 4 * part + e;
+        const int row = r0 + lr;
+        if (row < n) {
+          float v = a[i][e];
+          if (w0 && lr <= k) {
+            if (Rf) Rf[(unsigned)row * un + c + k] = bad ? nan : v;
+            v = (lr == k) ? 1.f : 0.f;
+          }
+          dst[row] = bad ? nan : v;
+        }
+      }
+  }
+  if (!w0) return;
+  // T by columns: thread (k, part) sums T[k][l] S[l][j] over l = 4q + part.
+  for (int e = t; e < NB * BK_TSTR; e += BK_THREADS) Ts[e] = 0.f;
+  __syncthreads();
+  for (int j = 0; j < nb; ++j) {
+    float s = 0.f;
+    if (k < j) {
+      const int q0 = (k - part + BK_PARTS - 1) / BK_PARTS;   // first l = 4q + part >= k
+      for (int l = BK_PARTS * (q0 > 0 ? q0 : 0) + part; l < j; l += BK_PARTS)
+        s += Ts[k * BK_TSTR + l] * Ss[l * BK_TSTR + j];
+    }
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    if (part == 0 && k <= j) Ts[k * BK_TSTR + j] = (k < j) ? -bs[j] * s : bs[j];
+    __syncthreads();
+  }
+  float *T = p.T + bz * p.sT;
+  for (int e = t; e < NB * NB; e += BK_THREADS)
+    T[e] = bad ? nan : Ts[(e / NB) * BK_TSTR + e % NB];
+}
+
 // Final triangular factor: entries of an earlier outer block than their column
 // come from At, entries inside an outer block were stored by the panels; every
 // row i is then scaled by d_i so that diag(R) >= 0.  Strict lower part = 0.
@@ -532,7 +886,8 @@ __global__ __launch_bounds__(256) void transpose_kernel(float *dst, const float 
 // ------------------------------------------------------------ host driver
 struct QrLayout {
   int64_t n, nob;
-  size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, total;
+  bool block;          // outer blocks factored by qr_block_kernel (else the panel path)
+  size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, x_off, total;
   int64_t sT, sWbuf, sSk, sPart, sWi;
 };
 
@@ -560,6 +915,13 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.d_off = o;    o = align256(o + sizeof(float) * batch * n);
   L.b_off = o;    o = align256(o + sizeof(float) * batch * n);
   L.cnt_off = o;  o = align256(o + sizeof(unsigned) * batch);
+  // The resident-block path needs every workgroup of a launch resident at
+  // once: at most BK_MAX_WG workgroups (two such launches, one per factor,
+  // may run together on the 256 compute units).
+  const int64_t P0 = (n + BK_ROWS - 1) / BK_ROWS;
+  L.block = P0 <= BK_MAX_P && P0 * batch <= BK_MAX_WG;
+  L.x_off = o;
+  if (L.block) o = align256(o + sizeof(unsigned long long) * batch * BK_XSTRIDE);
   L.total = o;
   return L;
 }
@@ -594,115 +956,209 @@ hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t
     if (e_ != hipSuccess) return e_;        \
   } while (0)
 
+namespace {
+
+// Event pool for the fork/join of the look-ahead, one per host thread.  An
+// event is re-recorded only after the waits on its previous record have
+// been enqueued (waits capture the record current at the time of the call),
+// and the cursor cycles through many events before any reuse.
+struct EventPool {
+  std::vector<hipEvent_t> ev;
+  size_t next = 0;
+  hipError_t get(hipEvent_t *out) {
+    constexpr size_t CAP = 4096;
+    if (ev.size() < CAP && next >= ev.size()) {
+      hipEvent_t e = nullptr;
+      hipError_t err = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+      if (err != hipSuccess) return err;
+      ev.push_back(e);
+    }
+    *out = ev[next % ev.size()];
+    next = (next + 1) % CAP;
+    return hipSuccess;
+  }
+};
+
+thread_local EventPool t_events;
+
+struct QrCtx {
+  float *At, *Q, *Rf;
+  int64_t batch, n, sA;
+  int ni;
+  QrLayout L;
+  float *Tb, *Wb, *W2, *Sk, *Pt, *Wi, *dsign, *betas;
+  unsigned *cnt;
+  unsigned long long *xch;
+};
+
+hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
+
+// Factors outer block ob on stream s (resident-block kernel or panel path).
+hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
+  if (!x.L.block) return panel_phase(x, ob, s);
+  const int c = (int)(ob * NB);
+  const int nb = (int)std::min<int64_t>(NB, x.n - c);
+  const int P = (int)((x.n - c + BK_ROWS - 1) / BK_ROWS);
+  BlockParams bp{x.At, x.sA, x.ni, c, nb, x.Tb + ob * NB * NB, x.L.sT, x.Rf, x.dsign, x.betas,
+                 x.xch, P};
+  hipLaunchKernelGGL((qr_block_kernel<BK_R>), dim3((unsigned)P, (unsigned)x.batch),
+                     dim3(BK_THREADS), 0, s, bp);
+  return hipGetLastError();
+}
+
+// Factors the columns of outer block ob (inner panels, their row-parallel
+// reductions and applies) on stream s.
+hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s) {
+  const int n = x.ni;
+  const int c = (int)(ob * NB);
+  const int cend = (int)std::min<int64_t>(x.n, c + NB);
+  float *Tob = x.Tb + ob * NB * NB;
+  for (int ci = c; ci < cend;) {
+    const int64_t rows = x.n - ci;
+    const int B = panel_width(rows);
+    const int beff = std::min(B, cend - ci);
+    PanelParams pp{x.At, x.sA, n, c, ci, beff, Tob, x.L.sT, x.Rf, x.dsign, x.betas};
+    switch (B) {
+      case 16: SOAP_TRY((launch_panel<16, 8>(pp, x.batch, s))); break;
+      case 8: SOAP_TRY((launch_panel<8, 16>(pp, x.batch, s))); break;
+      default: SOAP_TRY((launch_panel<4, 32>(pp, x.batch, s))); break;
+    }
+    const int w = cend - (ci + beff);
+    {
+      const int P = (int)((rows + RCH - 1) / RCH);
+      InnerParams ip{x.At, x.sA, n, c, ci, beff, cend, Tob, x.L.sT, x.betas, x.Wi, x.L.sWi, x.Pt,
+                     x.L.sPart, x.cnt, P};
+      hipLaunchKernelGGL(qr_inner_reduce_kernel, dim3(P, (unsigned)x.batch), dim3(RED_THREADS), 0,
+                         s, ip);
+      SOAP_TRY(hipGetLastError());
+    }
+    if (w > 0) {
+      ApplyParams ap{x.At, x.sA, n, ci, beff, w, x.Wi, x.L.sWi};
+      const unsigned gx = (unsigned)((rows + 255) / 256);
+      hipLaunchKernelGGL(qr_inner_apply_kernel, dim3(gx, (unsigned)x.batch), dim3(256), 0, s, ap);
+      SOAP_TRY(hipGetLastError());
+    }
+    ci += beff;
+  }
+  return hipSuccess;
+}
+
+// Applies outer block ob's reflectors to the columns [j0, j1) of A (rows c..n):
+// A[c:, j0:j1] -= Y (T^T (Y^T A[c:, j0:j1])), on stream s.
+hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, hipStream_t s) {
+  const int64_t n = x.n;
+  const int64_t c = ob * NB;
+  const int64_t nb = std::min<int64_t>(n, c + NB) - c, Kr = n - c, Nt = j1 - j0;
+  if (Nt <= 0) return hipSuccess;
+  float *Tob = x.Tb + ob * NB * NB;
+  // W = Y^T A[c:n, j0:j1]:  W[i][j] = sum_k At[c+i][c+k] At[j0+j][c+k]
+  GemmDesc g1;
+  g1.trans_a = 0; g1.trans_b = 1; g1.M = nb; g1.N = Nt; g1.K = Kr;
+  g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
+  g1.B = x.At + j0 * n + c; g1.ldb = n; g1.sB = x.sA;
+  g1.C = x.Wb; g1.ldc = Nt; g1.sC = x.L.sWbuf; g1.batch = x.batch;
+  g1.splitk = choose_splitk(nb, Nt, Kr, x.batch, MAX_SPLIT);
+  g1.part = x.Sk;
+  SOAP_TRY(launch_gemm(g1, s));
+  // W2 = T^T W
+  GemmDesc g2;
+  g2.trans_a = 1; g2.trans_b = 0; g2.M = nb; g2.N = Nt; g2.K = nb;
+  g2.A = Tob; g2.lda = NB; g2.sA = x.L.sT;
+  g2.B = x.Wb; g2.ldb = Nt; g2.sB = x.L.sWbuf;
+  g2.C = x.W2; g2.ldc = Nt; g2.sC = x.L.sWbuf; g2.batch = x.batch;
+  SOAP_TRY(launch_gemm(g2, s));
+  // At[j0+j][c+k] -= sum_i W2[i][j] Y[k][i]
+  GemmDesc g3;
+  g3.trans_a = 1; g3.trans_b = 0; g3.M = Nt; g3.N = Kr; g3.K = nb;
+  g3.A = x.W2; g3.lda = Nt; g3.sA = x.L.sWbuf;
+  g3.B = x.At + c * n + c; g3.ldb = n; g3.sB = x.sA;
+  g3.C = x.At + j0 * n + c; g3.ldc = n; g3.sC = x.sA;
+  g3.alpha = -1.f; g3.beta = 1.f; g3.batch = x.batch;
+  return launch_gemm(g3, s);
+}
+
+}  // namespace
+
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
-                                void *ws, size_t ws_bytes, hipStream_t s) {
-  const QrLayout L = qr_layout(batch, n);
-  if (ws_bytes < L.total) return hipErrorInvalidValue;
+                                void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp) {
+  QrCtx x;
+  x.L = qr_layout(batch, n);
+  if (ws_bytes < x.L.total) return hipErrorInvalidValue;
   char *base = static_cast<char *>(ws);
-  float *Tb = reinterpret_cast<float *>(base + L.t_off);
-  float *Wb = reinterpret_cast<float *>(base + L.w_off);
-  float *W2 = reinterpret_cast<float *>(base + L.w2_off);
-  float *Sk = reinterpret_cast<float *>(base + L.sk_off);
-  float *Pt = reinterpret_cast<float *>(base + L.part_off);
-  float *Wi = reinterpret_cast<float *>(base + L.wi_off);
-  float *dsign = reinterpret_cast<float *>(base + L.d_off);
-  float *betas = reinterpret_cast<float *>(base + L.b_off);
-  unsigned *cnt = reinterpret_cast<unsigned *>(base + L.cnt_off);
-  const int64_t sA = n * n;
-  const int ni = (int)n;
+  x.At = At; x.Q = Q; x.Rf = Rf; x.batch = batch; x.n = n; x.sA = n * n; x.ni = (int)n;
+  x.Tb = reinterpret_cast<float *>(base + x.L.t_off);
+  x.Wb = reinterpret_cast<float *>(base + x.L.w_off);
+  x.W2 = reinterpret_cast<float *>(base + x.L.w2_off);
+  x.Sk = reinterpret_cast<float *>(base + x.L.sk_off);
+  x.Pt = reinterpret_cast<float *>(base + x.L.part_off);
+  x.Wi = reinterpret_cast<float *>(base + x.L.wi_off);
+  x.dsign = reinterpret_cast<float *>(base + x.L.d_off);
+  x.betas = reinterpret_cast<float *>(base + x.L.b_off);
+  x.cnt = reinterpret_cast<unsigned *>(base + x.L.cnt_off);
+  x.xch = reinterpret_cast<unsigned long long *>(base + x.L.x_off);
+  const int64_t nob = x.L.nob;
 
-  SOAP_TRY(launch_zero_u32(cnt, batch, s));
+  SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
+  if (x.L.block)   // generations restart at 1 every call: clear the old items
+    SOAP_TRY(launch_zero_u32(reinterpret_cast<uint32_t *>(x.xch), 2 * batch * BK_XSTRIDE, s));
 
-  for (int64_t ob = 0; ob < L.nob; ++ob) {
-    const int c = (int)(ob * NB);
-    const int cend = (int)std::min<int64_t>(n, c + NB);
-    float *Tob = Tb + ob * NB * NB;
-    for (int ci = c; ci < cend;) {
-      const int64_t rows = n - ci;
-      const int B = panel_width(rows);
-      const int beff = std::min(B, cend - ci);
-      PanelParams pp{At, sA, ni, c, ci, beff, Tob, L.sT, Rf, dsign, betas};
-      switch (B) {
-        case 16: SOAP_TRY((launch_panel<16, 8>(pp, batch, s))); break;
-        case 8: SOAP_TRY((launch_panel<8, 16>(pp, batch, s))); break;
-        default: SOAP_TRY((launch_panel<4, 32>(pp, batch, s))); break;
-      }
-      const int w = cend - (ci + beff);
-      {
-        const int P = (int)((rows + RCH - 1) / RCH);
-        InnerParams ip{At, sA, ni, c, ci, beff, cend, Tob, L.sT, betas, Wi, L.sWi, Pt, L.sPart,
-                       cnt, P};
-        hipLaunchKernelGGL(qr_inner_reduce_kernel, dim3(P, (unsigned)batch), dim3(RED_THREADS), 0,
-                           s, ip);
-        SOAP_TRY(hipGetLastError());
-      }
-      if (w > 0) {
-        ApplyParams ap{At, sA, ni, ci, beff, w, Wi, L.sWi};
-        const unsigned gx = (unsigned)((rows + 255) / 256);
-        hipLaunchKernelGGL(qr_inner_apply_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, ap);
-        SOAP_TRY(hipGetLastError());
-      }
-      ci += beff;
-    }
-    if (cend < n) {
-      const int64_t nb = cend - c, Nt = n - cend, Kr = n - c;
-      // W = Y^T A[c:n, cend:n]:  W[i][j] = sum_k At[c+i][c+k] At[cend+j][c+k]
-      GemmDesc g1;
-      g1.trans_a = 0; g1.trans_b = 1; g1.M = nb; g1.N = Nt; g1.K = Kr;
-      g1.A = At + (int64_t)c * n + c; g1.lda = n; g1.sA = sA;
-      g1.B = At + (int64_t)cend * n + c; g1.ldb = n; g1.sB = sA;
-      g1.C = Wb; g1.ldc = Nt; g1.sC = L.sWbuf; g1.batch = batch;
-      g1.splitk = choose_splitk(nb, Nt, Kr, batch, MAX_SPLIT);
-      g1.part = Sk;
-      SOAP_TRY(launch_gemm(g1, s));
-      // W2 = T^T W
-      GemmDesc g2;
-      g2.trans_a = 1; g2.trans_b = 0; g2.M = nb; g2.N = Nt; g2.K = nb;
-      g2.A = Tob; g2.lda = NB; g2.sA = L.sT;
-      g2.B = Wb; g2.ldb = Nt; g2.sB = L.sWbuf;
-      g2.C = W2; g2.ldc = Nt; g2.sC = L.sWbuf; g2.batch = batch;
-      SOAP_TRY(launch_gemm(g2, s));
-      // A[c:n, cend:n] -= Y W2, i.e.  At[cend+j][c+k] -= sum_i W2[i][j] Y[k][i]
-      GemmDesc g3;
-      g3.trans_a = 1; g3.trans_b = 0; g3.M = Nt; g3.N = Kr; g3.K = nb;
-      g3.A = W2; g3.lda = Nt; g3.sA = L.sWbuf;
-      g3.B = At + (int64_t)c * n + c; g3.ldb = n; g3.sB = sA;
-      g3.C = At + (int64_t)cend * n + c; g3.ldc = n; g3.sC = sA;
-      g3.alpha = -1.f; g3.beta = 1.f; g3.batch = batch;
-      SOAP_TRY(launch_gemm(g3, s));
-    }
+  // Look-ahead: block ob+1's columns are updated first (the "near" update),
+  // then block ob+1 is factored on the panel stream while this stream applies
+  // the rest of block ob's trailing update.
+  hipEvent_t ev;
+  SOAP_TRY(t_events.get(&ev));
+  SOAP_TRY(hipEventRecord(ev, s));
+  SOAP_TRY(hipStreamWaitEvent(sp, ev, 0));
+  SOAP_TRY(factor_block(x, 0, sp));
+  SOAP_TRY(t_events.get(&ev));
+  SOAP_TRY(hipEventRecord(ev, sp));
+  SOAP_TRY(hipStreamWaitEvent(s, ev, 0));        // block 0 factored
+  for (int64_t ob = 0; ob < nob; ++ob) {
+    const int64_t cend = std::min<int64_t>(n, (ob + 1) * NB);
+    if (cend >= n) break;
+    const int64_t cend2 = std::min<int64_t>(n, cend + NB);
+    SOAP_TRY(trailing_update(x, ob, cend, cend2, s));          // near: block ob+1
+    SOAP_TRY(t_events.get(&ev));
+    SOAP_TRY(hipEventRecord(ev, s));
+    SOAP_TRY(hipStreamWaitEvent(sp, ev, 0));
+    SOAP_TRY(factor_block(x, ob + 1, sp));                      // factor block ob+1
+    hipEvent_t ev_panel;
+    SOAP_TRY(t_events.get(&ev_panel));
+    SOAP_TRY(hipEventRecord(ev_panel, sp));
+    SOAP_TRY(trailing_update(x, ob, cend2, n, s));              // far: the rest
+    SOAP_TRY(hipStreamWaitEvent(s, ev_panel, 0));               // block ob+1 factored
   }
 
   // Explicit Q (row-major), accumulated backwards from diag(d).
   {
     const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
-    hipLaunchKernelGGL(qr_init_q_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, Q, dsign,
-                       ni, sA);
+    hipLaunchKernelGGL(qr_init_q_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, Q, x.dsign,
+                       x.ni, x.sA);
     SOAP_TRY(hipGetLastError());
   }
-  for (int64_t ob = L.nob - 1; ob >= 0; --ob) {
-    const int c = (int)(ob * NB);
+  for (int64_t ob = nob - 1; ob >= 0; --ob) {
+    const int64_t c = ob * NB;
     const int64_t nb = std::min<int64_t>(n, c + NB) - c, Kr = n - c;
-    float *Tob = Tb + ob * NB * NB;
+    float *Tob = x.Tb + ob * NB * NB;
     GemmDesc g1;  // W = Y^T Q[c:n, c:n]:  op(A)[i][k] = Y[k][i] = At[c+i][c+k]
     g1.trans_a = 0; g1.trans_b = 0; g1.M = nb; g1.N = Kr; g1.K = Kr;
-    g1.A = At + (int64_t)c * n + c; g1.lda = n; g1.sA = sA;
-    g1.B = Q + (int64_t)c * n + c; g1.ldb = n; g1.sB = sA;
-    g1.C = Wb; g1.ldc = Kr; g1.sC = L.sWbuf; g1.batch = batch;
+    g1.A = At + c * n + c; g1.lda = n; g1.sA = x.sA;
+    g1.B = Q + c * n + c; g1.ldb = n; g1.sB = x.sA;
+    g1.C = x.Wb; g1.ldc = Kr; g1.sC = x.L.sWbuf; g1.batch = batch;
     g1.splitk = choose_splitk(nb, Kr, Kr, batch, MAX_SPLIT);
-    g1.part = Sk;
+    g1.part = x.Sk;
     SOAP_TRY(launch_gemm(g1, s));
     GemmDesc g2;  // W2 = T W
     g2.trans_a = 0; g2.trans_b = 0; g2.M = nb; g2.N = Kr; g2.K = nb;
-    g2.A = Tob; g2.lda = NB; g2.sA = L.sT;
-    g2.B = Wb; g2.ldb = Kr; g2.sB = L.sWbuf;
-    g2.C = W2; g2.ldc = Kr; g2.sC = L.sWbuf; g2.batch = batch;
+    g2.A = Tob; g2.lda = NB; g2.sA = x.L.sT;
+    g2.B = x.Wb; g2.ldb = Kr; g2.sB = x.L.sWbuf;
+    g2.C = x.W2; g2.ldc = Kr; g2.sC = x.L.sWbuf; g2.batch = batch;
     SOAP_TRY(launch_gemm(g2, s));
     GemmDesc g3;  // Q[c:n, c:n] -= Y W2:  op(A)[k][i] = Y[k][i] = At[c+i][c+k]
     g3.trans_a = 1; g3.trans_b = 0; g3.M = Kr; g3.N = Kr; g3.K = nb;
-    g3.A = At + (int64_t)c * n + c; g3.lda = n; g3.sA = sA;
-    g3.B = W2; g3.ldb = Kr; g3.sB = L.sWbuf;
-    g3.C = Q + (int64_t)c * n + c; g3.ldc = n; g3.sC = sA;
+    g3.A = At + c * n + c; g3.lda = n; g3.sA = x.sA;
+    g3.B = x.W2; g3.ldb = Kr; g3.sB = x.L.sWbuf;
+    g3.C = Q + c * n + c; g3.ldc = n; g3.sC = x.sA;
     g3.alpha = -1.f; g3.beta = 1.f; g3.batch = batch;
     SOAP_TRY(launch_gemm(g3, s));
   }
@@ -711,7 +1167,7 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     const int64_t nn = n * n;
     const unsigned gx = (unsigned)std::min<int64_t>((nn + 255) / 256, 2048);
     hipLaunchKernelGGL(qr_extract_r_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, At, Rf,
-                       dsign, ni, sA);
+                       x.dsign, x.ni, x.sA);
     SOAP_TRY(hipGetLastError());
   }
   return hipSuccess;

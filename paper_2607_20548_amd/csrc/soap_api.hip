@@ -123,20 +123,23 @@ class StageScope {
 // chain are independent until the rotations; the L side runs on one
 // auxiliary stream per device (default priority, created on first use) and is
 // joined back with events, so its latency-bound QR panels overlap the R side.
+// Streams per device: 0 = L side, 1 = panels of the L-side QR, 2 = panels
+// of the R-side QR (look-ahead).
+constexpr int N_AUX = 3;
 std::mutex g_aux_mu;
-hipStream_t g_aux[64] = {};
+hipStream_t g_aux[64][N_AUX] = {};
 
-hipError_t aux_stream(hipStream_t *out) {
+hipError_t aux_stream(int which, hipStream_t *out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  if (dev < 0 || dev >= 64 || which < 0 || which >= N_AUX) return hipErrorInvalidDevice;
   std::lock_guard<std::mutex> g(g_aux_mu);
-  if (!g_aux[dev]) {
-    e = hipStreamCreateWithFlags(&g_aux[dev], hipStreamNonBlocking);
+  if (!g_aux[dev][which]) {
+    e = hipStreamCreateWithFlags(&g_aux[dev][which], hipStreamNonBlocking);
     if (e != hipSuccess) return e;
   }
-  *out = g_aux[dev];
+  *out = g_aux[dev][which];
   return hipSuccess;
 }
 
@@ -241,18 +244,20 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
       return hip_fail(e, "momentum");
   }
   // Fork: the L side on the auxiliary stream, the R side on the caller's.
-  hipStream_t sl = nullptr;
+  hipStream_t sl = nullptr, spl = nullptr, spr = nullptr;
   hipEvent_t ev_fork = nullptr, ev_join = nullptr;
-  if ((e = aux_stream(&sl)) != hipSuccess) return hip_fail(e, "auxiliary stream");
+  if ((e = aux_stream(0, &sl)) != hipSuccess || (e = aux_stream(1, &spl)) != hipSuccess ||
+      (e = aux_stream(2, &spr)) != hipSuccess)
+    return hip_fail(e, "auxiliary stream");
   if ((e = hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming)) != hipSuccess)
     return hip_fail(e, "event");
   if ((e = hipEventCreateWithFlags(&ev_join, hipEventDisableTiming)) != hipSuccess) {
-    hipEventDestroy(ev_fork);
+    (void)hipEventDestroy(ev_fork);
     return hip_fail(e, "event");
   }
   struct EventGuard {
     hipEvent_t a, b;
-    ~EventGuard() { hipEventDestroy(a); hipEventDestroy(b); }
+    ~EventGuard() { (void)hipEventDestroy(a); (void)hipEventDestroy(b); }
   } guard{ev_fork, ev_join};
   if ((e = hipEventRecord(ev_fork, s)) != hipSuccess) return hip_fail(e, "fork record");
   if ((e = hipStreamWaitEvent(sl, ev_fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
@@ -275,7 +280,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   }
   {  // Q_L = QR(A_L).Q
     StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
-    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl)) != hipSuccess)
+    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl)) != hipSuccess)
       return hip_fail(e, "QR L");
   }
   if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
@@ -297,7 +302,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   }
   {  // Q_R = QR(A_R).Q
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
-    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s)) != hipSuccess)
+    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr)) != hipSuccess)
       return hip_fail(e, "QR R");
   }  if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
   {  // T_G = Q_L^T G,  T_M = Q_L^T M
@@ -408,8 +413,13 @@ int soap_qr_f32(int64_t n, const float *A, float *Q, float *Rf, void *workspace,
   char *rest = static_cast<char *>(workspace) + align256(sizeof(float) * n * n);
   hipError_t e = soap::launch_transpose(Aw, A, n, stream);   // the QR factors A^T
   if (e == hipSuccess)
-    e = soap::qr_factor_and_form_q(Aw, Q, Rf, 1, n, rest, workspace_bytes - align256(sizeof(float) * n * n),
-                                   stream);
+  {
+    hipStream_t sp = nullptr;
+    if (e == hipSuccess) e = aux_stream(2, &sp);
+    if (e == hipSuccess)
+      e = soap::qr_factor_and_form_q(Aw, Q, Rf, 1, n, rest,
+                                     workspace_bytes - align256(sizeof(float) * n * n), stream, sp);
+  }
   if (e != hipSuccess) return hip_fail(e, "QR");
   return ok();
 }
