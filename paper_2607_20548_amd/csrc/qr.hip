@@ -486,35 +486,40 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
 // ------------------------------------------------ resident-block factorization
 // One launch factors a whole outer block (rows c..n-1, nb <= NB columns) with
 // the same reflectors as the panel path.  Workgroup g keeps rows
-// c + g*BK_ROWS .. c + (g+1)*BK_ROWS - 1 of the block in registers: thread t
-// owns column k = t/4 and, with part = t%4, the local rows 16 i + 4 part + e
-// (i < BK_R/4, e < 4).  Per column j:
+// c + g*BK_ROWS .. c + (g+1)*BK_ROWS - 1 of the block in registers: the four
+// lanes 4q..4q+3 of wave w own column k = 8q + w (so every wave keeps the
+// same number of active columns as the factorization advances) and lane part
+// holds the local rows 16 i + 4 part + e (i < BK_R/4, e < 4).  Per column j:
 //   * the pivot column is broadcast through LDS and every thread forms the
 //     partial dot of its column with the pivot below the diagonal row;
 //   * the partials are summed grid-wide in two hops through global memory.
 //     Every value travels as a 64-bit item (value bits | generation << 32)
 //     written and read with agent-scope atomics, so a reader recognises a
 //     fresh value by its generation (global column index + 1) and needs no
-//     barrier or flag: each workgroup posts its partial of every column; the
-//     owner of column k (workgroup 1 + k mod (P-1)) sums the P partials in
-//     workgroup order, reads the diagonal-row value from workgroup 0, and
-//     forwards both into a private copy for every workgroup (so that no
-//     cache line is polled by more than one workgroup); every workgroup reads
-//     the totals it needs from its copy, so all of them apply bit-identical
-//     reflectors.  Items are double-buffered by column parity: no workgroup
-//     can get two columns ahead of a reader;
+//     barrier or flag: each workgroup posts its partials of all columns (one
+//     contiguous row of items); one wave of the owner of each chunk of 8
+//     columns (workgroup 1 + chunk mod (P-1)) sums the P partials of each of
+//     its columns in a fixed order, reads the diagonal-row values from
+//     workgroup 0, and forwards both into a private copy for every workgroup
+//     (so that no cache line is polled by more than one workgroup); every
+//     workgroup reads the totals it needs from its copy, so all of them apply
+//     bit-identical reflectors.  Items are double-buffered by column parity:
+//     no workgroup can get two columns ahead of a reader;
 //   * every thread updates its own column.
 // Workgroup 0 holds the block's diagonal rows: its pivot broadcast is zero at
 // and above the diagonal row (so its dot products need no masks), it posts
 // the diagonal-row values, and it keeps S = strict upper part of Y^T Y,
 //   S[l][j] = y_l^T v_j = A_l + D_l / v0_j  (from the same dot products),
-// from which it forms T after the column loop:
-//   T[0:j, j] = -beta_j T[0:j, 0:j] S[0:j, j],  T[j][j] = beta_j.
+// from which it forms T after the column loop,
+//   T[k][k] = beta_k,  T[k][j] = -beta_j sum_{l=k}^{j-1} T[k][l] S[l][j]  (j > k),
+// by blocks of 8 columns (the diagonal blocks by this recurrence, the others
+// by T_IJ = -(sum_{K=I}^{J-1} T_IK S_KJ) T_JJ).
 // The launch needs all of its workgroups resident at once; the host limits it
 // to BK_MAX_WG workgroups.  Waits are bounded: one that exceeds BK_SPIN_LIMIT
 // polls raises a per-matrix abort flag, after which every wait returns at
 // once and the block is written as NaN, so the kernel always ends.
 constexpr int BK_THREADS = 512;
+constexpr int BK_WAVES = BK_THREADS / 64;
 constexpr int BK_PARTS = 4;                     // threads per column
 constexpr int BK_R = 64;                        // rows per thread
 constexpr int BK_ROWS = BK_PARTS * BK_R;        // rows per workgroup
@@ -523,7 +528,7 @@ constexpr int BK_MAX_P = BK_PARTS * BK_MAX_ITEMS;   // workgroups per matrix (n 
 constexpr int BK_MAX_WG = 96;                   // workgroups per launch
 constexpr unsigned BK_SPIN_LIMIT = 1u << 22;
 constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (spreads banks)
-// exchange area per matrix, in 64-bit items: partials [2][NB][BK_MAX_P],
+// exchange area per matrix, in 64-bit items: partials [2][BK_MAX_P][NB],
 // diagonal-row values of workgroup 0 [2][NB], per-reader copies of
 // (total, diagonal-row value) [BK_MAX_P][2][NB][2] (4 KiB per reader), abort flag
 constexpr int64_t BK_XD = 0;
@@ -572,11 +577,11 @@ __device__ __forceinline__ bool bk_give_up(unsigned &spins, unsigned *abort_flag
   return false;
 }
 
-// Owner hop: waits for generation `gen` of the partials p[0], p[4], ...,
-// p[4 (cnt-1)] (re-reading only those not yet current) and returns their sum
-// in order.  false: aborted.
-__device__ __forceinline__ bool bk_sum_partials(const unsigned long long *p, int cnt, unsigned gen,
-                                                unsigned *abort_flag, float &sum) {
+// Owner hop: waits for generation `gen` of the partials p[0], p[stride], ...,
+// p[stride (cnt-1)] (re-reading only those not yet current) and returns their
+// sum in order.  false: aborted.
+__device__ __forceinline__ bool bk_sum_partials(const unsigned long long *p, int stride, int cnt,
+                                                unsigned gen, unsigned *abort_flag, float &sum) {
   float v[BK_MAX_ITEMS];
   unsigned pending = (cnt >= 32) ? ~0u : ((1u << cnt) - 1u);
   unsigned spins = 0;
@@ -584,7 +589,7 @@ __device__ __forceinline__ bool bk_sum_partials(const unsigned long long *p, int
 #pragma unroll
     for (int u = 0; u < BK_MAX_ITEMS; ++u)
       if (pending & (1u << u)) {
-        const unsigned long long it = bk_get(p + BK_PARTS * u);
+        const unsigned long long it = bk_get(p + (int64_t)stride * u);
         v[u] = __uint_as_float((unsigned)it);
         if ((unsigned)(it >> 32) == gen) pending &= ~(1u << u);
       }
@@ -637,14 +642,14 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
 
   const int g = blockIdx.x;
   const int64_t bz = blockIdx.y;
-  const int t = threadIdx.x, k = t >> 2, part = t & 3;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, part = t & 3;
+  const int k = 8 * (lane >> 2) + wave;
   const int n = p.n, c = p.c, nb = p.nb, P = p.P;
   const unsigned un = (unsigned)n;     // n*n < 2^31
   float *At = p.At + bz * p.sA;
   const int r0 = c + g * RS;
   const bool w0 = (g == 0);
   const bool col = k < nb;
-  const bool owner = P > 1 && col && 1 + k % (P - 1) == g;
   unsigned long long *X = p.xch + bz * BK_XSTRIDE;
   unsigned *abort_flag = reinterpret_cast<unsigned *>(X + BK_XABORT);
 
@@ -660,6 +665,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       }
   }
   bool alive = true;
+  const int nchunk = (nb + 7) / 8;
 
   for (int j = 0; j < nb; ++j) {
     const int par = j & 1;
@@ -696,24 +702,32 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
     av += __shfl_xor(av, 2);
     float D = d, A = av;
     if (P > 1) {
-      unsigned long long *xd = X + BK_XD + ((int64_t)par * NB + k) * BK_MAX_P;
-      unsigned long long *xa = X + BK_XA + par * NB + k;
-      const int lead = (t & 63) & ~3;          // lane of part 0 of this column
-      if (col && part == 0) bk_put(xd + g, d, gen);
-      if (w0 && col && part == 1) bk_put(xa, av, gen);
-      if (owner) {                             // owner hop
+      unsigned long long *xa = X + BK_XA + par * NB;
+      const int lead = lane & ~3;              // lane of part 0 of this column
+      if (col && part == 0) bk_put(X + BK_XD + ((int64_t)par * BK_MAX_P + g) * NB + k, d, gen);
+      if (w0 && col && part == 1) bk_put(xa + k, av, gen);
+      // owner hop: chunk ch (columns 8ch..8ch+7) belongs to one wave of
+      // workgroup 1 + ch mod (P-1); lane (u, c8) sums the partials of
+      // workgroups u, u+8, ... of column 8ch+c8, then the wave adds across u.
+      // (wave w of workgroup g >= 1 owns chunks g-1 + (P-1)(w + 8m), m >= 0)
+      for (int ch = g - 1 + (P - 1) * wave; g > 0 && ch < nchunk; ch += (P - 1) * BK_WAVES) {
+        const int c8 = lane & 7, u = lane >> 3, kc = 8 * ch + c8;
         float s = 0.f, aval = 0.f, unused = 0.f;
-        const int cnt = (P - part + BK_PARTS - 1) / BK_PARTS;
-        if (alive) alive = bk_sum_partials(xd + part, cnt, gen, abort_flag, s);
-        s += __shfl_xor(s, 1);
-        s += __shfl_xor(s, 2);
-        if (part == 0 && alive) alive = bk_read2(xa, nullptr, gen, abort_flag, aval, unused);
-        aval = __shfl(aval, lead);
-        for (int r = part; r < P; r += BK_PARTS) {
-          unsigned long long *cp = X + BK_XC + (((int64_t)r * 2 + par) * NB + k) * 2;
-          bk_put(cp, s, gen);
-          bk_put(cp + 1, aval, gen);
-        }
+        const int cnt = (P - u + 7) / 8;
+        if (kc < nb && alive)
+          alive = bk_sum_partials(X + BK_XD + ((int64_t)par * BK_MAX_P + u) * NB + kc, 8 * NB, cnt,
+                                  gen, abort_flag, s);
+        s += __shfl_xor(s, 8);
+        s += __shfl_xor(s, 16);
+        s += __shfl_xor(s, 32);
+        if (kc < nb && u == 0 && alive) alive = bk_read2(xa + kc, nullptr, gen, abort_flag, aval, unused);
+        aval = __shfl(aval, c8);
+        if (kc < nb)
+          for (int r = u; r < P; r += 8) {
+            unsigned long long *cp = X + BK_XC + (((int64_t)r * 2 + par) * NB + kc) * 2;
+            bk_put(cp, s, gen);
+            bk_put(cp + 1, aval, gen);
+          }
       }
       if (col && (w0 || k >= j)) {             // reader hop (one lane per column)
         const unsigned long long *cp = X + BK_XC + (((int64_t)g * 2 + par) * NB + k) * 2;
@@ -816,21 +830,66 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       }
   }
   if (!w0) return;
-  // T by columns: thread (k, part) sums T[k][l] S[l][j] over l = 4q + part.
+  // T by blocks of 8 columns: first every diagonal block T_JJ (rows of one
+  // block are independent recurrences of at most 8 steps), then, row by row,
+  //   T_IJ = -(sum_{K=I}^{J-1} T_IK S_KJ) T_JJ  for J > I.
+  // Row k belongs to the four lanes of column k; they exchange values only
+  // through shuffles and their own row of Ts, so no barrier is needed after
+  // the diagonal blocks.
   for (int e = t; e < NB * BK_TSTR; e += BK_THREADS) Ts[e] = 0.f;
   __syncthreads();
-  for (int j = 0; j < nb; ++j) {
-    float s = 0.f;
-    if (k < j) {
-      const int q0 = (k - part + BK_PARTS - 1) / BK_PARTS;   // first l = 4q + part >= k
-      for (int l = BK_PARTS * (q0 > 0 ? q0 : 0) + part; l < j; l += BK_PARTS)
-        s += Ts[k * BK_TSTR + l] * Ss[l * BK_TSTR + j];
+  float *trow = Ts + k * BK_TSTR;
+  const int J0 = k >> 3;
+  if (col) {
+    const int jend = min(nb, 8 * J0 + 8);
+    for (int j = k; j < jend; ++j) {
+      float s = 0.f;
+      for (int l = k + part; l < j; l += BK_PARTS) s += trow[l] * Ss[l * BK_TSTR + j];
+      s += __shfl_xor(s, 1);
+      s += __shfl_xor(s, 2);
+      __builtin_amdgcn_wave_barrier();
+      if (part == 0) trow[j] = (j == k) ? bs[j] : -bs[j] * s;
+      __builtin_amdgcn_wave_barrier();
     }
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
-    if (part == 0 && k <= j) Ts[k * BK_TSTR + j] = (k < j) ? -bs[j] * s : bs[j];
-    __syncthreads();
   }
+  __syncthreads();
+  if (col) {
+    const int lead = lane & ~3;
+    for (int J = J0 + 1; 8 * J < nb; ++J) {
+      // X[c] = sum_{l=k}^{8J-1} T[k][l] S[l][8J+c]; lane part forms c = part, part+4
+      const int c0 = 8 * J + part, c1 = c0 + 4;
+      float x0a = 0.f, x0b = 0.f, x1a = 0.f, x1b = 0.f;
+      int l = k;
+      for (; l + 1 < 8 * J; l += 2) {
+        const float t0 = trow[l], t1 = trow[l + 1];
+        x0a += t0 * Ss[l * BK_TSTR + c0];
+        x1a += t0 * Ss[l * BK_TSTR + c1];
+        x0b += t1 * Ss[(l + 1) * BK_TSTR + c0];
+        x1b += t1 * Ss[(l + 1) * BK_TSTR + c1];
+      }
+      if (l < 8 * J) {
+        const float t0 = trow[l];
+        x0a += t0 * Ss[l * BK_TSTR + c0];
+        x1a += t0 * Ss[l * BK_TSTR + c1];
+      }
+      // columns past nb of S were never written: keep them out of X
+      const float xa = (c0 < nb) ? x0a + x0b : 0.f, xb = (c1 < nb) ? x1a + x1b : 0.f;
+      // T[k][8J+q] = -sum_c X[c] T_JJ[c][q],  X[c] from lane lead + (c & 3)
+      float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) {
+        const float xc = __shfl((cc < 4) ? xa : xb, lead + (cc & 3));
+        const float *tjj = Ts + (8 * J + cc) * BK_TSTR + 8 * J;
+        r0 += xc * tjj[part];
+        r1 += xc * tjj[part + 4];
+      }
+      __builtin_amdgcn_wave_barrier();
+      if (c0 < nb) trow[c0] = -r0;
+      if (c1 < nb) trow[c1] = -r1;
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  __syncthreads();
   float *T = p.T + bz * p.sT;
   for (int e = t; e < NB * NB; e += BK_THREADS)
     T[e] = bad ? nan : Ts[(e / NB) * BK_TSTR + e % NB];
