@@ -30,6 +30,7 @@ constexpr int BK = 16;
 constexpr int LDSK = BK + 4;            // padded LDS row stride in floats
 constexpr int TILE_FLOATS = 128 * LDSK;  // one operand tile in LDS
 constexpr int NTHREADS = 256;
+constexpr int SHORT_K = 512;    // products with at most this much K per slice use the rank-k kernel
 constexpr int GROUP_M = 8;
 
 enum { MODE_GENERAL = 0, MODE_SYRK = 1, MODE_ADAM = 2 };
@@ -154,8 +155,13 @@ __device__ __forceinline__ void tile_coords(const KParams &p, int &tm, int &tn) 
   }
 }
 
-template <int TA, int TB, int VEC, int MODE, int TAG>
-__global__ __launch_bounds__(NTHREADS) void gemm_f32_mfma(KParams p) {
+// MINB > 1 marks the short-K variant (K per slice <= SHORT_K, the QR's
+// rank-k updates): the bound on resident workgroups makes the compiler keep
+// the accumulators in VGPRs (4 workgroups per CU), and the epilogue batches
+// its reads of C.  Long-K products (MINB = 1) keep the accumulators in AGPRs.
+template <int TA, int TB, int VEC, int MODE, int TAG, int MINB>
+__global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
+  constexpr bool SHORTK = MINB > 1;
   constexpr int NA = (MODE == MODE_ADAM) ? 2 : 1;
   __shared__ __attribute__((aligned(16))) float lds[2 * (NA + 1) * TILE_FLOATS];
 
@@ -239,36 +245,72 @@ __global__ __launch_bounds__(NTHREADS) void gemm_f32_mfma(KParams p) {
   float *P = p.part ? p.part + (bz * gridDim.y + blockIdx.y) * (int64_t)p.M * p.N : nullptr;
   float *V = (MODE == MODE_ADAM) ? p.V + bz * p.sC : nullptr;
   float *Nout = (MODE == MODE_ADAM) ? p.Nout + bz * p.sC : nullptr;
+  // Short-K products (rank-k updates) spend a large share of their time
+  // here, so their C values are loaded 16 at a time before any store (the
+  // compiler cannot move a load of C above a store to C, and reading one
+  // element after storing the previous one serializes 64 memory latencies).
+  // Long-K products keep the register-lean element-by-element form.
+  if constexpr (SHORTK) {
+    const bool read_back = !P && p.beta != 0.f;
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int col = n0 + wn * 64 + j * 32 + xl;
+      for (int j = 0; j < 2; ++j) {
+        const int col = n0 + wn * 64 + j * 32 + xl;
+        float cv[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-        if (row >= p.M || col >= p.N) continue;
-        const int64_t off = (int64_t)row * p.ldc + col;
-        if (MODE == MODE_GENERAL && P) {
-          P[(int64_t)row * p.N + col] = acc[0][i][j][r];
-        } else if (MODE == MODE_GENERAL) {
-          float v = p.alpha * acc[0][i][j][r];
-          if (p.beta != 0.f) v += p.beta * C[off];
-          C[off] = v;
-        } else if (MODE == MODE_SYRK) {
-          if (row < col) continue;  // the mirror of (col,row) is written by its owner
-          const float v = p.beta * C[off] + p.alpha * acc[0][i][j][r];
-          C[off] = v;
-          if (row != col) C[(int64_t)col * p.ldc + row] = v;
-        } else {
-          const float g = acc[0][i][j][r];
-          const float mm = acc[1][i][j][r];
-          const float v = p.b2 * V[off] + (1.f - p.b2) * g * g;
-          V[off] = v;
-          Nout[off] = (mm / p.c1) / (sqrtf(v / p.c2) + p.eps);
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          const int64_t off = (int64_t)row * p.ldc + col;
+          cv[r] = 0.f;
+          if (read_back && row < p.M && col < p.N) cv[r] = C[off];
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (row >= p.M || col >= p.N) continue;
+          const int64_t off = (int64_t)row * p.ldc + col;
+          if (P) {
+            P[(int64_t)row * p.N + col] = acc[0][i][j][r];
+          } else {
+            float v = p.alpha * acc[0][i][j][r];
+            if (p.beta != 0.f) v += p.beta * cv[r];
+            C[off] = v;
+          }
         }
       }
-    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int col = n0 + wn * 64 + j * 32 + xl;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+          if (row >= p.M || col >= p.N) continue;
+          const int64_t off = (int64_t)row * p.ldc + col;
+          if (MODE == MODE_GENERAL && P) {
+            P[(int64_t)row * p.N + col] = acc[0][i][j][r];
+          } else if (MODE == MODE_GENERAL) {
+            float v = p.alpha * acc[0][i][j][r];
+            if (p.beta != 0.f) v += p.beta * C[off];
+            C[off] = v;
+          } else if (MODE == MODE_SYRK) {
+            if (row < col) continue;  // the mirror of (col,row) is written by its owner
+            const float v = p.beta * C[off] + p.alpha * acc[0][i][j][r];
+            C[off] = v;
+            if (row != col) C[(int64_t)col * p.ldc + row] = v;
+          } else {
+            const float g = acc[0][i][j][r];
+            const float mm = acc[1][i][j][r];
+            const float v = p.b2 * V[off] + (1.f - p.b2) * g * g;
+            V[off] = v;
+            Nout[off] = (mm / p.c1) / (sqrtf(v / p.c2) + p.eps);
+          }
+        }
+      }
+  }
 }
 
 // C = alpha * sum_s part[s] + beta * C, slices summed in index order.
@@ -297,12 +339,31 @@ hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) 
   const int S = (MODE == MODE_GENERAL && d.splitk > 1 && d.part) ? d.splitk : 1;
   dim3 grid(kp.ntiles, S, (unsigned)d.batch);
 #define SOAP_LAUNCH(TA, TB, VEC, TAG) \
-  hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE, TAG>), grid, block, 0, s, kp)
+  hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE, TAG, 1>), grid, block, 0, s, kp)
   const int code = d.trans_a * 2 + d.trans_b;
   if (MODE == MODE_GENERAL && d.tag != 0 && code == 2) {
     // the power products (transposed-A layout) under their own symbols
     if (d.tag == 1) { if (vec_ok) SOAP_LAUNCH(1, 0, 4, 1); else SOAP_LAUNCH(1, 0, 1, 1); }
     else { if (vec_ok) SOAP_LAUNCH(1, 0, 4, 2); else SOAP_LAUNCH(1, 0, 1, 2); }
+  } else if (MODE == MODE_GENERAL && kp.kslice <= SHORT_K) {
+#define SOAP_LAUNCH_RANK(TA, TB, VEC) \
+  hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE_GENERAL, 0, 3>), grid, block, 0, s, kp)
+    if (vec_ok) {
+      switch (code) {
+        case 0: SOAP_LAUNCH_RANK(0, 0, 4); break;
+        case 1: SOAP_LAUNCH_RANK(0, 1, 4); break;
+        case 2: SOAP_LAUNCH_RANK(1, 0, 4); break;
+        default: SOAP_LAUNCH_RANK(1, 1, 4); break;
+      }
+    } else {
+      switch (code) {
+        case 0: SOAP_LAUNCH_RANK(0, 0, 1); break;
+        case 1: SOAP_LAUNCH_RANK(0, 1, 1); break;
+        case 2: SOAP_LAUNCH_RANK(1, 0, 1); break;
+        default: SOAP_LAUNCH_RANK(1, 1, 1); break;
+      }
+    }
+#undef SOAP_LAUNCH_RANK
   } else if (vec_ok) {
     switch (code) {
       case 0: SOAP_LAUNCH(0, 0, 4, 0); break;
