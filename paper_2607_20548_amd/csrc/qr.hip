@@ -1,22 +1,26 @@
 // Blocked Householder QR with explicit Q, for the SOAP eigenbasis refresh
 // (the paper's Algorithm 2 takes QR(L_t Q_L).Q and QR(R_t Q_R).Q every step).
 //
-// Structure (two-level blocking):
+// Structure:
 //  * Outer blocks of NB = 128 columns.  After an outer block is factored, its
 //    reflectors act on the trailing matrix through the compact-WY form
 //    H_1 ... H_nb = I - Y T Y^T:  A_trail -= Y (T^T (Y^T A_trail)), three fp32
-//    MFMA GEMMs (the first one split over K).
-//  * Inside an outer block, inner panels of width b in {16, 8, 4} are each
-//    factored by ONE 512-thread workgroup that holds the whole panel
-//    (rows ci..n-1, b columns) in registers; the column loop uses wave64
-//    butterfly reductions and two workgroup barriers per column.  b is chosen
-//    so that b * rows-per-thread <= 128 registers.
-//  * After each inner panel a row-split reduction forms Y_p^T over the outer
-//    block (the panel's Gram matrix for its T block, Y_prev^T Y_p for the T
-//    column, Y_p^T A_rest for the update); its last workgroup finishes the
-//    small triangular products, and a row-parallel apply updates the rest of
-//    the outer block.
-//  * Q is formed backwards, Q[c:, c:] -= Y (T (Y^T Q[c:, c:])), starting from I.
+//    MFMA GEMMs (the first one split over K).  Look-ahead: the next block's
+//    columns are updated first, then the next block is factored on a second
+//    stream while the rest of the trailing matrix is updated.
+//  * An outer block is factored by qr_block_kernel: one launch whose
+//    workgroups keep the block in registers and sum the dot products of each
+//    column grid-wide (see the comment above the kernel).  It needs all of
+//    its workgroups resident; batches too large for that take the panel
+//    path:
+//  * Panel path: inner panels of width b in {16, 8, 4} are each factored by
+//    ONE 512-thread workgroup that holds the whole panel (rows ci..n-1, b
+//    columns) in registers (wave64 butterfly reductions, two barriers per
+//    column); a row-split reduction then forms the panel's T block, the T
+//    column and the update coefficients, and a row-parallel apply updates the
+//    rest of the outer block.
+//  * Q is formed backwards, Q[c:, c:] -= Y (T (Y^T Q[c:, c:])), starting from
+//    diag(d).
 //
 // Reflector convention (as in LAPACK's larfg): for x = A[j:, j] with
 // s = ||x[1:]||^2 and sigma = ||x||, v0 = x0 + sgn(x0) sigma (sgn(0) = +1),

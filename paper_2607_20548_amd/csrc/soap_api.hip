@@ -245,7 +245,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   }
   // Fork: the L side on the auxiliary stream, the R side on the caller's.
   hipStream_t sl = nullptr, spl = nullptr, spr = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_power = nullptr;
   if ((e = aux_stream(0, &sl)) != hipSuccess || (e = aux_stream(1, &spl)) != hipSuccess ||
       (e = aux_stream(2, &spr)) != hipSuccess)
     return hip_fail(e, "auxiliary stream");
@@ -255,10 +255,15 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     (void)hipEventDestroy(ev_fork);
     return hip_fail(e, "event");
   }
+  if ((e = hipEventCreateWithFlags(&ev_power, hipEventDisableTiming)) != hipSuccess) {
+    (void)hipEventDestroy(ev_fork);
+    (void)hipEventDestroy(ev_join);
+    return hip_fail(e, "event");
+  }
   struct EventGuard {
-    hipEvent_t a, b;
-    ~EventGuard() { (void)hipEventDestroy(a); (void)hipEventDestroy(b); }
-  } guard{ev_fork, ev_join};
+    hipEvent_t a, b, c;
+    ~EventGuard() { (void)hipEventDestroy(a); (void)hipEventDestroy(b); (void)hipEventDestroy(c); }
+  } guard{ev_fork, ev_join, ev_power};
   if ((e = hipEventRecord(ev_fork, s)) != hipSuccess) return hip_fail(e, "fork record");
   if ((e = hipStreamWaitEvent(sl, ev_fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
   {  // L <- b2 L + (1-b2) G G^T
@@ -278,12 +283,6 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "power L");
   }
-  {  // Q_L = QR(A_L).Q
-    StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
-    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl)) != hipSuccess)
-      return hip_fail(e, "QR L");
-  }
-  if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
   {  // R <- b2 R + (1-b2) G^T G
     StageScope sc(ST_FACTOR_R, B * nd * (nd + 1) * md, s);
     soap::GemmDesc d;
@@ -300,21 +299,32 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     d.C = AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
     if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power R");
   }
-  {  // Q_R = QR(A_R).Q
-    StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
-    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr)) != hipSuccess)
-      return hip_fail(e, "QR R");
-  }  if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
-  {  // T_G = Q_L^T G,  T_M = Q_L^T M
-    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, s);
+  // The L-side QR starts once the R-side power product is done: its resident
+  // block kernels need free compute units, which that long product holds.
+  if ((e = hipEventRecord(ev_power, s)) != hipSuccess) return hip_fail(e, "power record");
+  if ((e = hipStreamWaitEvent(sl, ev_power, 0)) != hipSuccess) return hip_fail(e, "power wait");
+  {  // Q_L = QR(A_L).Q
+    StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
+    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl)) != hipSuccess)
+      return hip_fail(e, "QR L");
+  }
+  {  // T_G = Q_L^T G,  T_M = Q_L^T M (needs only the L side: stays on its stream)
+    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, sl);
     soap::GemmDesc d;
     d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
     d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
     d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch;
-    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in G");
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in G");
     d.B = M; d.C = TM;
-    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in M");
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
   }
+  if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
+  {  // Q_R = QR(A_R).Q
+    StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
+    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr)) != hipSuccess)
+      return hip_fail(e, "QR R");
+  }
+  if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
   {  // G' = T_G Q_R, M' = T_M Q_R, then Adam in the eigenbasis
     StageScope sc(ST_ROT_IN_R_ADAM, B * 4.0 * md * nd * nd, s);
     soap::GemmDesc d;
