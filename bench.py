@@ -6,6 +6,7 @@ with per-step QR refresh of both eigenbases (R is 14336 x 14336).  Gradients
 are generated and copied to HBM before the timed region.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+                    [--calibration-copy-mib N]
 
 Prints ONE JSON line.  `value` is steps/s of the whole step; `roofline`
 describes the dominant kernel (timed with HIP events on the library's stream
@@ -13,6 +14,7 @@ through the soap_timing_* API); `cpu_baseline` times the fp64 oracle on a
 bounded sample of the same workload.
 """
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -37,6 +39,28 @@ def step_flops(m: int, n: int) -> float:
     qr = (8.0 / 3.0) * (m ** 3 + n ** 3)
     rot = 6.0 * m * n * (m + n)
     return syrk + power + qr + rot
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "power_product_R_4096x14336_traffic.json")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_20548_amd", "csrc", "gemm.hip")
+
+
+def gemm_source_hash() -> str:
+    with open(GEMM_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per power-product launch from the committed counter summary,
+    or None if there is none or it was taken on another GEMM source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("gemm_source_sha256") != gemm_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
 
 
 def cpu_baseline(m: int, n: int, rank: int, scale: int = 4):
@@ -69,6 +93,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibration-copy-mib", type=int, default=0)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the SOAP step of a "
@@ -95,6 +120,15 @@ def main():
     for t in range(1, args.warmup + 1):
         state.step(W, grads[t - 1], t, **HP)
     torch.cuda.synchronize()
+    if args.calibration_copy_mib > 0:
+        nel = args.calibration_copy_mib * (1 << 20) // 4
+        src = torch.ones(nel, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] calibration copy of {args.calibration_copy_mib} MiB done", file=sys.stderr,
+              flush=True)
+        del src, dst
     soap.soap_init_state(1, m, n, state.L, state.R, state.Q_L, state.Q_R, state.M, state.V)
     torch.cuda.synchronize()
     print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
@@ -145,8 +179,8 @@ def main():
         "step_frac_of_fp32_mfma_peak": F * value / 1e12 / PEAK_FP32_MFMA_TFLOPS,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
                      "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
-                     "avg_launch_ms": d_ms / d_n},
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": measured_traffic(),
+                     "traffic_unit": "HBM bytes per launch", "avg_launch_ms": d_ms / d_n},
         "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
     }
     if not args.no_cpu_baseline:
