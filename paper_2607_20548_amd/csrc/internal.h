@@ -78,10 +78,12 @@ hipError_t launch_copy(float *dst, const float *src, int64_t count, hipStream_t 
 // by the factorization; the Q factor with non-negative diag(R) is written
 // row-major to Q.  If Rf is non-null the triangular factor is written there
 // (row-major, strict lower part zero).  Work is ordered on stream s; the
-// panel factorizations run on stream sp (joined back into s with events).
+// block factorizations run on stream sp and the T matrices of block pairs on
+// stream st (both joined back into s with events; st may equal sp).
 size_t qr_workspace_bytes(int64_t batch, int64_t n);
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
-                                void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp);
+                                void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
+                                hipStream_t st);
 // dst = src^T for one n x n row-major matrix.
 hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t s);
 

@@ -917,6 +917,34 @@ __global__ __launch_bounds__(256) void qr_extract_r_kernel(const float *At, floa
   }
 }
 
+// Zeroes, in At, the entries of each column above its outer block's rows
+// (At[j][i] for i < NB floor(j / NB)): R entries, no longer needed once R has
+// been extracted.  Y then has explicit zeros above every block, so two
+// consecutive blocks form one unit lower-trapezoidal Y of 2 NB columns.
+__global__ __launch_bounds__(256) void qr_zero_above_blocks_kernel(float *At, int n, int64_t sA) {
+  float *A = At + (int64_t)blockIdx.y * sA;
+  const int64_t nn = (int64_t)n * n;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += (int64_t)gridDim.x * 256) {
+    const int j = (int)(e / n), i = (int)(e - (int64_t)j * n);
+    if (i < (j / NB) * NB) A[e] = 0.f;
+  }
+}
+
+// T of a pair of consecutive full blocks a, b (2 NB x 2 NB, row-major):
+//   [[T_a, T_ab], [0, T_b]]; T_ab was written in place by the caller.
+__global__ __launch_bounds__(256) void qr_assemble_pair_t_kernel(float *TP, int64_t sTP,
+                                                                 const float *Ta, const float *Tb,
+                                                                 int64_t sT) {
+  float *P = TP + (int64_t)blockIdx.y * sTP;
+  const float *A = Ta + (int64_t)blockIdx.y * sT, *B = Tb + (int64_t)blockIdx.y * sT;
+  for (int e = blockIdx.x * 256 + threadIdx.x; e < 4 * NB * NB; e += gridDim.x * 256) {
+    const int r = e / (2 * NB), c = e % (2 * NB);
+    if (r < NB && c < NB) P[e] = A[r * NB + c];
+    else if (r >= NB && c < NB) P[e] = 0.f;
+    else if (r >= NB) P[e] = B[(r - NB) * NB + (c - NB)];
+  }
+}
+
 // Q <- diag(d) for each matrix of the batch.
 __global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *dsign, int n,
                                                         int64_t sA) {
@@ -951,7 +979,10 @@ struct QrLayout {
   int64_t n, nob;
   bool block;          // outer blocks factored by qr_block_kernel (else the panel path)
   size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, x_off, total;
+  size_t tp_off, sx_off, skp_off;
   int64_t sT, sWbuf, sSk, sPart, sWi;
+  int64_t np;          // pairs of full outer blocks (Q is formed by pairs)
+  int64_t sTP, sSx, sSkp;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -964,8 +995,12 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.nob = (n + NB - 1) / NB;
   const int64_t P = (n + RCH - 1) / RCH;
   L.sT = L.nob * NB * NB;
-  L.sWbuf = (int64_t)NB * n;
-  L.sSk = (int64_t)MAX_SPLIT * NB * n;
+  L.np = (n / NB) / 2;
+  L.sWbuf = (int64_t)2 * NB * n;
+  L.sSk = (int64_t)MAX_SPLIT * 2 * NB * n;
+  L.sTP = L.np * 4 * NB * NB;
+  L.sSx = L.np * 2 * NB * NB;
+  L.sSkp = (int64_t)MAX_SPLIT * NB * NB;
   L.sPart = P * PART_STRIDE;
   L.sWi = (int64_t)MAX_B * NB;
   size_t o = 0;
@@ -978,6 +1013,9 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.d_off = o;    o = align256(o + sizeof(float) * batch * n);
   L.b_off = o;    o = align256(o + sizeof(float) * batch * n);
   L.cnt_off = o;  o = align256(o + sizeof(unsigned) * batch);
+  L.tp_off = o;   o = align256(o + sizeof(float) * batch * L.sTP);
+  L.sx_off = o;   o = align256(o + sizeof(float) * batch * L.sSx);
+  L.skp_off = o;  o = align256(o + sizeof(float) * batch * L.sSkp);
   // The resident-block path needs every workgroup of a launch resident at
   // once: at most BK_MAX_WG workgroups (two such launches, one per factor,
   // may run together on the 256 compute units).
@@ -1052,6 +1090,7 @@ struct QrCtx {
   float *Tb, *Wb, *W2, *Sk, *Pt, *Wi, *dsign, *betas;
   unsigned *cnt;
   unsigned long long *xch;
+  float *TP, *Sx, *Skp;
 };
 
 hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
@@ -1140,10 +1179,75 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   return launch_gemm(g3, s);
 }
 
+// T of pair p (full blocks a = 2p, b = 2p+1), on stream st:
+//   S = Y_a^T Y_b over rows >= c_b (where Y_b is nonzero), X = T_a S,
+//   T_ab = -X T_b into the top-right block of the pair's T, then the
+//   diagonal blocks.  Reads only At rows of the two blocks at columns >= c_b
+//   and their T, which the concurrent trailing update does not touch.
+hipError_t pair_t(const QrCtx &x, int64_t p, hipStream_t st) {
+  const int64_t n = x.n, ca = 2 * p * NB, cb = ca + NB;
+  float *S = x.Sx + p * 2 * NB * NB, *X = S + NB * NB;
+  const float *Ta = x.Tb + (2 * p) * NB * NB, *Tbk = Ta + NB * NB;
+  float *TP = x.TP + p * 4 * NB * NB;
+  GemmDesc gs;  // S[i][j] = sum_r At[ca+i][r] At[cb+j][r], r in [cb, n)
+  gs.trans_a = 0; gs.trans_b = 1; gs.M = NB; gs.N = NB; gs.K = n - cb;
+  gs.A = x.At + ca * n + cb; gs.lda = n; gs.sA = x.sA;
+  gs.B = x.At + cb * n + cb; gs.ldb = n; gs.sB = x.sA;
+  gs.C = S; gs.ldc = NB; gs.sC = x.L.sSx; gs.batch = x.batch;
+  gs.splitk = choose_splitk(NB, NB, n - cb, x.batch, MAX_SPLIT);
+  gs.part = x.Skp;
+  SOAP_TRY(launch_gemm(gs, st));
+  GemmDesc gx;  // X = T_a S
+  gx.M = NB; gx.N = NB; gx.K = NB;
+  gx.A = Ta; gx.lda = NB; gx.sA = x.L.sT;
+  gx.B = S; gx.ldb = NB; gx.sB = x.L.sSx;
+  gx.C = X; gx.ldc = NB; gx.sC = x.L.sSx; gx.batch = x.batch;
+  SOAP_TRY(launch_gemm(gx, st));
+  GemmDesc gt;  // T_ab = -X T_b
+  gt.M = NB; gt.N = NB; gt.K = NB;
+  gt.A = X; gt.lda = NB; gt.sA = x.L.sSx;
+  gt.B = Tbk; gt.ldb = NB; gt.sB = x.L.sT;
+  gt.C = TP + NB; gt.ldc = 2 * NB; gt.sC = x.L.sTP; gt.alpha = -1.f; gt.batch = x.batch;
+  SOAP_TRY(launch_gemm(gt, st));
+  hipLaunchKernelGGL(qr_assemble_pair_t_kernel, dim3(64, (unsigned)x.batch), dim3(256), 0, st, TP,
+                     x.L.sTP, Ta, Tbk, x.L.sT);
+  return hipGetLastError();
+}
+
+// Q[c:, c:] -= Y (T (Y^T Q[c:, c:])) for the w reflectors stored in At rows
+// c..c+w-1 (zero above row c + their index) with T (w x w, leading dimension
+// ldt, batch stride sT).
+hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_t ldt,
+                    int64_t sT, hipStream_t s) {
+  const int64_t n = x.n, Kr = n - c;
+  GemmDesc g1;  // W = Y^T Q[c:n, c:n]:  op(A)[i][k] = Y[k][i] = At[c+i][c+k]
+  g1.trans_a = 0; g1.trans_b = 0; g1.M = w; g1.N = Kr; g1.K = Kr;
+  g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
+  g1.B = x.Q + c * n + c; g1.ldb = n; g1.sB = x.sA;
+  g1.C = x.Wb; g1.ldc = Kr; g1.sC = x.L.sWbuf; g1.batch = x.batch;
+  g1.splitk = choose_splitk(w, Kr, Kr, x.batch, MAX_SPLIT);
+  g1.part = x.Sk;
+  SOAP_TRY(launch_gemm(g1, s));
+  GemmDesc g2;  // W2 = T W
+  g2.trans_a = 0; g2.trans_b = 0; g2.M = w; g2.N = Kr; g2.K = w;
+  g2.A = T; g2.lda = ldt; g2.sA = sT;
+  g2.B = x.Wb; g2.ldb = Kr; g2.sB = x.L.sWbuf;
+  g2.C = x.W2; g2.ldc = Kr; g2.sC = x.L.sWbuf; g2.batch = x.batch;
+  SOAP_TRY(launch_gemm(g2, s));
+  GemmDesc g3;  // Q[c:n, c:n] -= Y W2:  op(A)[k][i] = Y[k][i] = At[c+i][c+k]
+  g3.trans_a = 1; g3.trans_b = 0; g3.M = Kr; g3.N = Kr; g3.K = w;
+  g3.A = x.At + c * n + c; g3.lda = n; g3.sA = x.sA;
+  g3.B = x.W2; g3.ldb = Kr; g3.sB = x.L.sWbuf;
+  g3.C = x.Q + c * n + c; g3.ldc = n; g3.sC = x.sA;
+  g3.alpha = -1.f; g3.beta = 1.f; g3.batch = x.batch;
+  return launch_gemm(g3, s);
+}
+
 }  // namespace
 
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
-                                void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp) {
+                                void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
+                                hipStream_t st) {
   QrCtx x;
   x.L = qr_layout(batch, n);
   if (ws_bytes < x.L.total) return hipErrorInvalidValue;
@@ -1159,7 +1263,10 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   x.betas = reinterpret_cast<float *>(base + x.L.b_off);
   x.cnt = reinterpret_cast<unsigned *>(base + x.L.cnt_off);
   x.xch = reinterpret_cast<unsigned long long *>(base + x.L.x_off);
-  const int64_t nob = x.L.nob;
+  x.TP = reinterpret_cast<float *>(base + x.L.tp_off);
+  x.Sx = reinterpret_cast<float *>(base + x.L.sx_off);
+  x.Skp = reinterpret_cast<float *>(base + x.L.skp_off);
+  const int64_t nob = x.L.nob, np = x.L.np;
 
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
   if (x.L.block)   // generations restart at 1 every call: clear the old items
@@ -1188,8 +1295,30 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     hipEvent_t ev_panel;
     SOAP_TRY(t_events.get(&ev_panel));
     SOAP_TRY(hipEventRecord(ev_panel, sp));
+    if ((ob + 1) % 2 == 1 && (ob + 1) / 2 < np) {               // pair (ob, ob+1) complete
+      SOAP_TRY(hipStreamWaitEvent(st, ev_panel, 0));
+      SOAP_TRY(pair_t(x, (ob + 1) / 2, st));
+    }
     SOAP_TRY(trailing_update(x, ob, cend2, n, s));              // far: the rest
     SOAP_TRY(hipStreamWaitEvent(s, ev_panel, 0));               // block ob+1 factored
+  }
+  if (np > 0) {                                                 // pair T's done
+    SOAP_TRY(t_events.get(&ev));
+    SOAP_TRY(hipEventRecord(ev, st));
+    SOAP_TRY(hipStreamWaitEvent(s, ev, 0));
+  }
+  if (Rf) {
+    const int64_t nn = n * n;
+    const unsigned gx = (unsigned)std::min<int64_t>((nn + 255) / 256, 2048);
+    hipLaunchKernelGGL(qr_extract_r_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, At, Rf,
+                       x.dsign, x.ni, x.sA);
+    SOAP_TRY(hipGetLastError());
+  }
+  if (np > 0) {   // R is no longer needed: clear it above the block rows of every column
+    const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
+    hipLaunchKernelGGL(qr_zero_above_blocks_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s,
+                       At, x.ni, x.sA);
+    SOAP_TRY(hipGetLastError());
   }
 
   // Explicit Q (row-major), accumulated backwards from diag(d).
@@ -1199,40 +1328,14 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
                        x.ni, x.sA);
     SOAP_TRY(hipGetLastError());
   }
-  for (int64_t ob = nob - 1; ob >= 0; --ob) {
+  // Blocks past the last full pair one by one (backwards), then the pairs as
+  // rank-2NB updates.
+  for (int64_t ob = nob - 1; ob >= 2 * np; --ob) {
     const int64_t c = ob * NB;
-    const int64_t nb = std::min<int64_t>(n, c + NB) - c, Kr = n - c;
-    float *Tob = x.Tb + ob * NB * NB;
-    GemmDesc g1;  // W = Y^T Q[c:n, c:n]:  op(A)[i][k] = Y[k][i] = At[c+i][c+k]
-    g1.trans_a = 0; g1.trans_b = 0; g1.M = nb; g1.N = Kr; g1.K = Kr;
-    g1.A = At + c * n + c; g1.lda = n; g1.sA = x.sA;
-    g1.B = Q + c * n + c; g1.ldb = n; g1.sB = x.sA;
-    g1.C = x.Wb; g1.ldc = Kr; g1.sC = x.L.sWbuf; g1.batch = batch;
-    g1.splitk = choose_splitk(nb, Kr, Kr, batch, MAX_SPLIT);
-    g1.part = x.Sk;
-    SOAP_TRY(launch_gemm(g1, s));
-    GemmDesc g2;  // W2 = T W
-    g2.trans_a = 0; g2.trans_b = 0; g2.M = nb; g2.N = Kr; g2.K = nb;
-    g2.A = Tob; g2.lda = NB; g2.sA = x.L.sT;
-    g2.B = x.Wb; g2.ldb = Kr; g2.sB = x.L.sWbuf;
-    g2.C = x.W2; g2.ldc = Kr; g2.sC = x.L.sWbuf; g2.batch = batch;
-    SOAP_TRY(launch_gemm(g2, s));
-    GemmDesc g3;  // Q[c:n, c:n] -= Y W2:  op(A)[k][i] = Y[k][i] = At[c+i][c+k]
-    g3.trans_a = 1; g3.trans_b = 0; g3.M = Kr; g3.N = Kr; g3.K = nb;
-    g3.A = At + c * n + c; g3.lda = n; g3.sA = x.sA;
-    g3.B = x.W2; g3.ldb = Kr; g3.sB = x.L.sWbuf;
-    g3.C = Q + c * n + c; g3.ldc = n; g3.sC = x.sA;
-    g3.alpha = -1.f; g3.beta = 1.f; g3.batch = batch;
-    SOAP_TRY(launch_gemm(g3, s));
+    SOAP_TRY(q_update(x, c, std::min<int64_t>(n, c + NB) - c, x.Tb + ob * NB * NB, NB, x.L.sT, s));
   }
-
-  if (Rf) {
-    const int64_t nn = n * n;
-    const unsigned gx = (unsigned)std::min<int64_t>((nn + 255) / 256, 2048);
-    hipLaunchKernelGGL(qr_extract_r_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, At, Rf,
-                       x.dsign, x.ni, x.sA);
-    SOAP_TRY(hipGetLastError());
-  }
+  for (int64_t p = np - 1; p >= 0; --p)
+    SOAP_TRY(q_update(x, 2 * p * NB, 2 * NB, x.TP + p * 4 * NB * NB, 2 * NB, x.L.sTP, s));
   return hipSuccess;
 }
 

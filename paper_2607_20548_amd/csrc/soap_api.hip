@@ -123,8 +123,12 @@ class StageScope {
 // chain are independent until the rotations; the L side runs on one
 // auxiliary stream per device (default priority, created on first use) and is
 // joined back with events, so its latency-bound QR panels overlap the R side.
-// Streams per device: 0 = L side, 1 = panels of the L-side QR, 2 = panels
-// of the R-side QR (look-ahead).
+// Streams per device: 0 = L side, 1 / 2 = block factorizations of the L- /
+// R-side QR (look-ahead).  With the caller's stream that is four: HIP maps a
+// process's streams onto a few hardware queues (four by default) and streams
+// that share a queue run in submission order, so the step uses no more.
+// The T matrices of block pairs go on streams with slack: the R side's on
+// the L-side stream, the L side's on the L-side block stream.
 constexpr int N_AUX = 3;
 std::mutex g_aux_mu;
 hipStream_t g_aux[64][N_AUX] = {};
@@ -305,26 +309,27 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   if ((e = hipStreamWaitEvent(sl, ev_power, 0)) != hipSuccess) return hip_fail(e, "power wait");
   {  // Q_L = QR(A_L).Q
     StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
-    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl)) != hipSuccess)
+    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl, spl)) != hipSuccess)
       return hip_fail(e, "QR L");
-  }
-  {  // T_G = Q_L^T G,  T_M = Q_L^T M (needs only the L side: stays on its stream)
-    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, sl);
-    soap::GemmDesc d;
-    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
-    d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
-    d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch;
-    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in G");
-    d.B = M; d.C = TM;
-    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
   }
   if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
   {  // Q_R = QR(A_R).Q
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
-    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr)) != hipSuccess)
+    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl)) != hipSuccess)
       return hip_fail(e, "QR R");
   }
   if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
+  {  // T_G = Q_L^T G,  T_M = Q_L^T M (after the join: run earlier on the L-side stream,
+     // this long product would keep the R-side block kernels from their compute units)
+    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
+    d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in G");
+    d.B = M; d.C = TM;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in M");
+  }
   {  // G' = T_G Q_R, M' = T_M Q_R, then Adam in the eigenbasis
     StageScope sc(ST_ROT_IN_R_ADAM, B * 4.0 * md * nd * nd, s);
     soap::GemmDesc d;
@@ -424,11 +429,13 @@ int soap_qr_f32(int64_t n, const float *A, float *Q, float *Rf, void *workspace,
   hipError_t e = soap::launch_transpose(Aw, A, n, stream);   // the QR factors A^T
   if (e == hipSuccess)
   {
-    hipStream_t sp = nullptr;
+    hipStream_t sp = nullptr, st = nullptr;
     if (e == hipSuccess) e = aux_stream(2, &sp);
+    if (e == hipSuccess) e = aux_stream(1, &st);
     if (e == hipSuccess)
       e = soap::qr_factor_and_form_q(Aw, Q, Rf, 1, n, rest,
-                                     workspace_bytes - align256(sizeof(float) * n * n), stream, sp);
+                                     workspace_bytes - align256(sizeof(float) * n * n), stream, sp,
+                                     st);
   }
   if (e != hipSuccess) return hip_fail(e, "QR");
   return ok();
