@@ -1000,7 +1000,7 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.sSk = (int64_t)MAX_SPLIT * 2 * NB * n;
   L.sTP = L.np * 4 * NB * NB;
   L.sSx = L.np * 2 * NB * NB;
-  L.sSkp = (int64_t)MAX_SPLIT * NB * NB;
+  L.sSkp = (int64_t)64 * NB * NB;
   L.sPart = P * PART_STRIDE;
   L.sWi = (int64_t)MAX_B * NB;
   size_t o = 0;
@@ -1095,6 +1095,16 @@ struct QrCtx {
 
 hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
 
+// Split-K for a latency-critical product with a single tile row/column
+// (M, N <= NB, e.g. the near update's W = Y^T A_next): enough slices to fill
+// the GPU with at least 256 of K each, within the partial buffer of
+// cap_floats floats.
+int narrow_split(int64_t M, int64_t N, int64_t K, int64_t batch, int64_t cap_floats) {
+  int64_t s = std::min<int64_t>(64, K / 256);
+  s = std::min<int64_t>(s, cap_floats / std::max<int64_t>(1, M * N * batch));
+  return (int)std::max<int64_t>(1, s);
+}
+
 // Factors outer block ob on stream s (resident-block kernel or panel path).
 hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
   if (!x.L.block) return panel_phase(x, ob, s);
@@ -1159,7 +1169,8 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
   g1.B = x.At + j0 * n + c; g1.ldb = n; g1.sB = x.sA;
   g1.C = x.Wb; g1.ldc = Nt; g1.sC = x.L.sWbuf; g1.batch = x.batch;
-  g1.splitk = choose_splitk(nb, Nt, Kr, x.batch, MAX_SPLIT);
+  g1.splitk = (Nt <= NB) ? narrow_split(nb, Nt, Kr, x.batch, x.batch * x.L.sSk)
+                          : choose_splitk(nb, Nt, Kr, x.batch, MAX_SPLIT);
   g1.part = x.Sk;
   SOAP_TRY(launch_gemm(g1, s));
   // W2 = T^T W
@@ -1194,7 +1205,7 @@ hipError_t pair_t(const QrCtx &x, int64_t p, hipStream_t st) {
   gs.A = x.At + ca * n + cb; gs.lda = n; gs.sA = x.sA;
   gs.B = x.At + cb * n + cb; gs.ldb = n; gs.sB = x.sA;
   gs.C = S; gs.ldc = NB; gs.sC = x.L.sSx; gs.batch = x.batch;
-  gs.splitk = choose_splitk(NB, NB, n - cb, x.batch, MAX_SPLIT);
+  gs.splitk = narrow_split(NB, NB, n - cb, x.batch, x.batch * x.L.sSkp);
   gs.part = x.Skp;
   SOAP_TRY(launch_gemm(gs, st));
   GemmDesc gx;  // X = T_a S
