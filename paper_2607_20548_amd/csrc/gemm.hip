@@ -133,8 +133,7 @@ __device__ __forceinline__ void read_frag(const float *lds, int x, int h, float 
 
 // Maps the linear workgroup id to a (tile-row, tile-column) pair.
 template <int MODE>
-__device__ __forceinline__ void tile_coords(const KParams &p, int &tm, int &tn) {
-  int t = blockIdx.x;
+__device__ __forceinline__ void tile_coords(const KParams &p, int t, int &tm, int &tn) {
   const int nt = p.ntiles;
   if ((nt & 7) == 0) t = (t & 7) * (nt >> 3) + (t >> 3);  // contiguous run per XCD
   if (MODE == MODE_SYRK) {
@@ -159,14 +158,17 @@ __device__ __forceinline__ void tile_coords(const KParams &p, int &tm, int &tn) 
 // rank-k updates): the bound on resident workgroups makes the compiler keep
 // the accumulators in VGPRs (4 workgroups per CU), and the epilogue batches
 // its reads of C.  Long-K products (MINB = 1) keep the accumulators in AGPRs.
-template <int TA, int TB, int VEC, int MODE, int TAG, int MINB>
+template <int TA, int TB, int VEC, int MODE, int TAG, int MINB, bool PERSIST = false>
 __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   constexpr bool SHORTK = MINB > 1;
   constexpr int NA = (MODE == MODE_ADAM) ? 2 : 1;
   __shared__ __attribute__((aligned(16))) float lds[2 * (NA + 1) * TILE_FLOATS];
 
+  // One tile per workgroup; PERSIST: a loop over tiles when the grid was
+  // capped (the caller limited the compute units this product may hold).
+  for (int tile = blockIdx.x;;) {
   int tm, tn;
-  tile_coords<MODE>(p, tm, tn);
+  tile_coords<MODE>(p, tile, tm, tn);
   const int64_t bz = blockIdx.z;
   const float *A = p.A + bz * p.sA;
   const float *A2 = (MODE == MODE_ADAM) ? p.A2 + bz * p.sA : nullptr;
@@ -311,6 +313,10 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
         }
       }
   }
+  if constexpr (!PERSIST) break;
+  tile += gridDim.x;
+  if (tile >= p.ntiles) break;
+  }  // tile loop
 }
 
 // C = alpha * sum_s part[s] + beta * C, slices summed in index order.
@@ -337,11 +343,36 @@ template <int MODE>
 hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) {
   dim3 block(NTHREADS);
   const int S = (MODE == MODE_GENERAL && d.splitk > 1 && d.part) ? d.splitk : 1;
-  dim3 grid(kp.ntiles, S, (unsigned)d.batch);
+  const bool capped = MODE == MODE_GENERAL && d.max_wg > 0 && d.max_wg < kp.ntiles;
+  const int wgs = capped ? std::max(8, d.max_wg & ~7) : kp.ntiles;   // multiple of 8: XCD locality
+  dim3 grid(std::min(wgs, kp.ntiles), S, (unsigned)d.batch);
 #define SOAP_LAUNCH(TA, TB, VEC, TAG) \
   hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE, TAG, 1>), grid, block, 0, s, kp)
   const int code = d.trans_a * 2 + d.trans_b;
-  if (MODE == MODE_GENERAL && d.tag != 0 && code == 2) {
+  if (capped) {
+#define SOAP_LAUNCH_P(TA, TB, VEC, MINB) \
+  hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE_GENERAL, 0, MINB, true>), grid, block, 0, s, kp)
+    const bool shortk = kp.kslice <= SHORT_K;
+    switch (code * 4 + (vec_ok ? 2 : 0) + (shortk ? 1 : 0)) {
+      case 0: SOAP_LAUNCH_P(0, 0, 1, 1); break;
+      case 1: SOAP_LAUNCH_P(0, 0, 1, 3); break;
+      case 2: SOAP_LAUNCH_P(0, 0, 4, 1); break;
+      case 3: SOAP_LAUNCH_P(0, 0, 4, 3); break;
+      case 4: SOAP_LAUNCH_P(0, 1, 1, 1); break;
+      case 5: SOAP_LAUNCH_P(0, 1, 1, 3); break;
+      case 6: SOAP_LAUNCH_P(0, 1, 4, 1); break;
+      case 7: SOAP_LAUNCH_P(0, 1, 4, 3); break;
+      case 8: SOAP_LAUNCH_P(1, 0, 1, 1); break;
+      case 9: SOAP_LAUNCH_P(1, 0, 1, 3); break;
+      case 10: SOAP_LAUNCH_P(1, 0, 4, 1); break;
+      case 11: SOAP_LAUNCH_P(1, 0, 4, 3); break;
+      case 12: SOAP_LAUNCH_P(1, 1, 1, 1); break;
+      case 13: SOAP_LAUNCH_P(1, 1, 1, 3); break;
+      case 14: SOAP_LAUNCH_P(1, 1, 4, 1); break;
+      default: SOAP_LAUNCH_P(1, 1, 4, 3); break;
+    }
+#undef SOAP_LAUNCH_P
+  } else if (MODE == MODE_GENERAL && d.tag != 0 && code == 2) {
     // the power products (transposed-A layout) under their own symbols
     if (d.tag == 1) { if (vec_ok) SOAP_LAUNCH(1, 0, 4, 1); else SOAP_LAUNCH(1, 0, 1, 1); }
     else { if (vec_ok) SOAP_LAUNCH(1, 0, 4, 2); else SOAP_LAUNCH(1, 0, 1, 2); }

@@ -33,6 +33,10 @@ struct GemmDesc {
   // Distinct kernel symbol for profiling (0 = shared GEMM; 1, 2 = the power
   // products L Q_L and R Q_R), so that a trace can attribute time per stage.
   int tag = 0;
+  // If > 0, at most this many workgroups (rounded down to a multiple of 8)
+  // are launched and each loops over tiles: the product then holds only part
+  // of the compute units, leaving the rest to concurrent work.
+  int max_wg = 0;
 };
 
 // A split-K factor that gives at least ~2 workgroups per CU for a product with

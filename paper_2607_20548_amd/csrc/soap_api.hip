@@ -130,6 +130,9 @@ class StageScope {
 // The T matrices of block pairs go on streams with slack: the R side's on
 // the L-side stream, the L side's on the L-side block stream.
 constexpr int N_AUX = 3;
+// Workgroup cap of products that run beside the resident block kernels of
+// the other side's QR: 160 of the 256 compute units, leaving about 12 per XCD.
+constexpr int kSideWorkgroups = 160;
 std::mutex g_aux_mu;
 hipStream_t g_aux[64][N_AUX] = {};
 
@@ -312,6 +315,18 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl, spl)) != hipSuccess)
       return hip_fail(e, "QR L");
   }
+  {  // T_G = Q_L^T G,  T_M = Q_L^T M on the L-side stream, capped to part of the
+     // GPU: it overlaps the R-side QR, whose resident block kernels need whole
+     // compute units free.
+    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
+    d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch; d.max_wg = kSideWorkgroups;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in G");
+    d.B = M; d.C = TM;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
+  }
   if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
   {  // Q_R = QR(A_R).Q
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
@@ -319,17 +334,6 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
       return hip_fail(e, "QR R");
   }
   if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
-  {  // T_G = Q_L^T G,  T_M = Q_L^T M (after the join: run earlier on the L-side stream,
-     // this long product would keep the R-side block kernels from their compute units)
-    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, s);
-    soap::GemmDesc d;
-    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
-    d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
-    d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch;
-    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in G");
-    d.B = M; d.C = TM;
-    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "rotate in M");
-  }
   {  // G' = T_G Q_R, M' = T_M Q_R, then Adam in the eigenbasis
     StageScope sc(ST_ROT_IN_R_ADAM, B * 4.0 * md * nd * nd, s);
     soap::GemmDesc d;
