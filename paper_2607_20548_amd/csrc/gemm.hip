@@ -343,8 +343,12 @@ template <int MODE>
 hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) {
   dim3 block(NTHREADS);
   const int S = (MODE == MODE_GENERAL && d.splitk > 1 && d.part) ? d.splitk : 1;
-  const bool capped = MODE == MODE_GENERAL && d.max_wg > 0 && d.max_wg < kp.ntiles;
-  const int wgs = capped ? std::max(8, d.max_wg & ~7) : kp.ntiles;   // multiple of 8: XCD locality
+  // A cap counts every workgroup (split slices and batch included); the
+  // tile dimension stays a multiple of 8 for XCD locality.
+  const int64_t per_tile = (int64_t)S * d.batch;
+  const bool capped =
+      MODE == MODE_GENERAL && d.max_wg > 0 && (int64_t)kp.ntiles * per_tile > d.max_wg;
+  const int wgs = capped ? (int)std::max<int64_t>(8, (d.max_wg / per_tile) & ~int64_t(7)) : kp.ntiles;
   dim3 grid(std::min(wgs, kp.ntiles), S, (unsigned)d.batch);
 #define SOAP_LAUNCH(TA, TB, VEC, TAG) \
   hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE, TAG, 1>), grid, block, 0, s, kp)
