@@ -8,10 +8,13 @@ does, and the two share no code.
 Parity status of each function is stated in its docstring; every function here
 is pinned by a ``-m "not gpu"`` test against something other than itself
 (closed forms, LAPACK, brute force in 50-digit arithmetic, the paper's
-reductions to AdamW and to the polar factor).
+reductions to AdamW and to the polar factor; for the KL-Shampoo accumulation,
+the exact-inverse rule, the fixed point and condition number of Appendix A.3,
+and the reduction to the plain factor EMA).
 """
 from .soap_oracle import (  # noqa: F401
     OracleState, init_state, factor_ema, householder_qr, momentum_ema, rotate_in,
     adam_eigenbasis, rotate_out, weight_update, bias_corrections, soap_step,
-    soap_step_batched,
+    soap_step_batched, eigenvalue_estimates, kl_factor_update, kl_factors, kl_soap_step,
+    kl_soap_step_batched,
 )

@@ -25,6 +25,10 @@ inconsistent:
   * QR(.).Q means the Q factor with non-negative diagonal R (unique for
     nonsingular input).
   * Initial state: L = R = Q_L = Q_R = I, M = V = 0.
+
+kl_soap_step is the KL-SOAP variant the paper recommends (Sections 5.4.3 and
+7): the factors are accumulated by the KL-Shampoo rule of Algorithm 2
+(readings in kl_factor_update), the rest of the step is unchanged.
 """
 from __future__ import annotations
 
@@ -151,20 +155,41 @@ def weight_update(W: np.ndarray, dW: np.ndarray, lr: float, wd: float) -> np.nda
     return (1.0 - lr * wd) * W - lr * dW
 
 
-def soap_step(state: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
-              eps: float, lr: float, weight_decay: float, bias_correction: bool = True,
-              diagnostics: bool = False):
-    """One SOAP step on one matrix (Algorithm 2 with F = 1, real-time refresh).
+def eigenvalue_estimates(F: np.ndarray, Q: np.ndarray) -> np.ndarray:
+    """Approximate eigenvalues of a Kronecker factor in the current eigenbasis
+    (Algorithm 2, KL-Shampoo accumulation): lambda = diag(Q^T F Q), with the
+    factor and basis of the previous step."""
+    return np.diag(Q.T @ F @ Q).copy()
 
-    Order: factor EMA with the current G, power product and QR refresh, first
-    moment EMA, rotation in, Adam, rotation out, weight update.  Returns the new
-    state (and a dict of intermediates when ``diagnostics``)."""
-    if t < 1:
-        raise ValueError("step t is 1-based")
-    G = np.asarray(G, dtype=np.float64)
-    s = state.copy()
-    s.L = factor_ema(s.L, G, beta2)
-    s.R = factor_ema(s.R, G.T, beta2)
+
+def kl_factor_update(F: np.ndarray, X: np.ndarray, Q_other: np.ndarray, lam_other: np.ndarray,
+                     beta_kron: float, eps: float, count: int) -> np.ndarray:
+    """KL-Shampoo accumulation of one Kronecker factor (Algorithm 2; the
+    KL-Shampoo rule restated in Appendix A.3):
+
+        F <- beta_kron F + (1 - beta_kron) / count * X S^{-1} X^T,
+        S^{-1} = Q_other diag(1 / (lam_other + eps)) Q_other^T.
+
+    For L pass X = G (m x n), the R-side basis and eigenvalue estimates and
+    count = n ("out"); for R pass X = G^T, the L-side ones and count = m
+    ("in").  Readings: beta_kron multiplies the old factor, like every EMA of
+    the Section 2 primer; the exponent applied to (lambda + eps) is -1, the
+    inverse the appendix's rule uses; and the eigenvalue estimates act in the
+    basis they were measured in, so S^{-1} is the inverse of the other factor
+    as that basis diagonalises it.  The result is symmetric by definition; it
+    is formed from its lower triangle and mirrored."""
+    Sinv = Q_other @ np.diag(1.0 / (lam_other + eps)) @ Q_other.T
+    S = beta_kron * np.asarray(F, dtype=np.float64) + ((1.0 - beta_kron) / count) * (X @ Sinv @ X.T)
+    low = np.tril(S)
+    return low + np.tril(low, -1).T
+
+
+def _refresh_and_update(s: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
+                        eps: float, lr: float, weight_decay: float, bias_correction: bool,
+                        diagnostics: bool):
+    """The part of the step after the factors hold the current gradient:
+    power product and QR refresh, first-moment EMA, rotation in, Adam, rotation
+    out, weight update (Algorithm 2 with F = 1)."""
     AL = s.L @ s.QL
     AR = s.R @ s.QR
     s.QL = householder_qr(AL)
@@ -181,6 +206,63 @@ def soap_step(state: OracleState, G: np.ndarray, t: int, beta1: float, beta2: fl
     return s
 
 
+def soap_step(state: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
+              eps: float, lr: float, weight_decay: float, bias_correction: bool = True,
+              diagnostics: bool = False):
+    """One SOAP step on one matrix (Algorithm 2 with F = 1, real-time refresh).
+
+    Order: factor EMA with the current G, power product and QR refresh, first
+    moment EMA, rotation in, Adam, rotation out, weight update.  Returns the new
+    state (and a dict of intermediates when ``diagnostics``)."""
+    if t < 1:
+        raise ValueError("step t is 1-based")
+    G = np.asarray(G, dtype=np.float64)
+    s = state.copy()
+    s.L = factor_ema(s.L, G, beta2)
+    s.R = factor_ema(s.R, G.T, beta2)
+    return _refresh_and_update(s, G, t, beta1, beta2, eps, lr, weight_decay, bias_correction,
+                               diagnostics)
+
+
+def kl_factors(L: np.ndarray, R: np.ndarray, QL: np.ndarray, QR: np.ndarray, G: np.ndarray,
+               beta_kron: float, eps: float):
+    """Both KL-Shampoo factor updates of Algorithm 2 from the previous step's
+    L, R, Q_L, Q_R: the eigenvalue estimates of both factors are taken first,
+    then each factor is accumulated with the other side's estimates.  Returns
+    (L_new, R_new, lam_L, lam_R)."""
+    G = np.asarray(G, dtype=np.float64)
+    m, n = G.shape
+    lam_L = eigenvalue_estimates(L, QL)
+    lam_R = eigenvalue_estimates(R, QR)
+    L_new = kl_factor_update(L, G, QR, lam_R, beta_kron, eps, n)
+    R_new = kl_factor_update(R, G.T, QL, lam_L, beta_kron, eps, m)
+    return L_new, R_new, lam_L, lam_R
+
+
+def kl_soap_step(state: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
+                 beta_kron: float, eps: float, lr: float, weight_decay: float,
+                 bias_correction: bool = True, diagnostics: bool = False):
+    """One KL-SOAP step (Algorithm 2 with F = 1, real-time refresh): the factor
+    EMA of soap_step is replaced by the KL-Shampoo accumulation (kl_factors);
+    the same eps serves the eigenvalue floor and Adam (hyperparameter table of
+    Section 5.4).  Everything after the accumulation is soap_step's."""
+    if t < 1:
+        raise ValueError("step t is 1-based")
+    G = np.asarray(G, dtype=np.float64)
+    s = state.copy()
+    s.L, s.R, lam_L, lam_R = kl_factors(s.L, s.R, s.QL, s.QR, G, beta_kron, eps)
+    out = _refresh_and_update(s, G, t, beta1, beta2, eps, lr, weight_decay, bias_correction,
+                              diagnostics)
+    if diagnostics:
+        out[1]["lam_L"], out[1]["lam_R"] = lam_L, lam_R
+    return out
+
+
 def soap_step_batched(states, Gs, t: int, **hp):
     """The batched entry point is B independent single-matrix steps."""
     return [soap_step(st, G, t, **hp) for st, G in zip(states, Gs)]
+
+
+def kl_soap_step_batched(states, Gs, t: int, **hp):
+    """The batched KL entry point is B independent single-matrix KL steps."""
+    return [kl_soap_step(st, G, t, **hp) for st, G in zip(states, Gs)]
