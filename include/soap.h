@@ -101,6 +101,36 @@ int soap_step_batched(int64_t batch, float *param, const float *grad, float *L, 
                       int64_t step, uint32_t flags, void *workspace, size_t workspace_bytes,
                       hipStream_t stream);
 
+/* ---- KL-SOAP (the variant the paper recommends: Sections 5.4.3 and 7) ----
+ * One KL-SOAP step replaces step 1 of soap_step by the KL-Shampoo accumulation
+ * of Algorithm 2.  With the bases and factors of the previous step:
+ *
+ *   lambda_L = diag(Q_L^T L Q_L),   lambda_R = diag(Q_R^T R Q_R)
+ *   L <- bk L + (1-bk)/n  G Q_R diag(1/(lambda_R+eps)) Q_R^T G^T
+ *   R <- bk R + (1-bk)/m  G^T Q_L diag(1/(lambda_L+eps)) Q_L^T G
+ *
+ * (bk = beta_kron; n = "out", m = "in").  Readings of Algorithm 2: bk
+ * multiplies the old factor, as every EMA of the Section 2 primer does; the
+ * exponent on (lambda + eps) is -1, the inverse that the KL-Shampoo rule of
+ * Appendix A.3 uses; the estimates act in the basis that measured them, so
+ * the weight is the other factor's inverse as that basis diagonalises it.
+ * Steps 2-5 are those of soap_step; eps serves both the eigenvalue floor and
+ * Adam (hyperparameter table of Section 5.4).  Arguments, layout, ownership
+ * and errors as for soap_step, except that L and R must hold both triangles
+ * on entry (the estimates read the whole stored factor; every step leaves
+ * them symmetric); beta_kron must lie in [0, 1).  The workspace is larger
+ * than soap_step's (one more m x n buffer and the estimates). */
+size_t soap_kl_workspace_bytes(int64_t batch, int64_t m, int64_t n);
+int soap_kl_step(float *param, const float *grad, float *L, float *R, float *Q_L, float *Q_R,
+                 float *M, float *V, int64_t m, int64_t n, float beta1, float beta2,
+                 float beta_kron, float eps, float lr, float weight_decay, int64_t step,
+                 uint32_t flags, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int soap_kl_step_batched(int64_t batch, float *param, const float *grad, float *L, float *R,
+                         float *Q_L, float *Q_R, float *M, float *V, int64_t m, int64_t n,
+                         float beta1, float beta2, float beta_kron, float eps, float lr,
+                         float weight_decay, int64_t step, uint32_t flags, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream);
+
 /* Description of the last failure on the calling thread ("" after success).
  * Valid until the next call on the same thread. */
 const char *soap_last_error(void);
@@ -129,6 +159,18 @@ int soap_gemm_f32(int trans_a, int trans_b, int64_t M, int64_t N, int64_t K, flo
 int soap_factor_ema_f32(int trans, int64_t m, int64_t n, const float *G, float *F, float beta,
                         hipStream_t stream);
 
+/* KL-Shampoo accumulation alone (step 1 of soap_kl_step) for one m x n
+ * gradient G: L (m x m) and R (n x n) are read whole (both triangles; the
+ * new term is added to the lower triangle) and written fully symmetric; Q_L,
+ * Q_R (the previous step's bases) are read only.  lam_L (m floats) and lam_R (n floats), if not NULL, receive the
+ * eigenvalue estimates diag(Q_L^T L Q_L), diag(Q_R^T R Q_R) of the factors
+ * as they were on entry.  All pointers are device pointers; the workspace
+ * (soap_kl_factors_workspace_bytes) is the caller's. */
+size_t soap_kl_factors_workspace_bytes(int64_t m, int64_t n);
+int soap_kl_factors_f32(int64_t m, int64_t n, const float *G, float *L, float *R,
+                        const float *Q_L, const float *Q_R, float beta_kron, float eps,
+                        float *lam_L, float *lam_R, void *workspace, size_t workspace_bytes,
+                        hipStream_t stream);
 /* ---- measurement ---- */
 
 /* When enabled, every stage of soap_step / soap_step_batched records a pair

@@ -33,6 +33,8 @@ EXPORTED = [
     "soap_last_error", "soap_qr_workspace_bytes", "soap_qr_f32", "soap_gemm_f32",
     "soap_factor_ema_f32", "soap_timing_enable", "soap_timing_num_stages",
     "soap_timing_stage_name", "soap_timing_collect", "soap_timing_reset", "soap_timing_get",
+    "soap_kl_workspace_bytes", "soap_kl_step", "soap_kl_step_batched",
+    "soap_kl_factors_workspace_bytes", "soap_kl_factors_f32",
 ]
 
 
@@ -67,6 +69,14 @@ def lib() -> ctypes.CDLL:
                              _I64, _U32, _P, _SZ, _P]),
         "soap_step_batched": (_INT, [_I64, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F,
                                      _F, _F, _F, _I64, _U32, _P, _SZ, _P]),
+        "soap_kl_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
+        "soap_kl_step": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _F, _F,
+                                _F, _I64, _U32, _P, _SZ, _P]),
+        "soap_kl_step_batched": (_INT, [_I64, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F,
+                                        _F, _F, _F, _F, _F, _I64, _U32, _P, _SZ, _P]),
+        "soap_kl_factors_workspace_bytes": (_SZ, [_I64, _I64]),
+        "soap_kl_factors_f32": (_INT, [_I64, _I64, _P, _P, _P, _P, _P, _F, _F, _P, _P, _P, _SZ,
+                                       _P]),
         "soap_last_error": (ctypes.c_char_p, []),
         "soap_qr_workspace_bytes": (_SZ, [_I64]),
         "soap_qr_f32": (_INT, [_I64, _P, _P, _P, _P, _SZ, _P]),
@@ -155,6 +165,38 @@ def soap_step_batched(batch, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, bet
                                    _stream(stream)))
 
 
+def soap_kl_workspace_bytes(batch: int, m: int, n: int) -> int:
+    return lib().soap_kl_workspace_bytes(batch, m, n)
+
+
+def soap_kl_step(param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, beta_kron, eps, lr,
+                 weight_decay, step, flags, workspace, workspace_bytes, stream=None) -> None:
+    _check(lib().soap_kl_step(_ptr(param), _ptr(grad), _ptr(L), _ptr(R), _ptr(Q_L), _ptr(Q_R),
+                              _ptr(M), _ptr(V), m, n, beta1, beta2, beta_kron, eps, lr,
+                              weight_decay, step, flags, _ptr(workspace), workspace_bytes,
+                              _stream(stream)))
+
+
+def soap_kl_step_batched(batch, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, beta_kron,
+                         eps, lr, weight_decay, step, flags, workspace, workspace_bytes,
+                         stream=None) -> None:
+    _check(lib().soap_kl_step_batched(batch, _ptr(param), _ptr(grad), _ptr(L), _ptr(R),
+                                      _ptr(Q_L), _ptr(Q_R), _ptr(M), _ptr(V), m, n, beta1, beta2,
+                                      beta_kron, eps, lr, weight_decay, step, flags,
+                                      _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def soap_kl_factors_workspace_bytes(m: int, n: int) -> int:
+    return lib().soap_kl_factors_workspace_bytes(m, n)
+
+
+def soap_kl_factors_f32(m, n, G, L, R, Q_L, Q_R, beta_kron, eps, lam_L, lam_R, workspace,
+                        workspace_bytes, stream=None) -> None:
+    _check(lib().soap_kl_factors_f32(m, n, _ptr(G), _ptr(L), _ptr(R), _ptr(Q_L), _ptr(Q_R),
+                                     beta_kron, eps, _ptr(lam_L), _ptr(lam_R), _ptr(workspace),
+                                     workspace_bytes, _stream(stream)))
+
+
 def soap_qr_f32(n, A, Q, Rf, workspace, workspace_bytes, stream=None) -> None:
     _check(lib().soap_qr_f32(n, _ptr(A), _ptr(Q), _ptr(Rf), _ptr(workspace), workspace_bytes,
                              _stream(stream)))
@@ -201,9 +243,11 @@ def soap_timing_get(stage: int):
 # ---------------------------------------------------------------- helpers
 class SoapState:
     """Device-resident SOAP state for `batch` m x n matrices (fp32, contiguous),
-    allocated with torch and initialised by soap_init_state."""
+    allocated with torch and initialised by soap_init_state.  With ``kl`` the
+    step is KL-SOAP (soap_kl_step), whose coefficient ``beta_kron`` step()
+    then takes."""
 
-    def __init__(self, m: int, n: int, batch: int = 1, device: str = "cuda"):
+    def __init__(self, m: int, n: int, batch: int = 1, device: str = "cuda", kl: bool = False):
         import torch
         self.m, self.n, self.batch = m, n, batch
         shp = (lambda r, c: (batch, r, c)) if batch > 1 else (lambda r, c: (r, c))
@@ -214,12 +258,28 @@ class SoapState:
         self.Q_R = torch.empty(shp(n, n), **kw)
         self.M = torch.empty(shp(m, n), **kw)
         self.V = torch.empty(shp(m, n), **kw)
-        self.ws_bytes = soap_workspace_bytes(batch, m, n)
+        self.kl = kl
+        self.ws_bytes = (soap_kl_workspace_bytes if kl else soap_workspace_bytes)(batch, m, n)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         soap_init_state(batch, m, n, self.L, self.R, self.Q_L, self.Q_R, self.M, self.V)
 
     def step(self, param, grad, t: int, beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3,
-             weight_decay=0.1, flags=0, stream=None) -> None:
+             weight_decay=0.1, flags=0, stream=None, beta_kron=None) -> None:
+        if self.kl:
+            if beta_kron is None:
+                raise ValueError("a KL-SOAP state needs beta_kron")
+            if self.batch == 1:
+                soap_kl_step(param, grad, self.L, self.R, self.Q_L, self.Q_R, self.M, self.V,
+                             self.m, self.n, beta1, beta2, beta_kron, eps, lr, weight_decay, t,
+                             flags, self.workspace, self.ws_bytes, stream)
+            else:
+                soap_kl_step_batched(self.batch, param, grad, self.L, self.R, self.Q_L, self.Q_R,
+                                     self.M, self.V, self.m, self.n, beta1, beta2, beta_kron, eps,
+                                     lr, weight_decay, t, flags, self.workspace, self.ws_bytes,
+                                     stream)
+            return
+        if beta_kron is not None:
+            raise ValueError("beta_kron applies to KL-SOAP states only")
         if self.batch == 1:
             soap_step(param, grad, self.L, self.R, self.Q_L, self.Q_R, self.M, self.V, self.m,
                       self.n, beta1, beta2, eps, lr, weight_decay, t, flags, self.workspace,

@@ -76,6 +76,20 @@ hipError_t launch_zero_u32(uint32_t *p, int64_t count, hipStream_t s);
 // Copy `count` floats.
 hipError_t launch_copy(float *dst, const float *src, int64_t count, hipStream_t s);
 
+// ------------------------------------------------------------ KL factors
+// lambda[b][k] = sum_i X[b][k][i] Q[b][i][k] for `batch` d x d row-major X, Q
+// (element stride d*d): the diagonal of X Q, i.e. diag(Q^T F Q) when
+// X = Q^T F.  `part` holds diag_partial_floats(batch, d) floats of partial sums.
+int diag_chunks(int64_t batch, int64_t d);
+size_t diag_partial_floats(int64_t batch, int64_t d);
+hipError_t launch_diag_of_product(const float *X, const float *Q, int64_t batch, int64_t d,
+                                  float *part, float *lam, hipStream_t s);
+// Z = Y diag(1/(lambda+eps)) (by_row = 0; lambda has `cols` entries per
+// matrix) or Z = diag(1/(lambda+eps)) Y (by_row = 1; `rows` entries), for
+// `batch` contiguous rows x cols matrices.
+hipError_t launch_kl_scale(const float *Y, float *Z, const float *lam, int64_t batch,
+                           int64_t rows, int64_t cols, int by_row, float eps, hipStream_t s);
+
 // ----------------------------------------------------------------- QR
 // Blocked Householder QR of `batch` n x n matrices A, each given TRANSPOSED:
 // At = A^T row-major (element stride n*n between matrices).  At is overwritten

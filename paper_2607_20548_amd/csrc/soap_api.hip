@@ -52,13 +52,21 @@ enum Stage {
   ST_ROT_IN_R_ADAM,
   ST_ROT_OUT_L,
   ST_ROT_OUT_R_UPDATE,
+  ST_KL_EIG_L,
+  ST_KL_EIG_R,
+  ST_KL_PROJ_L,
+  ST_KL_PROJ_R,
+  ST_KL_FACTOR_L,
+  ST_KL_FACTOR_R,
   ST_COUNT
 };
 
 const char *kStageNames[ST_COUNT] = {
     "momentum_ema",     "factor_ema_L",    "factor_ema_R",  "power_L",
     "power_R",          "qr_L",            "qr_R",          "rotate_in_QLt",
-    "rotate_in_QR_adam", "rotate_out_QL",  "rotate_out_QRt_update"};
+    "rotate_in_QR_adam", "rotate_out_QL",  "rotate_out_QRt_update", "kl_eig_L",
+    "kl_eig_R",         "kl_proj_L",       "kl_proj_R",     "kl_factor_L",
+    "kl_factor_R"};
 
 struct Pending {
   int stage;
@@ -151,11 +159,14 @@ hipError_t aux_stream(int which, hipStream_t *out) {
 }
 
 // ------------------------------------------------------------- workspace
+// The KL step adds one m x n buffer, the eigenvalue estimates and their
+// partial sums; the QR workspaces stay last (each QR uses up to the next
+// region, the R side up to the end).
 struct StepLayout {
-  size_t al, ar, tg, tm, nb, qrl, qrr, total;
+  size_t al, ar, tg, tm, nb, kz, laml, lamr, partl, partr, qrl, qrr, total;
 };
 
-StepLayout step_layout(int64_t batch, int64_t m, int64_t n) {
+StepLayout step_layout(int64_t batch, int64_t m, int64_t n, bool kl) {
   StepLayout L{};
   const size_t f = sizeof(float);
   size_t o = 0;
@@ -164,10 +175,135 @@ StepLayout step_layout(int64_t batch, int64_t m, int64_t n) {
   L.tg = o; o = align256(o + f * batch * m * n);
   L.tm = o; o = align256(o + f * batch * m * n);
   L.nb = o; o = align256(o + f * batch * m * n);
+  if (kl) {
+    L.kz = o; o = align256(o + f * batch * m * n);
+    L.laml = o; o = align256(o + f * batch * m);
+    L.lamr = o; o = align256(o + f * batch * n);
+    L.partl = o; o = align256(o + f * soap::diag_partial_floats(batch, m));
+    L.partr = o; o = align256(o + f * soap::diag_partial_floats(batch, n));
+  }
   L.qrl = o; o = align256(o + soap::qr_workspace_bytes(batch, m));
   L.qrr = o; o = align256(o + soap::qr_workspace_bytes(batch, n));
   L.total = o;
   return L;
+}
+
+// Workspace of the KL accumulation alone (soap_kl_factors_f32).
+struct KlLayout {
+  size_t xl, xr, yl, zl, yr, zr, laml, lamr, partl, partr, total;
+};
+
+KlLayout kl_layout(int64_t m, int64_t n) {
+  KlLayout L{};
+  const size_t f = sizeof(float);
+  size_t o = 0;
+  L.xl = o; o = align256(o + f * m * m);
+  L.xr = o; o = align256(o + f * n * n);
+  L.yl = o; o = align256(o + f * m * n);
+  L.zl = o; o = align256(o + f * m * n);
+  L.yr = o; o = align256(o + f * m * n);
+  L.zr = o; o = align256(o + f * m * n);
+  L.laml = o; o = align256(o + f * m);
+  L.lamr = o; o = align256(o + f * n);
+  L.partl = o; o = align256(o + f * soap::diag_partial_floats(1, m));
+  L.partr = o; o = align256(o + f * soap::diag_partial_floats(1, n));
+  L.total = o;
+  return L;
+}
+
+// ------------------------------------------------- KL-Shampoo accumulation
+// Buffers of the accumulation: X = Q^T F of each side (d x d), the projected
+// gradients Y_L = Q_L^T G, Y_R = G Q_R and their inverse-eigenvalue-scaled
+// copies Z (m x n), the estimates lambda and the diagonal's partial sums.
+struct KlBufs {
+  float *XL, *XR, *YL, *ZL, *YR, *ZR, *lamL, *lamR, *partL, *partR;
+};
+
+// Algorithm 2's KL-Shampoo accumulation, enqueued on two streams: the L side
+// (sl) and the R side (s).  With the previous step's bases,
+//   lambda_L = diag(Q_L^T L Q_L),   lambda_R = diag(Q_R^T R Q_R),
+//   L <- bk L + (1-bk)/n  Y_R diag(1/(lambda_R+eps)) Y_R^T,   Y_R = G Q_R,
+//   R <- bk R + (1-bk)/m  Y_L^T diag(1/(lambda_L+eps)) Y_L,   Y_L = Q_L^T G,
+// i.e. each factor's new term weighs G by the other factor's inverse as its
+// basis diagonalises it.  Cross-stream order: ev_lamr (s -> sl) carries
+// lambda_R, ev_zl (sl -> s) carries Y_L and Z_L; ev_yr is recorded on sl once
+// Q_R has been read, and the caller must make Q_R's writer wait for it.
+// Returns the failing step's name in *where.
+hipError_t kl_accumulate(int64_t batch, int64_t m, int64_t n, const float *G, float *L, float *R,
+                         const float *QL, const float *QR, float bk, float eps, const KlBufs &b,
+                         hipStream_t s, hipStream_t sl, hipEvent_t ev_lamr, hipEvent_t ev_zl,
+                         hipEvent_t ev_yr, const char **where) {
+  const int64_t mn = m * n, mm = m * m, nn = n * n;
+  const double B = (double)batch, md = (double)m, nd = (double)n;
+  hipError_t e;
+  {  // X_L = Q_L^T L, lambda_L = diag(X_L Q_L)
+    StageScope sc(ST_KL_EIG_L, B * 2.0 * md * md * md, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = m; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
+    d.C = b.XL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) { *where = "KL eigenvalues L"; return e; }
+    if ((e = soap::launch_diag_of_product(b.XL, QL, batch, m, b.partL, b.lamL, sl)) != hipSuccess) {
+      *where = "KL eigenvalues L"; return e;
+    }
+  }
+  {  // Y_L = Q_L^T G, Z_L = diag(1/(lambda_L+eps)) Y_L
+    StageScope sc(ST_KL_PROJ_L, B * 2.0 * md * md * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = G; d.ldb = n; d.sB = mn;
+    d.C = b.YL; d.ldc = n; d.sC = mn; d.batch = batch;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) { *where = "KL projection L"; return e; }
+    if ((e = soap::launch_kl_scale(b.YL, b.ZL, b.lamL, batch, m, n, 1, eps, sl)) != hipSuccess) {
+      *where = "KL scaling L"; return e;
+    }
+  }
+  if ((e = hipEventRecord(ev_zl, sl)) != hipSuccess) { *where = "KL event"; return e; }
+  {  // X_R = Q_R^T R, lambda_R = diag(X_R Q_R)
+    StageScope sc(ST_KL_EIG_R, B * 2.0 * nd * nd * nd, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = n;
+    d.A = QR; d.lda = n; d.sA = nn; d.B = R; d.ldb = n; d.sB = nn;
+    d.C = b.XR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) { *where = "KL eigenvalues R"; return e; }
+    if ((e = soap::launch_diag_of_product(b.XR, QR, batch, n, b.partR, b.lamR, s)) != hipSuccess) {
+      *where = "KL eigenvalues R"; return e;
+    }
+  }
+  if ((e = hipEventRecord(ev_lamr, s)) != hipSuccess) { *where = "KL event"; return e; }
+  if ((e = hipStreamWaitEvent(sl, ev_lamr, 0)) != hipSuccess) { *where = "KL event"; return e; }
+  {  // Y_R = G Q_R, Z_R = Y_R diag(1/(lambda_R+eps))
+    StageScope sc(ST_KL_PROJ_R, B * 2.0 * md * nd * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 0; d.M = m; d.N = n; d.K = n;
+    d.A = G; d.lda = n; d.sA = mn; d.B = QR; d.ldb = n; d.sB = nn;
+    d.C = b.YR; d.ldc = n; d.sC = mn; d.batch = batch;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) { *where = "KL projection R"; return e; }
+    if ((e = hipEventRecord(ev_yr, sl)) != hipSuccess) { *where = "KL event"; return e; }
+    if ((e = soap::launch_kl_scale(b.YR, b.ZR, b.lamR, batch, m, n, 0, eps, sl)) != hipSuccess) {
+      *where = "KL scaling R"; return e;
+    }
+  }
+  {  // L <- bk L + (1-bk)/n Y_R Z_R^T (lower triangle, mirrored)
+    StageScope sc(ST_KL_FACTOR_L, B * md * (md + 1) * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
+    d.A = b.YR; d.lda = n; d.sA = mn; d.B = b.ZR; d.ldb = n; d.sB = mn;
+    d.C = L; d.ldc = m; d.sC = mm; d.alpha = (float)((1.0 - (double)bk) / nd); d.beta = bk;
+    d.batch = batch;
+    if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) { *where = "KL factor L"; return e; }
+  }
+  if ((e = hipStreamWaitEvent(s, ev_zl, 0)) != hipSuccess) { *where = "KL event"; return e; }
+  {  // R <- bk R + (1-bk)/m Y_L^T Z_L
+    StageScope sc(ST_KL_FACTOR_R, B * nd * (nd + 1) * md, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
+    d.A = b.YL; d.lda = n; d.sA = mn; d.B = b.ZL; d.ldb = n; d.sB = mn;
+    d.C = R; d.ldc = n; d.sC = nn; d.alpha = (float)((1.0 - (double)bk) / md); d.beta = bk;
+    d.batch = batch;
+    if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) { *where = "KL factor R"; return e; }
+  }
+  return hipSuccess;
 }
 
 struct Range {
@@ -199,10 +335,29 @@ int check_hparams(float beta1, float beta2, float eps, float lr, float wd, int64
   return SOAP_OK;
 }
 
+// Owns the events of one step; destroys whichever were created.
+struct StepEvents {
+  static constexpr int kCount = 6;
+  hipEvent_t ev[kCount] = {};
+  hipError_t create() {
+    for (hipEvent_t &e : ev) {
+      hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+      if (r != hipSuccess) return r;
+    }
+    return hipSuccess;
+  }
+  ~StepEvents() {
+    for (hipEvent_t e : ev)
+      if (e) (void)hipEventDestroy(e);
+  }
+};
+
+// One SOAP step (kl = false: factor EMA of the Section 2 primer) or KL-SOAP
+// step (kl = true: KL-Shampoo accumulation with coefficient beta_kron).
 int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R, float *QL,
               float *QR, float *M, float *V, int64_t m, int64_t n, float beta1, float beta2,
               float eps, float lr, float wd, int64_t step, uint32_t flags, void *ws,
-              size_t ws_bytes, hipStream_t s) {
+              size_t ws_bytes, hipStream_t s, bool kl, float beta_kron) {
   if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n))
     return fail(SOAP_ERR_SHAPE, "batch=%lld m=%lld n=%lld: each must be in [1, %d]",
                 (long long)batch, (long long)m, (long long)n, SOAP_MAX_DIM);
@@ -216,7 +371,9 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if (!b.p) return fail(SOAP_ERR_NULL, "%s is NULL", b.name);
   int rc = check_hparams(beta1, beta2, eps, lr, wd, step, flags);
   if (rc != SOAP_OK) return rc;
-  const StepLayout lay = step_layout(batch, m, n);
+  if (kl && (!std::isfinite(beta_kron) || beta_kron < 0.f || beta_kron >= 1.f))
+    return fail(SOAP_ERR_HPARAM, "beta_kron = %g is outside [0, 1)", (double)beta_kron);
+  const StepLayout lay = step_layout(batch, m, n, kl);
   if (ws_bytes < lay.total)
     return fail(SOAP_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
   for (const Range &b : bufs)
@@ -252,35 +409,35 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   }
   // Fork: the L side on the auxiliary stream, the R side on the caller's.
   hipStream_t sl = nullptr, spl = nullptr, spr = nullptr;
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr, ev_power = nullptr;
   if ((e = aux_stream(0, &sl)) != hipSuccess || (e = aux_stream(1, &spl)) != hipSuccess ||
       (e = aux_stream(2, &spr)) != hipSuccess)
     return hip_fail(e, "auxiliary stream");
-  if ((e = hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming)) != hipSuccess)
-    return hip_fail(e, "event");
-  if ((e = hipEventCreateWithFlags(&ev_join, hipEventDisableTiming)) != hipSuccess) {
-    (void)hipEventDestroy(ev_fork);
-    return hip_fail(e, "event");
-  }
-  if ((e = hipEventCreateWithFlags(&ev_power, hipEventDisableTiming)) != hipSuccess) {
-    (void)hipEventDestroy(ev_fork);
-    (void)hipEventDestroy(ev_join);
-    return hip_fail(e, "event");
-  }
-  struct EventGuard {
-    hipEvent_t a, b, c;
-    ~EventGuard() { (void)hipEventDestroy(a); (void)hipEventDestroy(b); (void)hipEventDestroy(c); }
-  } guard{ev_fork, ev_join, ev_power};
+  StepEvents evs;
+  if ((e = evs.create()) != hipSuccess) return hip_fail(e, "event");
+  hipEvent_t ev_fork = evs.ev[0], ev_join = evs.ev[1], ev_power = evs.ev[2];
+  hipEvent_t ev_lamr = evs.ev[3], ev_zl = evs.ev[4], ev_yr = evs.ev[5];
   if ((e = hipEventRecord(ev_fork, s)) != hipSuccess) return hip_fail(e, "fork record");
   if ((e = hipStreamWaitEvent(sl, ev_fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
-  {  // L <- b2 L + (1-b2) G G^T
+  if (kl) {
+    // KL-Shampoo accumulation; its buffers are dead before the stages that
+    // reuse them (A_L, A_R: the power products; T_G, T_M: written on the L
+    // stream after the join with the R-side power product; N: after the join).
+    const KlBufs kb{AL, AR, TG, TM, NN, reinterpret_cast<float *>(w + lay.kz),
+                    reinterpret_cast<float *>(w + lay.laml), reinterpret_cast<float *>(w + lay.lamr),
+                    reinterpret_cast<float *>(w + lay.partl), reinterpret_cast<float *>(w + lay.partr)};
+    const char *where = "";
+    if ((e = kl_accumulate(batch, m, n, grad, L, R, QL, QR, beta_kron, eps, kb, s, sl, ev_lamr,
+                           ev_zl, ev_yr, &where)) != hipSuccess)
+      return hip_fail(e, where);
+  } else {  // L <- b2 L + (1-b2) G G^T
     StageScope sc(ST_FACTOR_L, B * md * (md + 1) * nd, sl);
     soap::GemmDesc d;
     d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
     d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
     d.C = L; d.ldc = m; d.sC = mm; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
     if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "factor EMA L");
-  }  // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L since
+  }
+  // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L since
   // L is symmetric (both triangles are stored).
   {  // A_L^T = Q_L^T L
     StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, sl);
@@ -290,7 +447,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "power L");
   }
-  {  // R <- b2 R + (1-b2) G^T G
+  if (!kl) {  // R <- b2 R + (1-b2) G^T G
     StageScope sc(ST_FACTOR_R, B * nd * (nd + 1) * md, s);
     soap::GemmDesc d;
     d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
@@ -328,6 +485,8 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
   }
   if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
+  // The KL projection G Q_R on the L stream reads the old Q_R.
+  if (kl && (e = hipStreamWaitEvent(s, ev_yr, 0)) != hipSuccess) return hip_fail(e, "KL wait");
   {  // Q_R = QR(A_R).Q
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
     if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl)) != hipSuccess)
@@ -367,7 +526,7 @@ extern "C" {
 
 size_t soap_workspace_bytes(int64_t batch, int64_t m, int64_t n) {
   if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n)) return 0;
-  return step_layout(batch, m, n).total;
+  return step_layout(batch, m, n, false).total;
 }
 
 int soap_init_state(int64_t batch, int64_t m, int64_t n, float *L, float *R, float *Q_L,
@@ -393,7 +552,7 @@ int soap_step(float *param, const float *grad, float *L, float *R, float *Q_L, f
               float lr, float weight_decay, int64_t step, uint32_t flags, void *workspace,
               size_t workspace_bytes, hipStream_t stream) {
   return step_impl(1, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
-                   weight_decay, step, flags, workspace, workspace_bytes, stream);
+                   weight_decay, step, flags, workspace, workspace_bytes, stream, false, 0.f);
 }
 
 int soap_step_batched(int64_t batch, float *param, const float *grad, float *L, float *R,
@@ -402,7 +561,78 @@ int soap_step_batched(int64_t batch, float *param, const float *grad, float *L, 
                       int64_t step, uint32_t flags, void *workspace, size_t workspace_bytes,
                       hipStream_t stream) {
   return step_impl(batch, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
-                   weight_decay, step, flags, workspace, workspace_bytes, stream);
+                   weight_decay, step, flags, workspace, workspace_bytes, stream, false, 0.f);
+}
+
+size_t soap_kl_workspace_bytes(int64_t batch, int64_t m, int64_t n) {
+  if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n)) return 0;
+  return step_layout(batch, m, n, true).total;
+}
+
+int soap_kl_step(float *param, const float *grad, float *L, float *R, float *Q_L, float *Q_R,
+                 float *M, float *V, int64_t m, int64_t n, float beta1, float beta2,
+                 float beta_kron, float eps, float lr, float weight_decay, int64_t step,
+                 uint32_t flags, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  return step_impl(1, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
+                   weight_decay, step, flags, workspace, workspace_bytes, stream, true, beta_kron);
+}
+
+int soap_kl_step_batched(int64_t batch, float *param, const float *grad, float *L, float *R,
+                         float *Q_L, float *Q_R, float *M, float *V, int64_t m, int64_t n,
+                         float beta1, float beta2, float beta_kron, float eps, float lr,
+                         float weight_decay, int64_t step, uint32_t flags, void *workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+  return step_impl(batch, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
+                   weight_decay, step, flags, workspace, workspace_bytes, stream, true, beta_kron);
+}
+
+size_t soap_kl_factors_workspace_bytes(int64_t m, int64_t n) {
+  if (!dim_ok(m) || !dim_ok(n)) return 0;
+  return kl_layout(m, n).total;
+}
+
+int soap_kl_factors_f32(int64_t m, int64_t n, const float *G, float *L, float *R,
+                        const float *Q_L, const float *Q_R, float beta_kron, float eps,
+                        float *lam_L, float *lam_R, void *workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+  if (!dim_ok(m) || !dim_ok(n))
+    return fail(SOAP_ERR_SHAPE, "m=%lld n=%lld: each must be in [1, %d]", (long long)m,
+                (long long)n, SOAP_MAX_DIM);
+  if (!std::isfinite(beta_kron) || beta_kron < 0.f || beta_kron >= 1.f)
+    return fail(SOAP_ERR_HPARAM, "beta_kron = %g is outside [0, 1)", (double)beta_kron);
+  if (!std::isfinite(eps) || eps < 0.f)
+    return fail(SOAP_ERR_HPARAM, "eps = %g must be finite and >= 0", (double)eps);
+  const Range bufs[] = {{G, sizeof(float) * m * n, "G"},     {L, sizeof(float) * m * m, "L"},
+                        {R, sizeof(float) * n * n, "R"},     {Q_L, sizeof(float) * m * m, "Q_L"},
+                        {Q_R, sizeof(float) * n * n, "Q_R"}, {workspace, workspace_bytes, "workspace"}};
+  for (const Range &b : bufs)
+    if (!b.p) return fail(SOAP_ERR_NULL, "%s is NULL", b.name);
+  const KlLayout lay = kl_layout(m, n);
+  if (workspace_bytes < lay.total)
+    return fail(SOAP_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", workspace_bytes, lay.total);
+  for (const Range &b : bufs)
+    if (!aligned16(b.p)) return fail(SOAP_ERR_ALIGN, "%s is not 16-byte aligned", b.name);
+  std::vector<Range> all(bufs, bufs + 6);
+  if (lam_L) all.push_back({lam_L, sizeof(float) * m, "lam_L"});
+  if (lam_R) all.push_back({lam_R, sizeof(float) * n, "lam_R"});
+  for (size_t i = 0; i < all.size(); ++i)
+    for (size_t j = i + 1; j < all.size(); ++j)
+      if (overlap(all[i], all[j]))
+        return fail(SOAP_ERR_ALIAS, "%s overlaps %s", all[i].name, all[j].name);
+  char *w = static_cast<char *>(workspace);
+  auto at = [&](size_t off) { return reinterpret_cast<float *>(w + off); };
+  const KlBufs kb{at(lay.xl), at(lay.xr), at(lay.yl), at(lay.zl), at(lay.yr), at(lay.zr),
+                  lam_L ? lam_L : at(lay.laml), lam_R ? lam_R : at(lay.lamr), at(lay.partl),
+                  at(lay.partr)};
+  StepEvents evs;
+  hipError_t e = evs.create();
+  if (e != hipSuccess) return hip_fail(e, "event");
+  const char *where = "";
+  // Both sides on the caller's stream: the events then order nothing new.
+  if ((e = kl_accumulate(1, m, n, G, L, R, Q_L, Q_R, beta_kron, eps, kb, stream, stream,
+                         evs.ev[0], evs.ev[1], evs.ev[2], &where)) != hipSuccess)
+    return hip_fail(e, where);
+  return ok();
 }
 
 const char *soap_last_error(void) { return g_err; }

@@ -117,3 +117,58 @@ def test_success_clears_error(L):
     assert soap.soap_last_error() != ""
     soap.soap_timing_reset()   # a call that succeeds without touching the GPU
     assert L.soap_workspace_bytes(1, 4, 4) > 0
+
+
+def call_kl_step(L, a, beta_kron=0.95, batch=None):
+    args = (a["param"], a["grad"], a["L"], a["R"], a["Q_L"], a["Q_R"], a["M"], a["V"], a["m"],
+            a["n"], a["beta1"], a["beta2"], beta_kron, a["eps"], a["lr"], a["weight_decay"],
+            a["step"], a["flags"], a["workspace"], a["workspace_bytes"], None)
+    if batch is None:
+        return L.soap_kl_step(*args)
+    return L.soap_kl_step_batched(batch, *args)
+
+
+@pytest.mark.parametrize("over,beta_kron,code", [
+    (dict(), 1.0, soap.SOAP_ERR_HPARAM),
+    (dict(), -0.5, soap.SOAP_ERR_HPARAM),
+    (dict(), float("nan"), soap.SOAP_ERR_HPARAM),
+    (dict(L=None), 0.95, soap.SOAP_ERR_NULL),
+    (dict(m=0), 0.95, soap.SOAP_ERR_SHAPE),
+    (dict(beta1=1.0), 0.95, soap.SOAP_ERR_HPARAM),
+    (dict(grad=BASE), 0.95, soap.SOAP_ERR_ALIAS),
+])
+def test_kl_step_validation(L, over, beta_kron, code):
+    a = fake_args(ws=soap.soap_kl_workspace_bytes(1, 8, 12), **over)
+    assert call_kl_step(L, a, beta_kron) == code
+    assert soap.soap_last_error() != ""
+    assert call_kl_step(L, a, beta_kron, batch=1) == code
+
+
+def test_kl_workspace(L):
+    m, n = 8, 12
+    plain = soap.soap_workspace_bytes(1, m, n)
+    kl = soap.soap_kl_workspace_bytes(1, m, n)
+    assert kl > plain                       # one more m x n buffer and the estimates
+    assert call_kl_step(L, fake_args(ws=plain)) == soap.SOAP_ERR_WORKSPACE
+    assert soap.soap_kl_workspace_bytes(0, m, n) == 0
+    assert soap.soap_kl_factors_workspace_bytes(m, 0) == 0
+    big = soap.soap_kl_workspace_bytes(1, 4096, 14336)
+    assert big > soap.soap_workspace_bytes(1, 4096, 14336) + 4 * 4096 * 14336
+
+
+def test_kl_factors_validation(L):
+    ws = soap.soap_kl_factors_workspace_bytes(8, 12)
+    p = [BASE + i * MB for i in range(8)]
+    # G, L, R, Q_L, Q_R, lam_L, lam_R, workspace
+    assert L.soap_kl_factors_f32(8, 12, p[0], p[1], p[2], p[3], p[4], 1.0, 1e-8, None, None,
+                                 p[7], ws, None) == soap.SOAP_ERR_HPARAM
+    assert L.soap_kl_factors_f32(8, 12, p[0], p[1], p[2], p[3], p[4], 0.9, -1.0, None, None,
+                                 p[7], ws, None) == soap.SOAP_ERR_HPARAM
+    assert L.soap_kl_factors_f32(8, 12, None, p[1], p[2], p[3], p[4], 0.9, 1e-8, None, None,
+                                 p[7], ws, None) == soap.SOAP_ERR_NULL
+    assert L.soap_kl_factors_f32(8, 12, p[0], p[1], p[2], p[3], p[4], 0.9, 1e-8, None, None,
+                                 p[7], ws - 1, None) == soap.SOAP_ERR_WORKSPACE
+    assert L.soap_kl_factors_f32(8, 12, p[0], p[1], p[2], p[3], p[4], 0.9, 1e-8, p[1] + 64,
+                                 None, p[7], ws, None) == soap.SOAP_ERR_ALIAS
+    assert L.soap_kl_factors_f32(8, 12, p[0], p[1] + 4, p[2], p[3], p[4], 0.9, 1e-8, None, None,
+                                 p[7], ws, None) == soap.SOAP_ERR_ALIGN

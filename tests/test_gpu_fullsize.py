@@ -20,7 +20,8 @@ expert bank full oracle parity on two experts.
 import numpy as np
 import pytest
 
-from tests.gpu_helpers import dev, host, rel, log, adam_fp32_bound, column_signs_agree
+from tests.gpu_helpers import (dev, host, rel, log, column_signs_agree, check_factor_ema_sampled,
+                                check_refresh_adam_sampled)
 
 pytestmark = pytest.mark.gpu
 
@@ -45,56 +46,8 @@ def _snap(gs, W, b=None):
 
 def _sampled_step_checks(pre, post, G, t, rng, nsamp=48, ncols=16):
     """All checks of one step from the GPU state `pre` to `post` (fp64 arrays)."""
-    b1, b2, eps, lr, wd = (HP[k] for k in ("beta1", "beta2", "eps", "lr", "weight_decay"))
-    m, n = G.shape
-    c1, c2 = 1 - b1 ** t, 1 - b2 ** t
-    # factor EMAs, entry by entry (exact definitions)
-    for F, X, d in (("L", G, m), ("R", G.T, n)):
-        ii = rng.integers(0, d, nsamp)
-        jj = rng.integers(0, d, nsamp)
-        want = b2 * pre[F][ii, jj] + (1 - b2) * np.einsum("ij,ij->i", X[ii], X[jj])
-        got = post[F][ii, jj]
-        assert rel(got, want) <= TOL, F
-        assert np.array_equal(post[F][ii, jj], post[F][jj, ii])
-    # momentum
-    ii, jj = rng.integers(0, m, nsamp), rng.integers(0, n, nsamp)
-    assert rel(post["M"][ii, jj], b1 * pre["M"][ii, jj] + (1 - b1) * G[ii, jj]) <= TOL
-    # eigenbases: Q^T Q = I and Q^T (F Q_prev) upper triangular, positive diagonal
-    for F, Qp, Qn, d in (("L", pre["QL"], post["QL"], m), ("R", pre["QR"], post["QR"], n)):
-        cols = np.unique(np.concatenate([rng.integers(0, d, ncols), [0, d - 1]]))
-        A_cols = post[F] @ Qp[:, cols]                      # columns of F_t Q_prev
-        QtA = Qn.T @ A_cols                                 # d x len(cols)
-        colnorm = np.linalg.norm(A_cols, axis=0)
-        for k, j in enumerate(cols):
-            below = QtA[j + 1:, k]
-            assert np.linalg.norm(below) <= TOL * colnorm[k], (F, j)
-            assert QtA[j, k] > 0, (F, j)
-        ortho = Qn.T @ Qn[:, cols]
-        ortho[cols, np.arange(len(cols))] -= 1.0
-        assert np.linalg.norm(ortho) / np.sqrt(len(cols)) <= TOL, F
-    # V and N at sampled eigenbasis entries
-    QL, QR = post["QL"], post["QR"]
-    kk, ll = rng.integers(0, m, nsamp), rng.integers(0, n, nsamp)
-    Mn = post["M"]
-    GQ = G @ QR[:, ll]                 # m x nsamp
-    MQ = Mn @ QR[:, ll]
-    Gp = np.einsum("ik,ik->k", QL[:, kk], GQ)
-    Mp = np.einsum("ik,ik->k", QL[:, kk], MQ)
-    V_want = b2 * pre["V"][kk, ll] + (1 - b2) * Gp * Gp
-    assert rel(post["V"][kk, ll], V_want) <= TOL
-    N_want = (Mp / c1) / (np.sqrt(post["V"][kk, ll] / c2) + eps)
-    beta_w = float(np.float32(1.0) - np.float32(lr) * np.float32(wd))
-    dW = (beta_w * pre["W"] - post["W"]) / float(np.float32(lr))
-    N_got = np.einsum("ik,ik->k", QL[:, kk], dW @ QR[:, ll])
-    g_scale = np.linalg.norm(G, 2)
-    bound = adam_fp32_bound(N_want, post["V"][kk, ll] / c2, g_scale, eps)
-    assert np.all(np.abs(N_got - N_want) <= 1e-4 * np.abs(N_want) + bound + 1e-5)
-    well = adam_fp32_bound(N_want, post["V"][kk, ll] / c2, g_scale, eps, factor=1.0) <= 1e-2 * np.abs(N_want)
-    if well.sum() >= nsamp // 2:
-        assert rel(N_got[well], N_want[well]) <= TOL
-    # update-RMS identity (Section 5.2): ||dW||_F = ||N||_F, and dW is finite
-    assert np.all(np.isfinite(dW))
-    return {"N_rel_well": rel(N_got[well], N_want[well]) if well.any() else 0.0}
+    check_factor_ema_sampled(pre, post, G, rng, HP["beta2"], nsamp)
+    return check_refresh_adam_sampled(pre, post, G, t, rng, HP, nsamp, ncols)
 
 
 def _run_single(spec, cfg, steps_before, seed=0):

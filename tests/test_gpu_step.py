@@ -7,8 +7,7 @@ sign)."""
 import numpy as np
 import pytest
 
-from tests.gpu_helpers import (dev, host, rel, column_signs_agree, log, adam_fp32_bound,
-                                update_from_weights)
+from tests.gpu_helpers import dev, host, rel, run_open_loop
 
 pytestmark = pytest.mark.gpu
 
@@ -25,61 +24,8 @@ def _lib():
     soap.lib()
 
 
-def _compare(st, gs, tag):
-    errs = {
-        "L": rel(host(gs.L), st.L), "R": rel(host(gs.R), st.R),
-        "Q_L": rel(host(gs.Q_L), st.QL), "Q_R": rel(host(gs.Q_R), st.QR),
-        "M": rel(host(gs.M), st.M), "V": rel(host(gs.V), st.V),
-    }
-    for k, v in errs.items():
-        assert v <= TOL, (tag, k, v)
-    assert column_signs_agree(host(gs.Q_L), st.QL) and column_signs_agree(host(gs.Q_R), st.QR)
-    return errs
-
-
 def _run_open_loop(m, n, grads, W0, hp=HP, flags=0, bias_correction=True):
-    """Open loop over the given gradients.  Every step:
-      * L, R, Q_L, Q_R, M, V: relative Frobenius error <= TOL;
-      * the update N (recovered from the GPU weights): every entry within
-        1e-4 |N| plus 64x the first-order fp32 error of the eigenbasis quotient,
-        and relative Frobenius error <= TOL over the well-determined entries
-        (those whose first-order fp32 error is below 1% of |N|);
-      * W: relative Frobenius error <= TOL against the oracle's weights re-based
-        on the GPU's N at the entries that are not well determined."""
-    import paper_2607_20548_amd as soap
-    import oracle
-    gs = soap.SoapState(m, n)
-    W = dev(W0)
-    st = oracle.init_state(W0.astype(np.float64))
-    W_adj = W0.astype(np.float64)
-    lr, wd, eps = hp["lr"], hp["weight_decay"], hp["eps"]
-    g_scale = 0.0
-    for t, G in enumerate(grads, start=1):
-        W_prev = host(W)
-        gs.step(W, dev(G), t, flags=flags, **hp)
-        st, d = oracle.soap_step(st, G.astype(np.float64), t, bias_correction=bias_correction,
-                                 diagnostics=True, **hp)
-        errs = _compare(st, gs, f"{m}x{n} t={t}")
-        g_scale = max(g_scale, np.linalg.norm(G.astype(np.float64), 2))
-        Wg = host(W)
-        N_gpu = update_from_weights(W_prev, Wg, host(gs.Q_L), host(gs.Q_R), lr, wd)
-        _, c2 = oracle.bias_corrections(hp["beta1"], hp["beta2"], t, bias_correction)
-        N_ora = d["N"]
-        bound = adam_fp32_bound(N_ora, st.V / c2, g_scale, eps)
-        dN = np.abs(N_gpu - N_ora)
-        assert np.all(dN <= 1e-4 * np.abs(N_ora) + bound + 1e-6), (t, float(np.max(dN - bound)))
-        # well determined: the expected fp32 error (factor 1) is below 1% of |N|
-        well = adam_fp32_bound(N_ora, st.V / c2, g_scale, eps, factor=1.0) <= 1e-2 * np.abs(N_ora)
-        errs["N_well"] = rel(N_gpu[well], N_ora[well]) if well.any() else 0.0
-        assert errs["N_well"] <= TOL, (t, errs["N_well"])
-        N_adj = np.where(well, N_ora, N_gpu)
-        W_adj = (1.0 - lr * wd) * W_adj - lr * (st.QL @ N_adj @ st.QR.T)
-        errs["W"] = rel(Wg, W_adj)
-        errs["W_plain"] = rel(Wg, st.W)
-        log(f"{m}x{n} t={t} not_well_determined={int((~well).sum())} " +
-            " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
-        assert errs["W"] <= TOL, (t, errs["W"])
-    return gs, W, st
+    return run_open_loop(m, n, grads, W0, hp=hp, flags=flags, bias_correction=bias_correction)
 
 
 def test_workload0_ten_steps_open_loop():
