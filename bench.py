@@ -6,7 +6,11 @@ with per-step QR refresh of both eigenbases (R is 14336 x 14336).  Gradients
 are generated and copied to HBM before the timed region.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                    [--calibration-copy-mib N]
+                    [--calibration-copy-mib N] [--kl]
+
+--kl times the KL-SOAP step instead (soap_kl_step, beta_kron 0.95): the
+factors are accumulated by the KL-Shampoo rule, the rest of the step is the
+same.
 
 Prints ONE JSON line.  `value` is steps/s of the whole step; `roofline`
 describes the dominant kernel (timed with HIP events on the library's stream
@@ -28,6 +32,7 @@ sys.path.insert(0, ROOT)
 PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak (256 CU x 256 flop/clk x 2.4 GHz)
 PEAK_HBM_GBS = 8000.0
 HP = dict(beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3, weight_decay=0.1)
+BETA_KRON = 0.95   # KL-Shampoo accumulation coefficient (hyperparameter table of Section 5.4)
 
 
 def step_flops(m: int, n: int) -> float:
@@ -39,6 +44,12 @@ def step_flops(m: int, n: int) -> float:
     qr = (8.0 / 3.0) * (m ** 3 + n ** 3)
     rot = 6.0 * m * n * (m + n)
     return syrk + power + qr + rot
+
+
+def kl_step_flops(m: int, n: int) -> float:
+    """step_flops plus the KL accumulation's extra products: Q^T F for the
+    eigenvalue estimates of both factors and the projections Q_L^T G, G Q_R."""
+    return step_flops(m, n) + 2.0 * (m ** 3 + n ** 3) + 2.0 * m * n * (m + n)
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "power_product_R_4096x14336_traffic.json")
@@ -63,7 +74,7 @@ def measured_traffic():
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(m: int, n: int, rank: int, scale: int = 4):
+def cpu_baseline(m: int, n: int, rank: int, scale: int = 4, kl: bool = False):
     """Times one fp64 oracle step on the workload shrunk by `scale` per side
     (same aspect ratio, rank and noise recipe) and scales the time by
     step_flops(m, n) / step_flops(m/scale, n/scale) (= scale^3: the step's work
@@ -75,13 +86,17 @@ def cpu_baseline(m: int, n: int, rank: int, scale: int = 4):
     G = next(sg.make_matrix_stream(spec, 2, 1)).astype(np.float64)
     st = oracle.init_state(sg.initial_weight(spec, 2).astype(np.float64))
     t0 = time.perf_counter()
-    oracle.soap_step(st, G, 1, **HP)
+    if kl:
+        oracle.kl_soap_step(st, G, 1, beta_kron=BETA_KRON, **HP)
+    else:
+        oracle.soap_step(st, G, 1, **HP)
     dt = time.perf_counter() - t0
-    ratio = step_flops(m, n) / step_flops(ms, ns)
+    fl = kl_step_flops if kl else step_flops
+    ratio = fl(m, n) / fl(ms, ns)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
     return {
         "value": 1.0 / (dt * ratio), "unit": "steps/s", "cores": threads, "kind": "oracle",
-        "sample": (f"one fp64 oracle step on a {ms}x{ns} matrix (the {m}x{n} workload at 1/{scale} "
+        "sample": (f"one fp64 oracle {'KL-SOAP ' if kl else ''}step on a {ms}x{ns} matrix (the {m}x{n} workload at 1/{scale} "
                    f"per side, rank {spec.rank}, 10% noise) took {dt:.2f} s; scaled by the exact "
                    f"flop ratio {ratio:.1f}"),
     }
@@ -94,6 +109,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibration-copy-mib", type=int, default=0)
+    ap.add_argument("--kl", action="store_true", help="time the KL-SOAP step")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the SOAP step of a "
@@ -114,11 +130,12 @@ def main():
     print(f"[bench] generating {total} gradients {m}x{n}", file=sys.stderr, flush=True)
     grads = [torch.from_numpy(G).cuda() for G in sg.make_matrix_stream(spec, 2, total)]
     W = torch.from_numpy(sg.initial_weight(spec, 2)).cuda()
-    state = soap.SoapState(m, n)
+    state = soap.SoapState(m, n, kl=args.kl)
     stream = torch.cuda.current_stream()
+    extra = dict(beta_kron=BETA_KRON) if args.kl else {}
 
     for t in range(1, args.warmup + 1):
-        state.step(W, grads[t - 1], t, **HP)
+        state.step(W, grads[t - 1], t, **extra, **HP)
     torch.cuda.synchronize()
     if args.calibration_copy_mib > 0:
         nel = args.calibration_copy_mib * (1 << 20) // 4
@@ -138,7 +155,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(1, args.steps + 1):
-        state.step(W, grads[args.warmup + t - 1], t, stream=stream, **HP)
+        state.step(W, grads[args.warmup + t - 1], t, stream=stream, **extra, **HP)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     soap.soap_timing_enable(False)
@@ -156,10 +173,11 @@ def main():
     d_ms, d_n, d_fl = single[dom]
     achieved = d_fl / (d_ms / d_n * 1e-3) / d_n / 1e12
 
-    F = step_flops(m, n)
+    F = (kl_step_flops if args.kl else step_flops)(m, n)
     value = args.steps / elapsed
+    name = "KL-SOAP" if args.kl else "SOAP"
     out = {
-        "metric": "SOAP steps/s per weight shape + achieved MFMA TFLOPS fraction (1 GPU)",
+        "metric": f"{name} steps/s per weight shape + achieved MFMA TFLOPS fraction (1 GPU)",
         "value": value,
         "unit": "steps/s",
         "n_gpus": 1,
@@ -171,8 +189,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic (seeded low-rank + noise gradients, rank 128, 10% noise)",
-        "config": {"workload": f"soap_step on one {m}x{n} fp32 weight (MLP up-projection), "
-                               f"QR refresh of both factors every step",
+        "config": {"workload": f"{'soap_kl_step' if args.kl else 'soap_step'} on one {m}x{n} fp32 "
+                               f"weight (MLP up-projection), QR refresh of both factors every step"
+                               + (f", KL-Shampoo factors (beta_kron {BETA_KRON})" if args.kl else ""),
                    "m": m, "n": n, "rank": spec.rank, "global_batch": 1, "seq_len": None,
                    "parallelism": "none (1 GPU)"},
         "step_tflops": F * value / 1e12,
@@ -185,7 +204,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(m, n, spec.rank)
+        out["cpu_baseline"] = cpu_baseline(m, n, spec.rank, kl=args.kl)
     print(json.dumps(out), flush=True)
 
 

@@ -346,14 +346,22 @@ hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) 
   // A cap counts every workgroup (split slices and batch included); the
   // tile dimension stays a multiple of 8 for XCD locality.
   const int64_t per_tile = (int64_t)S * d.batch;
-  const bool capped =
-      MODE == MODE_GENERAL && d.max_wg > 0 && (int64_t)kp.ntiles * per_tile > d.max_wg;
+  const bool capped = (MODE == MODE_GENERAL || MODE == MODE_SYRK) && d.max_wg > 0 &&
+                      (int64_t)kp.ntiles * per_tile > d.max_wg;
   const int wgs = capped ? (int)std::max<int64_t>(8, (d.max_wg / per_tile) & ~int64_t(7)) : kp.ntiles;
   dim3 grid(std::min(wgs, kp.ntiles), S, (unsigned)d.batch);
 #define SOAP_LAUNCH(TA, TB, VEC, TAG) \
   hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE, TAG, 1>), grid, block, 0, s, kp)
   const int code = d.trans_a * 2 + d.trans_b;
-  if (capped) {
+  if (MODE == MODE_SYRK && capped) {
+    // the two layouts of the factor products: X X^T (0, 1) and X^T X (1, 0)
+#define SOAP_LAUNCH_SP(TA, TB, VEC) \
+  hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE_SYRK, 0, 1, true>), grid, block, 0, s, kp)
+    if (code == 1) { if (vec_ok) SOAP_LAUNCH_SP(0, 1, 4); else SOAP_LAUNCH_SP(0, 1, 1); }
+    else if (code == 2) { if (vec_ok) SOAP_LAUNCH_SP(1, 0, 4); else SOAP_LAUNCH_SP(1, 0, 1); }
+    else return hipErrorInvalidValue;
+#undef SOAP_LAUNCH_SP
+  } else if (capped) {
 #define SOAP_LAUNCH_P(TA, TB, VEC, MINB) \
   hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE_GENERAL, 0, MINB, true>), grid, block, 0, s, kp)
     const bool shortk = kp.kslice <= SHORT_K;

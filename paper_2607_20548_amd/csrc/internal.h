@@ -47,8 +47,10 @@ int choose_splitk(int64_t M, int64_t N, int64_t K, int64_t batch, int max_split)
 hipError_t launch_gemm(const GemmDesc &d, hipStream_t s);
 
 // Symmetric rank-k EMA on one triangle:  C <- beta C + alpha op(A) op(B) where
-// op(B) = op(A)^T, only tiles on or below the diagonal are computed and each
-// result is stored at (i,j) and (j,i).  C is read from its lower triangle.
+// op(A) op(B) is symmetric (op(B) = op(A)^T, or op(A) D op(A)^T with the
+// diagonal scaling folded into B), only tiles on or below the diagonal are
+// computed and each result is stored at (i,j) and (j,i).  C is read from its
+// lower triangle.  max_wg caps it like a GEMM for the layouts (0, 1) and (1, 0).
 hipError_t launch_syrk_ema(const GemmDesc &d, hipStream_t s);
 
 // Fused second rotation + Adam in the eigenbasis.  With op(A) = T_G and
@@ -98,10 +100,12 @@ hipError_t launch_kl_scale(const float *Y, float *Z, const float *lam, int64_t b
 // (row-major, strict lower part zero).  Work is ordered on stream s; the
 // block factorizations run on stream sp and the T matrices of block pairs on
 // stream st (both joined back into s with events; st may equal sp).
+// If q_free is not null, s waits for it before Q is first written (Q may
+// still be read by work on other streams until then).
 size_t qr_workspace_bytes(int64_t batch, int64_t n);
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
-                                hipStream_t st);
+                                hipStream_t st, hipEvent_t q_free = nullptr);
 // dst = src^T for one n x n row-major matrix.
 hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t s);
 

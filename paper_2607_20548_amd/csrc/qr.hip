@@ -1258,7 +1258,7 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
 
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
-                                hipStream_t st) {
+                                hipStream_t st, hipEvent_t q_free) {
   QrCtx x;
   x.L = qr_layout(batch, n);
   if (ws_bytes < x.L.total) return hipErrorInvalidValue;
@@ -1333,6 +1333,7 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   }
 
   // Explicit Q (row-major), accumulated backwards from diag(d).
+  if (q_free) SOAP_TRY(hipStreamWaitEvent(s, q_free, 0));
   {
     const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
     hipLaunchKernelGGL(qr_init_q_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, Q, x.dsign,

@@ -58,6 +58,8 @@ enum Stage {
   ST_KL_PROJ_R,
   ST_KL_FACTOR_L,
   ST_KL_FACTOR_R,
+  ST_KL_LOWRANK_L,
+  ST_KL_LOWRANK_R,
   ST_COUNT
 };
 
@@ -66,7 +68,7 @@ const char *kStageNames[ST_COUNT] = {
     "power_R",          "qr_L",            "qr_R",          "rotate_in_QLt",
     "rotate_in_QR_adam", "rotate_out_QL",  "rotate_out_QRt_update", "kl_eig_L",
     "kl_eig_R",         "kl_proj_L",       "kl_proj_R",     "kl_factor_L",
-    "kl_factor_R"};
+    "kl_factor_R",      "kl_lowrank_L",    "kl_lowrank_R"};
 
 struct Pending {
   int stage;
@@ -163,7 +165,7 @@ hipError_t aux_stream(int which, hipStream_t *out) {
 // partial sums; the QR workspaces stay last (each QR uses up to the next
 // region, the R side up to the end).
 struct StepLayout {
-  size_t al, ar, tg, tm, nb, kz, laml, lamr, partl, partr, qrl, qrr, total;
+  size_t al, ar, tg, tm, nb, kz, kw, laml, lamr, partl, partr, qrl, qrr, total;
 };
 
 StepLayout step_layout(int64_t batch, int64_t m, int64_t n, bool kl) {
@@ -177,6 +179,7 @@ StepLayout step_layout(int64_t batch, int64_t m, int64_t n, bool kl) {
   L.nb = o; o = align256(o + f * batch * m * n);
   if (kl) {
     L.kz = o; o = align256(o + f * batch * m * n);
+    L.kw = o; o = align256(o + f * batch * m * n);
     L.laml = o; o = align256(o + f * batch * m);
     L.lamr = o; o = align256(o + f * batch * n);
     L.partl = o; o = align256(o + f * soap::diag_partial_floats(batch, m));
@@ -335,9 +338,155 @@ int check_hparams(float beta1, float beta2, float eps, float lr, float wd, int64
   return SOAP_OK;
 }
 
+// The front of a KL-SOAP step: the KL-Shampoo accumulation of both factors
+// and the transposed power products A_L^T = Q_L^T L_new, A_R^T = Q_R^T R_new
+// that the QRs consume, with the previous step's bases throughout.  The
+// product X = Q^T F_old of each side serves the eigenvalue estimates, and on
+// a side whose dimension d exceeds twice the other (e) it also gives the power
+// product without a second d^3 product, because the new term has rank e:
+//   A_R^T = bk X_R + cR W_R^T Z_L,   W_R = Y_L Q_R   (4 d^2 e flops, not 2 d^3)
+//   A_L^T = bk X_L + cL W_L Z_R^T,   W_L = Q_L^T Y_R
+// with Y_L = Q_L^T G, Z_L = diag(1/(lambda_L+eps)) Y_L, Y_R = G Q_R,
+// Z_R = Y_R diag(1/(lambda_R+eps)), cL = (1-bk)/n, cR = (1-bk)/m.
+// Streams: the R side on s, the L side on sl.  sl produces Y_L, Z_L (and
+// W_R) and records ev_a; s forms X_R, lambda_R, waits for ev_a, finishes
+// A_R^T and records ev_power; sl then waits for ev_power (R-side work first:
+// it is on the critical path), forms Y_R (recording ev_yr once the old Q_R is
+// read), Z_R, L_new and A_L^T.  On the R-trick side the update of R itself is
+// not needed before the QR and is left to the caller (*defer_r = true), who
+// runs it later on sl with the L side's Y_L, Z_L.
+struct KlStepBufs {
+  float *AL, *AR, *YL, *ZL, *YR, *ZR, *W, *lamL, *lamR, *partL, *partR;
+};
+
+hipError_t kl_front(int64_t batch, int64_t m, int64_t n, const float *G, float *L, float *R,
+                    const float *QL, const float *QR, float bk, float eps, const KlStepBufs &b,
+                    hipStream_t s, hipStream_t sl, hipEvent_t ev_a, hipEvent_t ev_power,
+                    hipEvent_t ev_yr, bool *defer_r, const char **where) {
+  const int64_t mn = m * n, mm = m * m, nn = n * n;
+  const double B = (double)batch, md = (double)m, nd = (double)n;
+  const bool trick_r = n > 2 * m, trick_l = m > 2 * n;
+  const float cL = (float)((1.0 - (double)bk) / nd), cR = (float)((1.0 - (double)bk) / md);
+  hipError_t e;
+  auto fail_at = [&](const char *w, hipError_t err) { *where = w; return err; };
+  {  // X_L = Q_L^T L, lambda_L = diag(X_L Q_L)
+    StageScope sc(ST_KL_EIG_L, B * 2.0 * md * md * md, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = m; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
+    d.C = b.AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("KL eigenvalues L", e);
+    if ((e = soap::launch_diag_of_product(b.AL, QL, batch, m, b.partL, b.lamL, sl)) != hipSuccess)
+      return fail_at("KL eigenvalues L", e);
+  }
+  {  // Y_L = Q_L^T G, Z_L = diag(1/(lambda_L+eps)) Y_L
+    StageScope sc(ST_KL_PROJ_L, B * 2.0 * md * md * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = G; d.ldb = n; d.sB = mn;
+    d.C = b.YL; d.ldc = n; d.sC = mn; d.batch = batch;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("KL projection L", e);
+    if ((e = soap::launch_kl_scale(b.YL, b.ZL, b.lamL, batch, m, n, 1, eps, sl)) != hipSuccess)
+      return fail_at("KL scaling L", e);
+  }
+  if (trick_r) {  // W_R = Y_L Q_R
+    StageScope sc(ST_KL_LOWRANK_R, B * 2.0 * md * nd * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 0; d.M = m; d.N = n; d.K = n;
+    d.A = b.YL; d.lda = n; d.sA = mn; d.B = QR; d.ldb = n; d.sB = nn;
+    d.C = b.W; d.ldc = n; d.sC = mn; d.batch = batch;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("KL low-rank R", e);
+  }
+  if ((e = hipEventRecord(ev_a, sl)) != hipSuccess) return fail_at("KL event", e);
+  {  // X_R = Q_R^T R, lambda_R = diag(X_R Q_R)
+    StageScope sc(ST_KL_EIG_R, B * 2.0 * nd * nd * nd, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = n;
+    d.A = QR; d.lda = n; d.sA = nn; d.B = R; d.ldb = n; d.sB = nn;
+    d.C = b.AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return fail_at("KL eigenvalues R", e);
+    if ((e = soap::launch_diag_of_product(b.AR, QR, batch, n, b.partR, b.lamR, s)) != hipSuccess)
+      return fail_at("KL eigenvalues R", e);
+  }
+  if ((e = hipStreamWaitEvent(s, ev_a, 0)) != hipSuccess) return fail_at("KL event", e);
+  if (trick_r) {  // A_R^T = bk X_R + cR W_R^T Z_L
+    StageScope sc(ST_KL_LOWRANK_R, B * 2.0 * nd * nd * md, s);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
+    d.A = b.W; d.lda = n; d.sA = mn; d.B = b.ZL; d.ldb = n; d.sB = mn;
+    d.C = b.AR; d.ldc = n; d.sC = nn; d.alpha = cR; d.beta = bk; d.batch = batch;
+    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return fail_at("KL low-rank R", e);
+  } else {
+    {  // R <- bk R + cR Y_L^T Z_L
+      StageScope sc(ST_KL_FACTOR_R, B * nd * (nd + 1) * md, s);
+      soap::GemmDesc d;
+      d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
+      d.A = b.YL; d.lda = n; d.sA = mn; d.B = b.ZL; d.ldb = n; d.sB = mn;
+      d.C = R; d.ldc = n; d.sC = nn; d.alpha = cR; d.beta = bk; d.batch = batch;
+      if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return fail_at("KL factor R", e);
+    }
+    {  // A_R^T = Q_R^T R
+      StageScope sc(ST_POWER_R, B * 2.0 * nd * nd * nd, s);
+      soap::GemmDesc d;
+      d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = n;
+      d.A = QR; d.lda = n; d.sA = nn; d.B = R; d.ldb = n; d.sB = nn;
+      d.C = b.AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
+      if ((e = soap::launch_gemm(d, s)) != hipSuccess) return fail_at("power R", e);
+    }
+  }
+  if ((e = hipEventRecord(ev_power, s)) != hipSuccess) return fail_at("KL event", e);
+  if ((e = hipStreamWaitEvent(sl, ev_power, 0)) != hipSuccess) return fail_at("KL event", e);
+  {  // Y_R = G Q_R, Z_R = Y_R diag(1/(lambda_R+eps))
+    StageScope sc(ST_KL_PROJ_R, B * 2.0 * md * nd * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 0; d.M = m; d.N = n; d.K = n;
+    d.A = G; d.lda = n; d.sA = mn; d.B = QR; d.ldb = n; d.sB = nn;
+    d.C = b.YR; d.ldc = n; d.sC = mn; d.batch = batch; d.max_wg = kSideWorkgroups;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("KL projection R", e);
+    if ((e = hipEventRecord(ev_yr, sl)) != hipSuccess) return fail_at("KL event", e);
+    if ((e = soap::launch_kl_scale(b.YR, b.ZR, b.lamR, batch, m, n, 0, eps, sl)) != hipSuccess)
+      return fail_at("KL scaling R", e);
+  }
+  if (trick_l) {  // W_L = Q_L^T Y_R
+    StageScope sc(ST_KL_LOWRANK_L, B * 2.0 * md * md * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = b.YR; d.ldb = n; d.sB = mn;
+    d.C = b.W; d.ldc = n; d.sC = mn; d.batch = batch; d.max_wg = kSideWorkgroups;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("KL low-rank L", e);
+  }
+  {  // L <- bk L + cL Y_R Z_R^T
+    StageScope sc(ST_KL_FACTOR_L, B * md * (md + 1) * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
+    d.A = b.YR; d.lda = n; d.sA = mn; d.B = b.ZR; d.ldb = n; d.sB = mn;
+    d.C = L; d.ldc = m; d.sC = mm; d.alpha = cL; d.beta = bk; d.batch = batch;
+    d.max_wg = kSideWorkgroups;
+    if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return fail_at("KL factor L", e);
+  }
+  if (trick_l) {  // A_L^T = bk X_L + cL W_L Z_R^T
+    StageScope sc(ST_KL_LOWRANK_L, B * 2.0 * md * md * nd, sl);
+    soap::GemmDesc d;
+    d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
+    d.A = b.W; d.lda = n; d.sA = mn; d.B = b.ZR; d.ldb = n; d.sB = mn;
+    d.C = b.AL; d.ldc = m; d.sC = mm; d.alpha = cL; d.beta = bk; d.batch = batch;
+    d.max_wg = kSideWorkgroups;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("KL low-rank L", e);
+  } else {  // A_L^T = Q_L^T L
+    StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = m; d.K = m;
+    d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
+    d.C = b.AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1; d.max_wg = kSideWorkgroups;
+    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("power L", e);
+  }
+  *defer_r = trick_r;
+  return hipSuccess;
+}
+
 // Owns the events of one step; destroys whichever were created.
 struct StepEvents {
-  static constexpr int kCount = 6;
+  static constexpr int kCount = 5;
   hipEvent_t ev[kCount] = {};
   hipError_t create() {
     for (hipEvent_t &e : ev) {
@@ -415,62 +564,76 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   StepEvents evs;
   if ((e = evs.create()) != hipSuccess) return hip_fail(e, "event");
   hipEvent_t ev_fork = evs.ev[0], ev_join = evs.ev[1], ev_power = evs.ev[2];
-  hipEvent_t ev_lamr = evs.ev[3], ev_zl = evs.ev[4], ev_yr = evs.ev[5];
+  hipEvent_t ev_a = evs.ev[3], ev_yr = evs.ev[4];
   if ((e = hipEventRecord(ev_fork, s)) != hipSuccess) return hip_fail(e, "fork record");
   if ((e = hipStreamWaitEvent(sl, ev_fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
+  bool defer_r = false;
   if (kl) {
-    // KL-Shampoo accumulation; its buffers are dead before the stages that
-    // reuse them (A_L, A_R: the power products; T_G, T_M: written on the L
-    // stream after the join with the R-side power product; N: after the join).
-    const KlBufs kb{AL, AR, TG, TM, NN, reinterpret_cast<float *>(w + lay.kz),
-                    reinterpret_cast<float *>(w + lay.laml), reinterpret_cast<float *>(w + lay.lamr),
-                    reinterpret_cast<float *>(w + lay.partl), reinterpret_cast<float *>(w + lay.partr)};
+    // KL-Shampoo accumulation and power products.  Buffer reuse: Y_L, Z_L in
+    // T_G, T_M (rewritten on the L stream by the rotation, after their last
+    // reads), Y_R in N (written after the join).
+    const KlStepBufs kb{AL, AR, TG, TM, NN,
+                        reinterpret_cast<float *>(w + lay.kz), reinterpret_cast<float *>(w + lay.kw),
+                        reinterpret_cast<float *>(w + lay.laml), reinterpret_cast<float *>(w + lay.lamr),
+                        reinterpret_cast<float *>(w + lay.partl), reinterpret_cast<float *>(w + lay.partr)};
     const char *where = "";
-    if ((e = kl_accumulate(batch, m, n, grad, L, R, QL, QR, beta_kron, eps, kb, s, sl, ev_lamr,
-                           ev_zl, ev_yr, &where)) != hipSuccess)
+    if ((e = kl_front(batch, m, n, grad, L, R, QL, QR, beta_kron, eps, kb, s, sl, ev_a,
+                      ev_power, ev_yr, &defer_r, &where)) != hipSuccess)
       return hip_fail(e, where);
-  } else {  // L <- b2 L + (1-b2) G G^T
-    StageScope sc(ST_FACTOR_L, B * md * (md + 1) * nd, sl);
-    soap::GemmDesc d;
-    d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
-    d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
-    d.C = L; d.ldc = m; d.sC = mm; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
-    if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "factor EMA L");
+  } else {
+    {  // L <- b2 L + (1-b2) G G^T
+      StageScope sc(ST_FACTOR_L, B * md * (md + 1) * nd, sl);
+      soap::GemmDesc d;
+      d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
+      d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
+      d.C = L; d.ldc = m; d.sC = mm; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
+      if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "factor EMA L");
+    }
+    // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L
+    // since L is symmetric (both triangles are stored).
+    {  // A_L^T = Q_L^T L
+      StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, sl);
+      soap::GemmDesc d;
+      d.trans_a = 1; d.trans_b = 0;
+      d.M = m; d.N = m; d.K = m; d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
+      d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
+      if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "power L");
+    }
+    {  // R <- b2 R + (1-b2) G^T G
+      StageScope sc(ST_FACTOR_R, B * nd * (nd + 1) * md, s);
+      soap::GemmDesc d;
+      d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
+      d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
+      d.C = R; d.ldc = n; d.sC = nn; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
+      if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return hip_fail(e, "factor EMA R");
+    }
+    {  // A_R^T = Q_R^T R
+      StageScope sc(ST_POWER_R, B * 2.0 * nd * nd * nd, s);
+      soap::GemmDesc d;
+      d.trans_a = 1; d.trans_b = 0;
+      d.M = n; d.N = n; d.K = n; d.A = QR; d.lda = n; d.sA = nn; d.B = R; d.ldb = n; d.sB = nn;
+      d.C = AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
+      if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power R");
+    }
+    // The L-side QR starts once the R-side power product is done: its
+    // resident block kernels need free compute units, which that long
+    // product holds.
+    if ((e = hipEventRecord(ev_power, s)) != hipSuccess) return hip_fail(e, "power record");
+    if ((e = hipStreamWaitEvent(sl, ev_power, 0)) != hipSuccess) return hip_fail(e, "power wait");
   }
-  // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L since
-  // L is symmetric (both triangles are stored).
-  {  // A_L^T = Q_L^T L
-    StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, sl);
-    soap::GemmDesc d;
-    d.trans_a = 1; d.trans_b = 0;
-    d.M = m; d.N = m; d.K = m; d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
-    d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
-    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "power L");
-  }
-  if (!kl) {  // R <- b2 R + (1-b2) G^T G
-    StageScope sc(ST_FACTOR_R, B * nd * (nd + 1) * md, s);
-    soap::GemmDesc d;
-    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
-    d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
-    d.C = R; d.ldc = n; d.sC = nn; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
-    if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return hip_fail(e, "factor EMA R");
-  }
-  {  // A_R^T = Q_R^T R
-    StageScope sc(ST_POWER_R, B * 2.0 * nd * nd * nd, s);
-    soap::GemmDesc d;
-    d.trans_a = 1; d.trans_b = 0;
-    d.M = n; d.N = n; d.K = n; d.A = QR; d.lda = n; d.sA = nn; d.B = R; d.ldb = n; d.sB = nn;
-    d.C = AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
-    if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power R");
-  }
-  // The L-side QR starts once the R-side power product is done: its resident
-  // block kernels need free compute units, which that long product holds.
-  if ((e = hipEventRecord(ev_power, s)) != hipSuccess) return hip_fail(e, "power record");
-  if ((e = hipStreamWaitEvent(sl, ev_power, 0)) != hipSuccess) return hip_fail(e, "power wait");
   {  // Q_L = QR(A_L).Q
     StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
     if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl, spl)) != hipSuccess)
       return hip_fail(e, "QR L");
+  }
+  if (defer_r) {  // R <- bk R + (1-bk)/m Y_L^T Z_L, beside the R-side QR
+    StageScope sc(ST_KL_FACTOR_R, B * nd * (nd + 1) * md, sl);
+    soap::GemmDesc d;
+    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
+    d.A = TG; d.lda = n; d.sA = mn; d.B = TM; d.ldb = n; d.sB = mn;
+    d.C = R; d.ldc = n; d.sC = nn; d.alpha = (float)((1.0 - (double)beta_kron) / md);
+    d.beta = beta_kron; d.batch = batch; d.max_wg = kSideWorkgroups;
+    if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "KL factor R");
   }
   {  // T_G = Q_L^T G,  T_M = Q_L^T M on the L-side stream, capped to part of the
      // GPU: it overlaps the R-side QR, whose resident block kernels need whole
@@ -485,11 +648,10 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
   }
   if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
-  // The KL projection G Q_R on the L stream reads the old Q_R.
-  if (kl && (e = hipStreamWaitEvent(s, ev_yr, 0)) != hipSuccess) return hip_fail(e, "KL wait");
-  {  // Q_R = QR(A_R).Q
+  {  // Q_R = QR(A_R).Q; under KL, Q_R is written only after G Q_R has read it
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
-    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl)) != hipSuccess)
+    if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl,
+                                        kl ? ev_yr : nullptr)) != hipSuccess)
       return hip_fail(e, "QR R");
   }
   if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");

@@ -88,6 +88,26 @@ def test_kl_ragged_shapes(m, n):
                   beta_kron=BK)
 
 
+@pytest.mark.parametrize("m,n", [(1, 3), (3, 1), (37, 80), (130, 300), (300, 130)])
+def test_kl_low_rank_power_update_shapes(m, n):
+    """Shapes where one side is more than twice the other: that side's power
+    product is formed from Q^T F_old plus the rank-(other side) update."""
+    rng = np.random.default_rng([m, n, 38])
+    grads = [rng.standard_normal((m, n)).astype(np.float32) for _ in range(3)]
+    run_open_loop(m, n, grads, (0.02 * rng.standard_normal((m, n))).astype(np.float32),
+                  beta_kron=BK)
+
+
+@pytest.mark.parametrize("m,n", [(2400, 100), (100, 2400)])
+def test_kl_capped_side_products(m, n):
+    """Large enough that the factor updates beside the other side's QR run as
+    capped (tile-looping) launches, with the low-rank power update."""
+    rng = np.random.default_rng([m, n, 39])
+    grads = [(1e-2 * rng.standard_normal((m, n))).astype(np.float32) for _ in range(2)]
+    run_open_loop(m, n, grads, (0.02 * rng.standard_normal((m, n))).astype(np.float32),
+                  beta_kron=BK)
+
+
 def test_kl_beta_kron_half_no_bias_correction():
     import paper_2607_20548_amd as soap
     rng = np.random.default_rng(34)
@@ -111,11 +131,12 @@ def test_kl_identity_eigenbasis_is_adamw():
         assert np.array_equal(np.diag(np.diag(Lh)), Lh) and np.array_equal(np.diag(np.diag(Rh)), Rh)
 
 
-def test_kl_batched_matches_single_and_oracle():
+@pytest.mark.parametrize("m,n", [(37, 70), (37, 80), (90, 40)])
+def test_kl_batched_matches_single_and_oracle(m, n):
     import paper_2607_20548_amd as soap
     import oracle
-    B, m, n = 4, 37, 70
-    rng = np.random.default_rng(35)
+    B = 4
+    rng = np.random.default_rng([m, n, 35])
     W0 = (0.02 * rng.standard_normal((B, m, n))).astype(np.float32)
     grads = [rng.standard_normal((B, m, n)).astype(np.float32) for _ in range(3)]
     gb = soap.SoapState(m, n, batch=B, kl=True)
