@@ -16,5 +16,5 @@ from .soap_oracle import (  # noqa: F401
     OracleState, init_state, factor_ema, householder_qr, momentum_ema, rotate_in,
     adam_eigenbasis, rotate_out, weight_update, bias_corrections, soap_step,
     soap_step_batched, eigenvalue_estimates, kl_factor_update, kl_factors, kl_soap_step,
-    kl_soap_step_batched,
+    kl_soap_step_batched, refresh_due,
 )

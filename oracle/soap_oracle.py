@@ -184,16 +184,29 @@ def kl_factor_update(F: np.ndarray, X: np.ndarray, Q_other: np.ndarray, lam_othe
     return low + np.tril(low, -1).T
 
 
+def refresh_due(t: int, refresh_every: int) -> bool:
+    """Algorithm 2 recomputes the eigenbasis when t mod F = 0 (t is 1-based,
+    so F = 1 refreshes every step)."""
+    if refresh_every < 1:
+        raise ValueError("the refresh period F must be >= 1")
+    return t % refresh_every == 0
+
+
 def _refresh_and_update(s: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
                         eps: float, lr: float, weight_decay: float, bias_correction: bool,
-                        diagnostics: bool):
-    """The part of the step after the factors hold the current gradient:
-    power product and QR refresh, first-moment EMA, rotation in, Adam, rotation
-    out, weight update (Algorithm 2 with F = 1)."""
-    AL = s.L @ s.QL
-    AR = s.R @ s.QR
-    s.QL = householder_qr(AL)
-    s.QR = householder_qr(AR)
+                        diagnostics: bool, FL: Optional[np.ndarray], FR: Optional[np.ndarray]):
+    """The part of the step after the factor update: power product and QR
+    refresh from the factors FL, FR (skipped when they are None: the bases are
+    kept), first-moment EMA, rotation in, Adam, rotation out, weight update
+    (Algorithm 2).  The first moment lives in weight space, so a refresh needs
+    no re-rotation of it: rotating it in with whichever bases are current is
+    Algorithm 2's rotate-back / rotate-in of an eigenbasis-resident m."""
+    AL = AR = None
+    if FL is not None:
+        AL = FL @ s.QL
+        AR = FR @ s.QR
+        s.QL = householder_qr(AL)
+        s.QR = householder_qr(AR)
     s.M = momentum_ema(s.M, G, beta1)
     Gp = rotate_in(s.QL, G, s.QR)
     Mp = rotate_in(s.QL, s.M, s.QR)
@@ -208,20 +221,28 @@ def _refresh_and_update(s: OracleState, G: np.ndarray, t: int, beta1: float, bet
 
 def soap_step(state: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
               eps: float, lr: float, weight_decay: float, bias_correction: bool = True,
-              diagnostics: bool = False):
-    """One SOAP step on one matrix (Algorithm 2 with F = 1, real-time refresh).
+              diagnostics: bool = False, refresh_every: int = 1, stale_refresh: bool = False):
+    """One SOAP step on one matrix (Algorithm 2).
 
     Order: factor EMA with the current G, power product and QR refresh, first
-    moment EMA, rotation in, Adam, rotation out, weight update.  Returns the new
-    state (and a dict of intermediates when ``diagnostics``)."""
+    moment EMA, rotation in, Adam, rotation out, weight update.  The refresh
+    runs when t mod refresh_every = 0 (Algorithm 2's F; F = 1 is the paper's
+    setting).  stale_refresh takes the power product from the factors as they
+    were before this step's gradient was added: the lagging preconditioner that
+    Section 5.4.1 shows unstable and Section 5.4.2 replaces (an ablation).
+    Returns the new state (and a dict of intermediates when ``diagnostics``)."""
     if t < 1:
         raise ValueError("step t is 1-based")
     G = np.asarray(G, dtype=np.float64)
     s = state.copy()
+    L_old, R_old = s.L, s.R
     s.L = factor_ema(s.L, G, beta2)
     s.R = factor_ema(s.R, G.T, beta2)
+    FL, FR = (L_old, R_old) if stale_refresh else (s.L, s.R)
+    if not refresh_due(t, refresh_every):
+        FL = FR = None
     return _refresh_and_update(s, G, t, beta1, beta2, eps, lr, weight_decay, bias_correction,
-                               diagnostics)
+                               diagnostics, FL, FR)
 
 
 def kl_factors(L: np.ndarray, R: np.ndarray, QL: np.ndarray, QR: np.ndarray, G: np.ndarray,
@@ -241,18 +262,24 @@ def kl_factors(L: np.ndarray, R: np.ndarray, QL: np.ndarray, QR: np.ndarray, G: 
 
 def kl_soap_step(state: OracleState, G: np.ndarray, t: int, beta1: float, beta2: float,
                  beta_kron: float, eps: float, lr: float, weight_decay: float,
-                 bias_correction: bool = True, diagnostics: bool = False):
-    """One KL-SOAP step (Algorithm 2 with F = 1, real-time refresh): the factor
-    EMA of soap_step is replaced by the KL-Shampoo accumulation (kl_factors);
-    the same eps serves the eigenvalue floor and Adam (hyperparameter table of
-    Section 5.4).  Everything after the accumulation is soap_step's."""
+                 bias_correction: bool = True, diagnostics: bool = False,
+                 refresh_every: int = 1, stale_refresh: bool = False):
+    """One KL-SOAP step (Algorithm 2): the factor EMA of soap_step is replaced
+    by the KL-Shampoo accumulation (kl_factors); the same eps serves the
+    eigenvalue floor and Adam (hyperparameter table of Section 5.4).
+    Everything after the accumulation, including refresh_every and
+    stale_refresh, is soap_step's."""
     if t < 1:
         raise ValueError("step t is 1-based")
     G = np.asarray(G, dtype=np.float64)
     s = state.copy()
+    L_old, R_old = s.L, s.R
     s.L, s.R, lam_L, lam_R = kl_factors(s.L, s.R, s.QL, s.QR, G, beta_kron, eps)
+    FL, FR = (L_old, R_old) if stale_refresh else (s.L, s.R)
+    if not refresh_due(t, refresh_every):
+        FL = FR = None
     out = _refresh_and_update(s, G, t, beta1, beta2, eps, lr, weight_decay, bias_correction,
-                              diagnostics)
+                              diagnostics, FL, FR)
     if diagnostics:
         out[1]["lam_L"], out[1]["lam_R"] = lam_L, lam_R
     return out

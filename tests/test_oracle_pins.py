@@ -317,3 +317,91 @@ def test_full_step_against_50_digit_brute_force():
     for got, want in [(new.L, Ld), (new.R, Rd), (new.QL, QLd), (new.QR, QRd), (new.M, Md),
                       (new.V, Vd), (new.W, Wd)]:
         assert rel(got, f(want)) <= 1e-13
+
+
+# ------------------------------------------- refresh period and stale refresh
+@pytest.mark.parametrize("F", [2, 3])
+def test_refresh_period_equals_algorithm2_literal(F):
+    """Algorithm 2 with t mod F gating: the eigenbasis-resident m is rotated
+    back and forward only at a refresh, V never.  The oracle's weight-space
+    momentum must give the same step for any F."""
+    rng = np.random.default_rng(40 + F)
+    m, n = 7, 11
+    b1, b2, eps, lr, wd = 0.9, 0.95, 1e-8, 1e-2, 0.1
+    W = rng.standard_normal((m, n))
+    st = oracle.init_state(W)
+    L, R, QL, QR = np.eye(m), np.eye(n), np.eye(m), np.eye(n)
+    me, v, Wl = np.zeros((m, n)), np.zeros((m, n)), W.copy()
+    for t in range(1, 9):
+        G = rng.standard_normal((m, n))
+        st = oracle.soap_step(st, G, t, beta1=b1, beta2=b2, eps=eps, lr=lr, weight_decay=wd,
+                              refresh_every=F)
+        L = b2 * L + (1 - b2) * G @ G.T
+        R = b2 * R + (1 - b2) * G.T @ G
+        if t % F == 0:
+            mhat = QL @ me @ QR.T
+            QL = _sign_fixed_lapack_q(L @ QL)
+            QR = _sign_fixed_lapack_q(R @ QR)
+            me = QL.T @ mhat @ QR
+        Gp = QL.T @ G @ QR
+        me = b1 * me + (1 - b1) * Gp
+        v = b2 * v + (1 - b2) * Gp * Gp
+        N = (me / (1 - b1 ** t)) / (np.sqrt(v / (1 - b2 ** t)) + eps)
+        Wl = (1 - lr * wd) * Wl - lr * QL @ N @ QR.T
+        assert rel(st.QL, QL) <= 1e-12 and rel(st.QR, QR) <= 1e-12
+        assert rel(st.V, v) <= 1e-11
+        assert rel(st.W, Wl) <= 1e-12
+        if t < F:
+            assert np.array_equal(st.QL, np.eye(m)) and np.array_equal(st.QR, np.eye(n))
+
+
+def test_stale_refresh_uses_the_previous_factors():
+    """Sections 5.4.1-5.4.2: the stale variant refreshes from the factors before
+    the current gradient enters them.  From the identity start its first
+    refresh is QR(I Q) = I exactly; afterwards each refresh equals the
+    sign-fixed LAPACK QR of L_{t-1} Q_{t-1}, R_{t-1} Q_{t-1}."""
+    rng = np.random.default_rng(44)
+    m, n = 6, 9
+    st = oracle.init_state(rng.standard_normal((m, n)))
+    for t in range(1, 6):
+        prev = st
+        st = oracle.soap_step(prev, rng.standard_normal((m, n)), t, stale_refresh=True, **HP)
+        if t == 1:
+            assert np.array_equal(st.QL, np.eye(m)) and np.array_equal(st.QR, np.eye(n))
+        assert rel(st.QL, _sign_fixed_lapack_q(prev.L @ prev.QL)) <= 1e-12
+        assert rel(st.QR, _sign_fixed_lapack_q(prev.R @ prev.QR)) <= 1e-12
+    # the KL variant refreshes from the same pre-gradient factors
+    st = oracle.init_state(rng.standard_normal((m, n)))
+    for t in range(1, 4):
+        prev = st
+        st = oracle.kl_soap_step(prev, rng.standard_normal((m, n)), t, beta_kron=0.95,
+                                 stale_refresh=True, **HP)
+        assert rel(st.QL, _sign_fixed_lapack_q(prev.L @ prev.QL)) <= 1e-12
+        assert rel(st.QR, _sign_fixed_lapack_q(prev.R @ prev.QR)) <= 1e-12
+
+
+def test_fresh_refresh_sees_the_new_gradient_first():
+    """The point of Section 5.4.2: after the gradient switches to a new
+    direction u2, the fresh refresh brings u2 into the leading two basis
+    vectors in the very next step; the stale one does so exactly one step
+    later (its refresh at step t is the fresh refresh of step t - 1)."""
+    m, n = 5, 8
+    rng = np.random.default_rng(45)
+    U, _ = np.linalg.qr(rng.standard_normal((m, m)))
+    u1, u2 = U[:, 0], U[:, 1]
+    v1 = rng.standard_normal(n)
+    v1 /= np.linalg.norm(v1)
+    hp = dict(HP, beta2=0.5)
+    fresh, stale = oracle.init_state(np.zeros((m, n))), oracle.init_state(np.zeros((m, n)))
+    for t in range(1, 6):
+        G = np.outer(u1, v1)
+        fresh = oracle.soap_step(fresh, G, t, **hp)
+        stale = oracle.soap_step(stale, G, t, stale_refresh=True, **hp)
+    reach = lambda Q: np.linalg.norm(Q[:, :2].T @ u2)
+    assert reach(fresh.QL) < 0.2 and reach(stale.QL) < 0.2
+    G = 10.0 * np.outer(u2, v1)
+    fresh = oracle.soap_step(fresh, G, 6, **hp)
+    stale = oracle.soap_step(stale, G, 6, stale_refresh=True, **hp)
+    assert reach(fresh.QL) > 0.9999 and reach(stale.QL) < 0.2
+    stale = oracle.soap_step(stale, G, 7, stale_refresh=True, **hp)
+    assert reach(stale.QL) > 0.9999
