@@ -64,7 +64,22 @@ typedef enum {
   SOAP_ERR_HIP = -7         /* a HIP runtime call failed                         */
 } soap_status;
 
-enum { SOAP_FLAG_NO_BIAS_CORRECTION = 1u << 0 };
+/* Step flags (bitwise or):
+ *  SOAP_FLAG_NO_BIAS_CORRECTION  c1 = c2 = 1 (Algorithm 2 as printed).
+ *  SOAP_FLAG_SKIP_REFRESH        keep Q_L, Q_R: no power product, no QR this
+ *                                step (Algorithm 2 refreshes when t mod F = 0;
+ *                                the caller sets this flag on the other steps).
+ *                                The factors and the Adam part are updated.
+ *  SOAP_FLAG_STALE_REFRESH       refresh from the factors as they were before
+ *                                this step's gradient was added: the lagging
+ *                                preconditioner of Section 5.4.1, which the
+ *                                real-time refresh of Section 5.4.2 replaces
+ *                                (an ablation; no effect with SKIP_REFRESH). */
+enum {
+  SOAP_FLAG_NO_BIAS_CORRECTION = 1u << 0,
+  SOAP_FLAG_SKIP_REFRESH = 1u << 1,
+  SOAP_FLAG_STALE_REFRESH = 1u << 2
+};
 
 #define SOAP_MAX_DIM 16384
 
@@ -86,7 +101,7 @@ int soap_init_state(int64_t batch, int64_t m, int64_t n, float *L, float *R, flo
  * Q_L, Q_R, M, V are updated in place; `grad` is read only.  L and R are read
  * from their lower triangle and written fully symmetric.  `step` is the
  * 1-based t of this update.  beta1, beta2 in [0,1); eps, lr, weight_decay
- * finite and >= 0; flags is 0 or SOAP_FLAG_NO_BIAS_CORRECTION. */
+ * finite and >= 0; flags is a combination of the SOAP_FLAG_* bits. */
 int soap_step(float *param, const float *grad, float *L, float *R, float *Q_L, float *Q_R,
               float *M, float *V, int64_t m, int64_t n, float beta1, float beta2, float eps,
               float lr, float weight_decay, int64_t step, uint32_t flags, void *workspace,

@@ -26,6 +26,8 @@ SOAP_ERR_ALIGN = -5
 SOAP_ERR_ALIAS = -6
 SOAP_ERR_HIP = -7
 SOAP_FLAG_NO_BIAS_CORRECTION = 1
+SOAP_FLAG_SKIP_REFRESH = 2
+SOAP_FLAG_STALE_REFRESH = 4
 SOAP_MAX_DIM = 16384
 
 EXPORTED = [
@@ -264,7 +266,17 @@ class SoapState:
         soap_init_state(batch, m, n, self.L, self.R, self.Q_L, self.Q_R, self.M, self.V)
 
     def step(self, param, grad, t: int, beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3,
-             weight_decay=0.1, flags=0, stream=None, beta_kron=None) -> None:
+             weight_decay=0.1, flags=0, stream=None, beta_kron=None, refresh_every=1,
+             stale_refresh=False) -> None:
+        """One step t (1-based).  refresh_every = F refreshes the eigenbases
+        when t mod F = 0 (SOAP_FLAG_SKIP_REFRESH on the other steps);
+        stale_refresh sets SOAP_FLAG_STALE_REFRESH."""
+        if refresh_every < 1:
+            raise ValueError("refresh_every must be >= 1")
+        if t % refresh_every != 0:
+            flags |= SOAP_FLAG_SKIP_REFRESH
+        if stale_refresh:
+            flags |= SOAP_FLAG_STALE_REFRESH
         if self.kl:
             if beta_kron is None:
                 raise ValueError("a KL-SOAP state needs beta_kron")

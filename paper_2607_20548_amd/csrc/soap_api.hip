@@ -333,7 +333,8 @@ int check_hparams(float beta1, float beta2, float eps, float lr, float wd, int64
   if (!std::isfinite(wd) || wd < 0.f)
     return fail(SOAP_ERR_HPARAM, "weight_decay = %g must be finite and >= 0", (double)wd);
   if (step < 1) return fail(SOAP_ERR_HPARAM, "step = %lld must be >= 1", (long long)step);
-  if (flags & ~uint32_t(SOAP_FLAG_NO_BIAS_CORRECTION))
+  if (flags & ~uint32_t(SOAP_FLAG_NO_BIAS_CORRECTION | SOAP_FLAG_SKIP_REFRESH |
+                        SOAP_FLAG_STALE_REFRESH))
     return fail(SOAP_ERR_HPARAM, "unknown flag bits 0x%x", flags);
   return SOAP_OK;
 }
@@ -354,7 +355,9 @@ int check_hparams(float beta1, float beta2, float eps, float lr, float wd, int64
 // it is on the critical path), forms Y_R (recording ev_yr once the old Q_R is
 // read), Z_R, L_new and A_L^T.  On the R-trick side the update of R itself is
 // not needed before the QR and is left to the caller (*defer_r = true), who
-// runs it later on sl with the L side's Y_L, Z_L.
+// runs it later on sl with the L side's Y_L, Z_L.  Without a refresh
+// (refresh = false) only the factors are updated; with a stale refresh the
+// power products are the products X = Q^T F_old of the estimates.
 struct KlStepBufs {
   float *AL, *AR, *YL, *ZL, *YR, *ZR, *W, *lamL, *lamR, *partL, *partR;
 };
@@ -362,10 +365,14 @@ struct KlStepBufs {
 hipError_t kl_front(int64_t batch, int64_t m, int64_t n, const float *G, float *L, float *R,
                     const float *QL, const float *QR, float bk, float eps, const KlStepBufs &b,
                     hipStream_t s, hipStream_t sl, hipEvent_t ev_a, hipEvent_t ev_power,
-                    hipEvent_t ev_yr, bool *defer_r, const char **where) {
+                    hipEvent_t ev_yr, bool refresh, bool stale, bool *defer_r,
+                    const char **where) {
   const int64_t mn = m * n, mm = m * m, nn = n * n;
   const double B = (double)batch, md = (double)m, nd = (double)n;
-  const bool trick_r = n > 2 * m, trick_l = m > 2 * n;
+  // Without a refresh no power product is formed; a stale refresh uses
+  // X = Q^T F_old itself, which the estimates leave in A_L, A_R.
+  const bool fresh = refresh && !stale;
+  const bool trick_r = fresh && n > 2 * m, trick_l = fresh && m > 2 * n;
   const float cL = (float)((1.0 - (double)bk) / nd), cR = (float)((1.0 - (double)bk) / md);
   hipError_t e;
   auto fail_at = [&](const char *w, hipError_t err) { *where = w; return err; };
@@ -425,7 +432,7 @@ hipError_t kl_front(int64_t batch, int64_t m, int64_t n, const float *G, float *
       d.C = R; d.ldc = n; d.sC = nn; d.alpha = cR; d.beta = bk; d.batch = batch;
       if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return fail_at("KL factor R", e);
     }
-    {  // A_R^T = Q_R^T R
+    if (fresh) {  // A_R^T = Q_R^T R
       StageScope sc(ST_POWER_R, B * 2.0 * nd * nd * nd, s);
       soap::GemmDesc d;
       d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = n;
@@ -472,7 +479,7 @@ hipError_t kl_front(int64_t batch, int64_t m, int64_t n, const float *G, float *
     d.C = b.AL; d.ldc = m; d.sC = mm; d.alpha = cL; d.beta = bk; d.batch = batch;
     d.max_wg = kSideWorkgroups;
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return fail_at("KL low-rank L", e);
-  } else {  // A_L^T = Q_L^T L
+  } else if (fresh) {  // A_L^T = Q_L^T L
     StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, sl);
     soap::GemmDesc d;
     d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = m; d.K = m;
@@ -534,6 +541,8 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
         return fail(SOAP_ERR_ALIAS, "%s overlaps %s", bufs[i].name, bufs[j].name);
 
   const bool bc = !(flags & SOAP_FLAG_NO_BIAS_CORRECTION);
+  const bool refresh = !(flags & SOAP_FLAG_SKIP_REFRESH);
+  const bool stale = (flags & SOAP_FLAG_STALE_REFRESH) != 0;
   const float c1 = bc ? (float)(1.0 - std::pow((double)beta1, (double)step)) : 1.f;
   const float c2 = bc ? (float)(1.0 - std::pow((double)beta2, (double)step)) : 1.f;
 
@@ -578,42 +587,55 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
                         reinterpret_cast<float *>(w + lay.partl), reinterpret_cast<float *>(w + lay.partr)};
     const char *where = "";
     if ((e = kl_front(batch, m, n, grad, L, R, QL, QR, beta_kron, eps, kb, s, sl, ev_a,
-                      ev_power, ev_yr, &defer_r, &where)) != hipSuccess)
+                      ev_power, ev_yr, refresh, stale, &defer_r, &where)) != hipSuccess)
       return hip_fail(e, where);
   } else {
-    {  // L <- b2 L + (1-b2) G G^T
+    auto factor_l = [&]() -> hipError_t {  // L <- b2 L + (1-b2) G G^T
       StageScope sc(ST_FACTOR_L, B * md * (md + 1) * nd, sl);
       soap::GemmDesc d;
       d.trans_a = 0; d.trans_b = 1; d.M = m; d.N = m; d.K = n;
       d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
       d.C = L; d.ldc = m; d.sC = mm; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
-      if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "factor EMA L");
-    }
+      return soap::launch_syrk_ema(d, sl);
+    };
     // Power products, produced transposed for the QR: (L Q_L)^T = Q_L^T L
     // since L is symmetric (both triangles are stored).
-    {  // A_L^T = Q_L^T L
+    auto power_l = [&]() -> hipError_t {  // A_L^T = Q_L^T L
       StageScope sc(ST_POWER_L, B * 2.0 * md * md * md, sl);
       soap::GemmDesc d;
       d.trans_a = 1; d.trans_b = 0;
       d.M = m; d.N = m; d.K = m; d.A = QL; d.lda = m; d.sA = mm; d.B = L; d.ldb = m; d.sB = mm;
       d.C = AL; d.ldc = m; d.sC = mm; d.batch = batch; d.tag = 1;
-      if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "power L");
-    }
-    {  // R <- b2 R + (1-b2) G^T G
+      return soap::launch_gemm(d, sl);
+    };
+    auto factor_r = [&]() -> hipError_t {  // R <- b2 R + (1-b2) G^T G
       StageScope sc(ST_FACTOR_R, B * nd * (nd + 1) * md, s);
       soap::GemmDesc d;
       d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
       d.A = grad; d.lda = n; d.sA = mn; d.B = grad; d.ldb = n; d.sB = mn;
       d.C = R; d.ldc = n; d.sC = nn; d.alpha = 1.f - beta2; d.beta = beta2; d.batch = batch;
-      if ((e = soap::launch_syrk_ema(d, s)) != hipSuccess) return hip_fail(e, "factor EMA R");
-    }
-    {  // A_R^T = Q_R^T R
+      return soap::launch_syrk_ema(d, s);
+    };
+    auto power_r = [&]() -> hipError_t {  // A_R^T = Q_R^T R
       StageScope sc(ST_POWER_R, B * 2.0 * nd * nd * nd, s);
       soap::GemmDesc d;
       d.trans_a = 1; d.trans_b = 0;
       d.M = n; d.N = n; d.K = n; d.A = QR; d.lda = n; d.sA = nn; d.B = R; d.ldb = n; d.sB = nn;
       d.C = AR; d.ldc = n; d.sC = nn; d.batch = batch; d.tag = 2;
-      if ((e = soap::launch_gemm(d, s)) != hipSuccess) return hip_fail(e, "power R");
+      return soap::launch_gemm(d, s);
+    };
+    // A stale refresh takes the power products before the gradient enters
+    // the factors; without a refresh there are none.
+    if (refresh && stale) {
+      if ((e = power_l()) != hipSuccess) return hip_fail(e, "power L");
+      if ((e = factor_l()) != hipSuccess) return hip_fail(e, "factor EMA L");
+      if ((e = power_r()) != hipSuccess) return hip_fail(e, "power R");
+      if ((e = factor_r()) != hipSuccess) return hip_fail(e, "factor EMA R");
+    } else {
+      if ((e = factor_l()) != hipSuccess) return hip_fail(e, "factor EMA L");
+      if (refresh && (e = power_l()) != hipSuccess) return hip_fail(e, "power L");
+      if ((e = factor_r()) != hipSuccess) return hip_fail(e, "factor EMA R");
+      if (refresh && (e = power_r()) != hipSuccess) return hip_fail(e, "power R");
     }
     // The L-side QR starts once the R-side power product is done: its
     // resident block kernels need free compute units, which that long
@@ -621,7 +643,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if ((e = hipEventRecord(ev_power, s)) != hipSuccess) return hip_fail(e, "power record");
     if ((e = hipStreamWaitEvent(sl, ev_power, 0)) != hipSuccess) return hip_fail(e, "power wait");
   }
-  {  // Q_L = QR(A_L).Q
+  if (refresh) {  // Q_L = QR(A_L).Q
     StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
     if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl, spl)) != hipSuccess)
       return hip_fail(e, "QR L");
@@ -648,7 +670,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
   }
   if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
-  {  // Q_R = QR(A_R).Q; under KL, Q_R is written only after G Q_R has read it
+  if (refresh) {  // Q_R = QR(A_R).Q; under KL, Q_R is written only after G Q_R has read it
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
     if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl,
                                         kl ? ev_yr : nullptr)) != hipSuccess)

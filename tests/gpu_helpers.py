@@ -75,7 +75,8 @@ def compare_state(st, gs, tag, tol=TOL):
     return errs
 
 
-def run_open_loop(m, n, grads, W0, hp=HP, flags=0, bias_correction=True, beta_kron=None):
+def run_open_loop(m, n, grads, W0, hp=HP, flags=0, bias_correction=True, beta_kron=None,
+                  refresh_every=1, stale_refresh=False):
     """Open loop over the given gradients (SOAP, or KL-SOAP when beta_kron is
     given).  Every step:
       * L, R, Q_L, Q_R, M, V: relative Frobenius error <= TOL;
@@ -97,10 +98,15 @@ def run_open_loop(m, n, grads, W0, hp=HP, flags=0, bias_correction=True, beta_kr
     extra = dict(beta_kron=beta_kron) if kl else {}
     for t, G in enumerate(grads, start=1):
         W_prev = host(W)
-        gs.step(W, dev(G), t, flags=flags, **extra, **hp)
+        Q_prev = (host(gs.Q_L), host(gs.Q_R))
+        gs.step(W, dev(G), t, flags=flags, refresh_every=refresh_every,
+                stale_refresh=stale_refresh, **extra, **hp)
         step_fn = oracle.kl_soap_step if kl else oracle.soap_step
         st, d = step_fn(st, G.astype(np.float64), t, bias_correction=bias_correction,
-                        diagnostics=True, **extra, **hp)
+                        diagnostics=True, refresh_every=refresh_every,
+                        stale_refresh=stale_refresh, **extra, **hp)
+        if t % refresh_every != 0:   # no refresh: the bases are kept bit for bit
+            assert np.array_equal(host(gs.Q_L), Q_prev[0]) and np.array_equal(host(gs.Q_R), Q_prev[1])
         errs = compare_state(st, gs, f"{m}x{n} t={t}")
         g_scale = max(g_scale, np.linalg.norm(G.astype(np.float64), 2))
         Wg = host(W)

@@ -64,7 +64,7 @@ def call_step(L, a):
     (dict(lr=float("inf")), soap.SOAP_ERR_HPARAM),
     (dict(weight_decay=-1.0), soap.SOAP_ERR_HPARAM),
     (dict(step=0), soap.SOAP_ERR_HPARAM),
-    (dict(flags=2), soap.SOAP_ERR_HPARAM),
+    (dict(flags=8), soap.SOAP_ERR_HPARAM),
     (dict(grad=BASE + 1 * MB + 4), soap.SOAP_ERR_ALIGN),
     (dict(grad=BASE), soap.SOAP_ERR_ALIAS),                 # grad == param
     (dict(R=BASE + 2 * MB + 64), soap.SOAP_ERR_ALIAS),      # R inside L

@@ -219,3 +219,12 @@ def test_kl_bench_shape_sampled_closed_loop():
     _check_kl_factors_sampled(pre, post, G, rng)
     info = check_refresh_adam_sampled(pre, post, G, 3, rng)
     log(f"  ok {info}")
+
+
+@pytest.mark.parametrize("m,n,F,stale", [(64, 96, 2, False), (37, 80, 3, False), (37, 80, 1, True),
+                                         (90, 40, 2, True)])
+def test_kl_refresh_period_and_stale_refresh(m, n, F, stale):
+    rng = np.random.default_rng([m, n, F, int(stale), 40])
+    grads = [rng.standard_normal((m, n)).astype(np.float32) for _ in range(5)]
+    run_open_loop(m, n, grads, (0.02 * rng.standard_normal((m, n))).astype(np.float32),
+                  beta_kron=BK, refresh_every=F, stale_refresh=stale)

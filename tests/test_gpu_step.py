@@ -131,3 +131,14 @@ def test_two_runs_are_bitwise_identical():
         outs.append([host(x) for x in (W, gs.L, gs.R, gs.Q_L, gs.Q_R, gs.M, gs.V)])
     for a, b in zip(*outs):
         assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("F,stale", [(3, False), (1, True), (2, True)])
+def test_refresh_period_and_stale_refresh(F, stale):
+    """Algorithm 2's refresh every F steps (bases kept bit for bit in between)
+    and the stale-refresh ablation, against the oracle."""
+    rng = np.random.default_rng([F, int(stale), 26])
+    m, n = 96, 160
+    grads = [rng.standard_normal((m, n)).astype(np.float32) for _ in range(6)]
+    run_open_loop(m, n, grads, (0.02 * rng.standard_normal((m, n))).astype(np.float32),
+                  refresh_every=F, stale_refresh=stale)
