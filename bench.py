@@ -6,11 +6,13 @@ with per-step QR refresh of both eigenbases (R is 14336 x 14336).  Gradients
 are generated and copied to HBM before the timed region.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
-                    [--calibration-copy-mib N] [--kl]
+                    [--calibration-copy-mib N] [--kl] [--refresh-every F] [--stale]
 
 --kl times the KL-SOAP step instead (soap_kl_step, beta_kron 0.95): the
 factors are accumulated by the KL-Shampoo rule, the rest of the step is the
-same.
+same.  --refresh-every F refreshes the eigenbases only when t mod F = 0
+(Algorithm 2's F; the paper uses 1), --stale takes the refresh from the
+factors before the step's gradient (the ablation of Section 5.4.1).
 
 Prints ONE JSON line.  `value` is steps/s of the whole step; `roofline`
 describes the dominant kernel (timed with HIP events on the library's stream
@@ -110,6 +112,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibration-copy-mib", type=int, default=0)
     ap.add_argument("--kl", action="store_true", help="time the KL-SOAP step")
+    ap.add_argument("--refresh-every", type=int, default=1)
+    ap.add_argument("--stale", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the SOAP step of a "
@@ -133,6 +137,7 @@ def main():
     state = soap.SoapState(m, n, kl=args.kl)
     stream = torch.cuda.current_stream()
     extra = dict(beta_kron=BETA_KRON) if args.kl else {}
+    extra.update(refresh_every=args.refresh_every, stale_refresh=args.stale)
 
     for t in range(1, args.warmup + 1):
         state.step(W, grads[t - 1], t, **extra, **HP)
@@ -174,6 +179,8 @@ def main():
     achieved = d_fl / (d_ms / d_n * 1e-3) / d_n / 1e12
 
     F = (kl_step_flops if args.kl else step_flops)(m, n)
+    if args.refresh_every > 1:   # the power products and QRs run on 1 step in F
+        F -= (1.0 - 1.0 / args.refresh_every) * (2.0 + 8.0 / 3.0) * (m ** 3 + n ** 3)
     value = args.steps / elapsed
     name = "KL-SOAP" if args.kl else "SOAP"
     out = {
@@ -191,7 +198,10 @@ def main():
         "data": "synthetic (seeded low-rank + noise gradients, rank 128, 10% noise)",
         "config": {"workload": f"{'soap_kl_step' if args.kl else 'soap_step'} on one {m}x{n} fp32 "
                                f"weight (MLP up-projection), QR refresh of both factors every step"
-                               + (f", KL-Shampoo factors (beta_kron {BETA_KRON})" if args.kl else ""),
+                               + (f", KL-Shampoo factors (beta_kron {BETA_KRON})" if args.kl else "")
+                               + (f", refresh every {args.refresh_every} steps"
+                                  if args.refresh_every > 1 else "")
+                               + (", stale refresh" if args.stale else ""),
                    "m": m, "n": n, "rank": spec.rank, "global_batch": 1, "seq_len": None,
                    "parallelism": "none (1 GPU)"},
         "step_tflops": F * value / 1e12,

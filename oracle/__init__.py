@@ -1,4 +1,4 @@
-"""fp64 CPU oracle for the SOAP optimizer step.
+"""fp64 CPU oracle for the SOAP optimizer step (and the Muon step).
 
 TEST INFRASTRUCTURE ONLY.  This package is the plain, slow reference that the
 HIP library is checked against.  Only ``tests/``, ``__graft_entry__.smoke()`` and
@@ -18,3 +18,4 @@ from .soap_oracle import (  # noqa: F401
     soap_step_batched, eigenvalue_estimates, kl_factor_update, kl_factors, kl_soap_step,
     kl_soap_step_batched, refresh_due,
 )
+from .muon_oracle import newton_schulz, muon_step  # noqa: F401
