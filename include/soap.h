@@ -146,6 +146,33 @@ int soap_kl_step_batched(int64_t batch, float *param, const float *grad, float *
                          float weight_decay, int64_t step, uint32_t flags, void *workspace,
                          size_t workspace_bytes, hipStream_t stream);
 
+/* ---- Muon (Algorithm 1, the paper's second optimizer) ----
+ * One Muon step on an m x n weight ("in" x "out"):
+ *
+ *   M <- beta1 M + (1 - beta1) G
+ *   X_0 = M / max(||M||_F, eps)
+ *   for i = 1..n_iters:  A = X X^T,  B = b_i A + c_i A^2,  X <- a_i X + B X
+ *   W <- (1 - lr wd) W - lr sqrt(max(m, n)) X_n
+ *
+ * The polynomial acts on singular values only, so the library forms the Gram
+ * matrix on the smaller side (X^T X and X <- a X + X B when m > n); the
+ * result is the same iterate.  coeffs is a HOST array of 3 n_iters floats
+ * (a_1, b_1, c_1, a_2, ...): the paper uses the PolarExpress schedule with
+ * n = 16 (hyperparameter table of Section 5.3) without printing it, so the
+ * caller supplies the schedule.  param, grad, M are device pointers in the
+ * layout of soap_step (grad read only, param and M updated); beta1 in [0, 1),
+ * lr and weight_decay finite and >= 0, eps finite and > 0, n_iters in
+ * [0, 1024], flags 0.  The products run in fp32 on the matrix cores.
+ * Ownership, streams and errors as for soap_step. */
+size_t soap_muon_workspace_bytes(int64_t batch, int64_t m, int64_t n);
+int soap_muon_step(float *param, const float *grad, float *M, int64_t m, int64_t n, float beta1,
+                   float lr, float weight_decay, float eps, const float *coeffs, int64_t n_iters,
+                   uint32_t flags, void *workspace, size_t workspace_bytes, hipStream_t stream);
+int soap_muon_step_batched(int64_t batch, float *param, const float *grad, float *M, int64_t m,
+                           int64_t n, float beta1, float lr, float weight_decay, float eps,
+                           const float *coeffs, int64_t n_iters, uint32_t flags, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
 /* Description of the last failure on the calling thread ("" after success).
  * Valid until the next call on the same thread. */
 const char *soap_last_error(void);

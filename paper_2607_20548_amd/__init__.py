@@ -36,7 +36,8 @@ EXPORTED = [
     "soap_factor_ema_f32", "soap_timing_enable", "soap_timing_num_stages",
     "soap_timing_stage_name", "soap_timing_collect", "soap_timing_reset", "soap_timing_get",
     "soap_kl_workspace_bytes", "soap_kl_step", "soap_kl_step_batched",
-    "soap_kl_factors_workspace_bytes", "soap_kl_factors_f32",
+    "soap_kl_factors_workspace_bytes", "soap_kl_factors_f32", "soap_muon_workspace_bytes",
+    "soap_muon_step", "soap_muon_step_batched",
 ]
 
 
@@ -79,6 +80,11 @@ def lib() -> ctypes.CDLL:
         "soap_kl_factors_workspace_bytes": (_SZ, [_I64, _I64]),
         "soap_kl_factors_f32": (_INT, [_I64, _I64, _P, _P, _P, _P, _P, _F, _F, _P, _P, _P, _SZ,
                                        _P]),
+        "soap_muon_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
+        "soap_muon_step": (_INT, [_P, _P, _P, _I64, _I64, _F, _F, _F, _F, _P, _I64, _U32, _P,
+                                  _SZ, _P]),
+        "soap_muon_step_batched": (_INT, [_I64, _P, _P, _P, _I64, _I64, _F, _F, _F, _F, _P, _I64,
+                                          _U32, _P, _SZ, _P]),
         "soap_last_error": (ctypes.c_char_p, []),
         "soap_qr_workspace_bytes": (_SZ, [_I64]),
         "soap_qr_f32": (_INT, [_I64, _P, _P, _P, _P, _SZ, _P]),
@@ -199,6 +205,38 @@ def soap_kl_factors_f32(m, n, G, L, R, Q_L, Q_R, beta_kron, eps, lam_L, lam_R, w
                                      workspace_bytes, _stream(stream)))
 
 
+def _host_floats(values):
+    """A host float array for a C `const float *` argument (kept alive by the caller)."""
+    import numpy as np
+    arr = np.ascontiguousarray(np.asarray(values, dtype=np.float32).ravel())
+    return arr, arr.ctypes.data_as(ctypes.c_void_p)
+
+
+def soap_muon_workspace_bytes(batch: int, m: int, n: int) -> int:
+    return lib().soap_muon_workspace_bytes(batch, m, n)
+
+
+def soap_muon_step(param, grad, M, m, n, beta1, lr, weight_decay, eps, coeffs, n_iters, flags,
+                   workspace, workspace_bytes, stream=None) -> None:
+    """coeffs: the 3 * n_iters Newton-Schulz coefficients (a_1, b_1, c_1, ...) on the host."""
+    arr, ptr = _host_floats(coeffs)
+    if arr.size < 3 * n_iters:
+        raise ValueError("coeffs needs 3 * n_iters values")
+    _check(lib().soap_muon_step(_ptr(param), _ptr(grad), _ptr(M), m, n, beta1, lr, weight_decay,
+                                eps, ptr, n_iters, flags, _ptr(workspace), workspace_bytes,
+                                _stream(stream)))
+
+
+def soap_muon_step_batched(batch, param, grad, M, m, n, beta1, lr, weight_decay, eps, coeffs,
+                           n_iters, flags, workspace, workspace_bytes, stream=None) -> None:
+    arr, ptr = _host_floats(coeffs)
+    if arr.size < 3 * n_iters:
+        raise ValueError("coeffs needs 3 * n_iters values")
+    _check(lib().soap_muon_step_batched(batch, _ptr(param), _ptr(grad), _ptr(M), m, n, beta1, lr,
+                                        weight_decay, eps, ptr, n_iters, flags, _ptr(workspace),
+                                        workspace_bytes, _stream(stream)))
+
+
 def soap_qr_f32(n, A, Q, Rf, workspace, workspace_bytes, stream=None) -> None:
     _check(lib().soap_qr_f32(n, _ptr(A), _ptr(Q), _ptr(Rf), _ptr(workspace), workspace_bytes,
                              _stream(stream)))
@@ -300,3 +338,29 @@ class SoapState:
             soap_step_batched(self.batch, param, grad, self.L, self.R, self.Q_L, self.Q_R, self.M,
                               self.V, self.m, self.n, beta1, beta2, eps, lr, weight_decay, t,
                               flags, self.workspace, self.ws_bytes, stream)
+
+
+class MuonState:
+    """Device-resident Muon state (the momentum buffer) for `batch` m x n
+    matrices, zero-initialised, with its workspace."""
+
+    def __init__(self, m: int, n: int, batch: int = 1, device: str = "cuda"):
+        import torch
+        self.m, self.n, self.batch = m, n, batch
+        shp = (batch, m, n) if batch > 1 else (m, n)
+        self.M = torch.zeros(shp, dtype=torch.float32, device=device)
+        self.ws_bytes = soap_muon_workspace_bytes(batch, m, n)
+        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+
+    def step(self, param, grad, coeffs, beta1=0.9, lr=1e-3, weight_decay=0.1, eps=1e-7,
+             stream=None) -> None:
+        """coeffs: a sequence of (a, b, c) Newton-Schulz triples, one per iteration."""
+        flat = [float(x) for abc in coeffs for x in abc]
+        n_iters = len(flat) // 3
+        if self.batch == 1:
+            soap_muon_step(param, grad, self.M, self.m, self.n, beta1, lr, weight_decay, eps, flat,
+                           n_iters, 0, self.workspace, self.ws_bytes, stream)
+        else:
+            soap_muon_step_batched(self.batch, param, grad, self.M, self.m, self.n, beta1, lr,
+                                   weight_decay, eps, flat, n_iters, 0, self.workspace,
+                                   self.ws_bytes, stream)

@@ -300,7 +300,7 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
             C[off] = v;
           } else if (MODE == MODE_SYRK) {
             if (row < col) continue;  // the mirror of (col,row) is written by its owner
-            const float v = p.beta * C[off] + p.alpha * acc[0][i][j][r];
+            const float v = (p.beta != 0.f ? p.beta * C[off] : 0.f) + p.alpha * acc[0][i][j][r];
             C[off] = v;
             if (row != col) C[(int64_t)col * p.ldc + row] = v;
           } else {

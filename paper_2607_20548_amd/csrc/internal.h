@@ -92,6 +92,17 @@ hipError_t launch_diag_of_product(const float *X, const float *Q, int64_t batch,
 hipError_t launch_kl_scale(const float *Y, float *Z, const float *lam, int64_t batch,
                            int64_t rows, int64_t cols, int by_row, float eps, hipStream_t s);
 
+// ----------------------------------------------------------------- Muon
+// X = M / max(||M||_F, eps) for `batch` contiguous matrices of `count` floats;
+// `part` holds muon_norm_partial_bytes(batch) bytes, inv receives the batch
+// factors 1 / max(||M||_F, eps).
+size_t muon_norm_partial_bytes(int64_t batch);
+hipError_t launch_muon_normalise(const float *M, float *X, int64_t batch, int64_t count,
+                                 float eps, double *part, float *inv, hipStream_t s);
+// W <- alpha W + beta X over `count` floats.
+hipError_t launch_axpby(float *W, const float *X, int64_t count, float alpha, float beta,
+                        hipStream_t s);
+
 // ----------------------------------------------------------------- QR
 // Blocked Householder QR of `batch` n x n matrices A, each given TRANSPOSED:
 // At = A^T row-major (element stride n*n between matrices).  At is overwritten

@@ -60,6 +60,9 @@ enum Stage {
   ST_KL_FACTOR_R,
   ST_KL_LOWRANK_L,
   ST_KL_LOWRANK_R,
+  ST_MUON_NORMALISE,
+  ST_MUON_NEWTON_SCHULZ,
+  ST_MUON_UPDATE,
   ST_COUNT
 };
 
@@ -68,7 +71,8 @@ const char *kStageNames[ST_COUNT] = {
     "power_R",          "qr_L",            "qr_R",          "rotate_in_QLt",
     "rotate_in_QR_adam", "rotate_out_QL",  "rotate_out_QRt_update", "kl_eig_L",
     "kl_eig_R",         "kl_proj_L",       "kl_proj_R",     "kl_factor_L",
-    "kl_factor_R",      "kl_lowrank_L",    "kl_lowrank_R"};
+    "kl_factor_R",      "kl_lowrank_L",    "kl_lowrank_R",  "muon_normalise",
+    "muon_newton_schulz", "muon_update"};
 
 struct Pending {
   int stage;
@@ -704,6 +708,140 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   return ok();
 }
 
+// ------------------------------------------------------------------ Muon
+struct MuonLayout {
+  size_t x, xn, a, bm, part, inv, total;
+};
+
+MuonLayout muon_layout(int64_t batch, int64_t m, int64_t n) {
+  MuonLayout L{};
+  const size_t f = sizeof(float);
+  const int64_t d = std::min(m, n);
+  size_t o = 0;
+  L.x = o; o = align256(o + f * batch * m * n);
+  L.xn = o; o = align256(o + f * batch * m * n);
+  L.a = o; o = align256(o + f * batch * d * d);
+  L.bm = o; o = align256(o + f * batch * d * d);
+  L.part = o; o = align256(o + soap::muon_norm_partial_bytes(batch));
+  L.inv = o; o = align256(o + f * batch);
+  L.total = o;
+  return L;
+}
+
+constexpr int64_t kMuonMaxIters = 1024;
+
+// One Muon step (Algorithm 1) on `batch` m x n matrices.  The Newton-Schulz
+// polynomial acts on singular values only, so its Gram matrix is formed on
+// the smaller side: A = X X^T (m x m) with X <- a X + B X when m <= n, and
+// A = X^T X (n x n) with X <- a X + X B otherwise; both are Algorithm 1's
+// iterate exactly (for the wide case the same steps applied to X^T).
+int muon_impl(int64_t batch, float *param, const float *grad, float *M, int64_t m, int64_t n,
+              float beta1, float lr, float wd, float eps, const float *coeffs, int64_t iters,
+              uint32_t flags, void *ws, size_t ws_bytes, hipStream_t s) {
+  if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n))
+    return fail(SOAP_ERR_SHAPE, "batch=%lld m=%lld n=%lld: each must be in [1, %d]",
+                (long long)batch, (long long)m, (long long)n, SOAP_MAX_DIM);
+  if (iters < 0 || iters > kMuonMaxIters)
+    return fail(SOAP_ERR_HPARAM, "n_iters = %lld is outside [0, %lld]", (long long)iters,
+                (long long)kMuonMaxIters);
+  const Range bufs[] = {{param, sizeof(float) * batch * m * n, "param"},
+                        {grad, sizeof(float) * batch * m * n, "grad"},
+                        {M, sizeof(float) * batch * m * n, "M"},
+                        {ws, ws_bytes, "workspace"}};
+  for (const Range &b : bufs)
+    if (!b.p) return fail(SOAP_ERR_NULL, "%s is NULL", b.name);
+  if (iters > 0 && !coeffs) return fail(SOAP_ERR_NULL, "coeffs is NULL");
+  if (!std::isfinite(beta1) || beta1 < 0.f || beta1 >= 1.f)
+    return fail(SOAP_ERR_HPARAM, "beta1 = %g is outside [0, 1)", (double)beta1);
+  if (!std::isfinite(lr) || lr < 0.f)
+    return fail(SOAP_ERR_HPARAM, "lr = %g must be finite and >= 0", (double)lr);
+  if (!std::isfinite(wd) || wd < 0.f)
+    return fail(SOAP_ERR_HPARAM, "weight_decay = %g must be finite and >= 0", (double)wd);
+  if (!std::isfinite(eps) || eps <= 0.f)
+    return fail(SOAP_ERR_HPARAM, "eps = %g must be finite and > 0", (double)eps);
+  for (int64_t i = 0; i < 3 * iters; ++i)
+    if (!std::isfinite(coeffs[i]))
+      return fail(SOAP_ERR_HPARAM, "coefficient %lld is not finite", (long long)i);
+  if (flags != 0) return fail(SOAP_ERR_HPARAM, "unknown flag bits 0x%x", flags);
+  const MuonLayout lay = muon_layout(batch, m, n);
+  if (ws_bytes < lay.total)
+    return fail(SOAP_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
+  for (const Range &b : bufs)
+    if (!aligned16(b.p)) return fail(SOAP_ERR_ALIGN, "%s is not 16-byte aligned", b.name);
+  for (int i = 0; i < 4; ++i)
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(bufs[i], bufs[j]))
+        return fail(SOAP_ERR_ALIAS, "%s overlaps %s", bufs[i].name, bufs[j].name);
+
+  char *w = static_cast<char *>(ws);
+  float *X = reinterpret_cast<float *>(w + lay.x);
+  float *Xn = reinterpret_cast<float *>(w + lay.xn);
+  float *A = reinterpret_cast<float *>(w + lay.a);
+  float *Bm = reinterpret_cast<float *>(w + lay.bm);
+  const bool tall = m > n;
+  const int64_t d = tall ? n : m, e2 = tall ? m : n;
+  const int64_t mn = m * n, dd = d * d;
+  const double Bt = (double)batch, dd_ = (double)d, ee = (double)e2;
+  hipError_t e;
+  {  // M <- b1 M + (1-b1) G
+    StageScope sc(ST_MOMENTUM, 0.0, s);
+    if ((e = soap::launch_momentum(M, grad, batch * mn, beta1, s)) != hipSuccess)
+      return hip_fail(e, "momentum");
+  }
+  {  // X_0 = M / max(||M||_F, eps)
+    StageScope sc(ST_MUON_NORMALISE, 0.0, s);
+    if ((e = soap::launch_muon_normalise(M, X, batch, mn, eps,
+                                         reinterpret_cast<double *>(w + lay.part),
+                                         reinterpret_cast<float *>(w + lay.inv), s)) != hipSuccess)
+      return hip_fail(e, "normalise");
+  }
+  for (int64_t it = 0; it < iters; ++it) {
+    const float a = coeffs[3 * it], b = coeffs[3 * it + 1], c = coeffs[3 * it + 2];
+    StageScope sc(ST_MUON_NEWTON_SCHULZ,
+                  Bt * (dd_ * (dd_ + 1) * ee + (c != 0.f ? 2.0 * dd_ * dd_ * dd_ : 0.0) +
+                        2.0 * dd_ * dd_ * ee), s);
+    {  // A = X X^T (wide) or X^T X (tall), one triangle mirrored
+      soap::GemmDesc g;
+      g.trans_a = tall ? 1 : 0; g.trans_b = tall ? 0 : 1;
+      g.M = d; g.N = d; g.K = e2;
+      g.A = X; g.lda = n; g.sA = mn; g.B = X; g.ldb = n; g.sB = mn;
+      g.C = A; g.ldc = d; g.sC = dd; g.alpha = 1.f; g.beta = 0.f; g.batch = batch;
+      if ((e = soap::launch_syrk_ema(g, s)) != hipSuccess) return hip_fail(e, "Newton-Schulz A");
+    }
+    const float *Bop = A;
+    float alpha_b = b;
+    if (c != 0.f) {  // B = b A + c A^2
+      if ((e = soap::launch_copy(Bm, A, batch * dd, s)) != hipSuccess) return hip_fail(e, "copy");
+      soap::GemmDesc g;
+      g.M = d; g.N = d; g.K = d;
+      g.A = A; g.lda = d; g.sA = dd; g.B = A; g.ldb = d; g.sB = dd;
+      g.C = Bm; g.ldc = d; g.sC = dd; g.alpha = c; g.beta = b; g.batch = batch;
+      if ((e = soap::launch_gemm(g, s)) != hipSuccess) return hip_fail(e, "Newton-Schulz B");
+      Bop = Bm;
+      alpha_b = 1.f;
+    }
+    // X <- a X + B X (wide) or a X + X B (tall)
+    if ((e = soap::launch_copy(Xn, X, batch * mn, s)) != hipSuccess) return hip_fail(e, "copy");
+    soap::GemmDesc g;
+    g.M = m; g.N = n; g.K = d;
+    if (tall) {
+      g.A = X; g.lda = n; g.sA = mn; g.B = Bop; g.ldb = d; g.sB = dd;
+    } else {
+      g.A = Bop; g.lda = d; g.sA = dd; g.B = X; g.ldb = n; g.sB = mn;
+    }
+    g.C = Xn; g.ldc = n; g.sC = mn; g.alpha = alpha_b; g.beta = a; g.batch = batch;
+    if ((e = soap::launch_gemm(g, s)) != hipSuccess) return hip_fail(e, "Newton-Schulz X");
+    std::swap(X, Xn);
+  }
+  {  // W <- (1 - lr wd) W - lr sqrt(max(m, n)) X_n
+    StageScope sc(ST_MUON_UPDATE, 0.0, s);
+    const float scale = (float)std::sqrt((double)std::max(m, n));
+    if ((e = soap::launch_axpby(param, X, batch * mn, 1.f - lr * wd, -lr * scale, s)) != hipSuccess)
+      return hip_fail(e, "update");
+  }
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -897,6 +1035,26 @@ int soap_factor_ema_f32(int trans, int64_t m, int64_t n, const float *G, float *
   hipError_t e = soap::launch_syrk_ema(g, stream);
   if (e != hipSuccess) return hip_fail(e, "factor EMA");
   return ok();
+}
+
+size_t soap_muon_workspace_bytes(int64_t batch, int64_t m, int64_t n) {
+  if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n)) return 0;
+  return muon_layout(batch, m, n).total;
+}
+
+int soap_muon_step(float *param, const float *grad, float *M, int64_t m, int64_t n, float beta1,
+                   float lr, float weight_decay, float eps, const float *coeffs, int64_t n_iters,
+                   uint32_t flags, void *workspace, size_t workspace_bytes, hipStream_t stream) {
+  return muon_impl(1, param, grad, M, m, n, beta1, lr, weight_decay, eps, coeffs, n_iters, flags,
+                   workspace, workspace_bytes, stream);
+}
+
+int soap_muon_step_batched(int64_t batch, float *param, const float *grad, float *M, int64_t m,
+                           int64_t n, float beta1, float lr, float weight_decay, float eps,
+                           const float *coeffs, int64_t n_iters, uint32_t flags, void *workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  return muon_impl(batch, param, grad, M, m, n, beta1, lr, weight_decay, eps, coeffs, n_iters,
+                   flags, workspace, workspace_bytes, stream);
 }
 
 int soap_timing_enable(int enable) {

@@ -172,3 +172,36 @@ def test_kl_factors_validation(L):
                                  None, p[7], ws, None) == soap.SOAP_ERR_ALIAS
     assert L.soap_kl_factors_f32(8, 12, p[0], p[1] + 4, p[2], p[3], p[4], 0.9, 1e-8, None, None,
                                  p[7], ws, None) == soap.SOAP_ERR_ALIGN
+
+
+def test_muon_validation(L):
+    import numpy as np
+    m, n = 8, 12
+    ws = soap.soap_muon_workspace_bytes(1, m, n)
+    assert ws > 0 and soap.soap_muon_workspace_bytes(1, 0, n) == 0
+    co = np.array([1.5, -0.5, 0.0] * 2, dtype=np.float32)
+    cp = co.ctypes.data
+    P, G, M, W = BASE, BASE + MB, BASE + 2 * MB, BASE + 3 * MB
+
+    def call(**o):
+        a = dict(param=P, grad=G, M=M, m=m, n=n, beta1=0.9, lr=1e-3, wd=0.1, eps=1e-7, co=cp,
+                 it=2, flags=0, ws=W, wsb=ws)
+        a.update(o)
+        return L.soap_muon_step(a["param"], a["grad"], a["M"], a["m"], a["n"], a["beta1"],
+                                a["lr"], a["wd"], a["eps"], a["co"], a["it"], a["flags"],
+                                a["ws"], a["wsb"], None)
+    assert call(m=0) == soap.SOAP_ERR_SHAPE
+    assert call(M=None) == soap.SOAP_ERR_NULL
+    assert call(co=None) == soap.SOAP_ERR_NULL
+    assert call(beta1=1.0) == soap.SOAP_ERR_HPARAM
+    assert call(eps=0.0) == soap.SOAP_ERR_HPARAM
+    assert call(it=-1) == soap.SOAP_ERR_HPARAM
+    assert call(it=2000) == soap.SOAP_ERR_HPARAM
+    assert call(flags=1) == soap.SOAP_ERR_HPARAM
+    assert call(wsb=ws - 1) == soap.SOAP_ERR_WORKSPACE
+    assert call(grad=P + 16) == soap.SOAP_ERR_ALIAS
+    assert call(M=M + 4) == soap.SOAP_ERR_ALIGN
+    bad = np.array([1.5, float("nan"), 0.0], dtype=np.float32)
+    assert call(co=bad.ctypes.data, it=1) == soap.SOAP_ERR_HPARAM
+    assert L.soap_muon_step_batched(0, P, G, M, m, n, 0.9, 1e-3, 0.1, 1e-7, cp, 2, 0, W, ws,
+                                    None) == soap.SOAP_ERR_SHAPE
