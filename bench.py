@@ -7,12 +7,17 @@ are generated and copied to HBM before the timed region.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
                     [--calibration-copy-mib N] [--kl] [--refresh-every F] [--stale]
+                    [--muon]
 
 --kl times the KL-SOAP step instead (soap_kl_step, beta_kron 0.95): the
 factors are accumulated by the KL-Shampoo rule, the rest of the step is the
 same.  --refresh-every F refreshes the eigenbases only when t mod F = 0
 (Algorithm 2's F; the paper uses 1), --stale takes the refresh from the
-factors before the step's gradient (the ablation of Section 5.4.1).
+factors before the step's gradient (the ablation of Section 5.4.1).  --muon
+times the Muon step of Algorithm 1 on the same weight instead (16
+Newton-Schulz iterations; the paper's PolarExpress coefficients are not
+printed, so the Taylor quintic (15/8, -5/4, 3/8) stands in: the cost does
+not depend on the values).
 
 Prints ONE JSON line.  `value` is steps/s of the whole step; `roofline`
 describes the dominant kernel (timed with HIP events on the library's stream
@@ -52,6 +57,84 @@ def kl_step_flops(m: int, n: int) -> float:
     """step_flops plus the KL accumulation's extra products: Q^T F for the
     eigenvalue estimates of both factors and the projections Q_L^T G, G Q_R."""
     return step_flops(m, n) + 2.0 * (m ** 3 + n ** 3) + 2.0 * m * n * (m + n)
+
+
+MUON_COEFFS = [(15 / 8, -5 / 4, 3 / 8)] * 16
+MUON_HP = dict(beta1=0.9, lr=2e-2, weight_decay=0.1, eps=1e-7)
+
+
+def muon_step_flops(m: int, n: int, iters: int = 16) -> float:
+    """Per Newton-Schulz iteration on the smaller side d (other side e): one
+    triangle of the Gram matrix d(d+1)e, the square 2d^3 and the product 2d^2e."""
+    d, e = min(m, n), max(m, n)
+    return iters * (d * (d + 1) * e + 2.0 * d ** 3 + 2.0 * d * d * e)
+
+
+def bench_muon(args, soap, torch, sg):
+    spec = sg.workload(2).matrices[0]
+    m, n = spec.m, spec.n
+    total = args.warmup + args.steps
+    grads = [torch.from_numpy(G).cuda() for G in sg.make_matrix_stream(spec, 2, total)]
+    W = torch.from_numpy(sg.initial_weight(spec, 2)).cuda()
+    state = soap.MuonState(m, n)
+    stream = torch.cuda.current_stream()
+    for t in range(args.warmup):
+        state.step(W, grads[t], MUON_COEFFS, **MUON_HP)
+    torch.cuda.synchronize()
+    soap.soap_timing_reset()
+    soap.soap_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.steps):
+        state.step(W, grads[args.warmup + t], MUON_COEFFS, stream=stream, **MUON_HP)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    soap.soap_timing_enable(False)
+    soap.soap_timing_collect()
+    stages = {}
+    for i in range(soap.soap_timing_num_stages()):
+        ms, launches, fl = soap.soap_timing_get(i)
+        if launches:
+            stages[soap.soap_timing_stage_name(i)] = (ms, launches, fl)
+    ns_ms, ns_n, ns_fl = stages["muon_newton_schulz"]
+    achieved = ns_fl / (ns_ms * 1e-3) / 1e12
+    F = muon_step_flops(m, n)
+    value = args.steps / elapsed
+    out = {
+        "metric": "Muon steps/s per weight shape + achieved MFMA TFLOPS fraction (1 GPU)",
+        "value": value, "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * elapsed / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded low-rank + noise gradients, rank 128, 10% noise)",
+        "config": {"workload": f"soap_muon_step on one {m}x{n} fp32 weight (MLP up-projection), "
+                               f"16 Newton-Schulz iterations in fp32",
+                   "m": m, "n": n, "rank": spec.rank, "global_batch": 1, "seq_len": None,
+                   "parallelism": "none (1 GPU)"},
+        "step_tflops": F * value / 1e12,
+        "step_frac_of_fp32_mfma_peak": F * value / 1e12 / PEAK_FP32_MFMA_TFLOPS,
+        "roofline": {"bound": "mfma", "kernel": "muon_newton_schulz (SYRK + two GEMMs per "
+                                                "iteration)",
+                     "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
+                     "avg_launch_ms": ns_ms / ns_n},
+        "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        ms_, ns_ = m // 4, n // 4
+        sp = sg.MatrixSpec("cpu_sample", ms_, ns_, max(1, spec.rank // 4), "rel", 0.10)
+        G = next(sg.make_matrix_stream(sp, 2, 1)).astype(np.float64)
+        t1 = time.perf_counter()
+        oracle.muon_step(np.zeros((ms_, ns_)), np.zeros((ms_, ns_)), G, coeffs=MUON_COEFFS,
+                         **MUON_HP)
+        dt = time.perf_counter() - t1
+        ratio = muon_step_flops(m, n) / muon_step_flops(ms_, ns_)
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or len(os.sched_getaffinity(0))
+        out["cpu_baseline"] = {
+            "value": 1.0 / (dt * ratio), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"one fp64 oracle Muon step on a {ms_}x{ns_} matrix took {dt:.2f} s; "
+                      f"scaled by the exact flop ratio {ratio:.1f}"}
+    print(json.dumps(out), flush=True)
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "power_product_R_4096x14336_traffic.json")
@@ -114,6 +197,7 @@ def main():
     ap.add_argument("--kl", action="store_true", help="time the KL-SOAP step")
     ap.add_argument("--refresh-every", type=int, default=1)
     ap.add_argument("--stale", action="store_true")
+    ap.add_argument("--muon", action="store_true", help="time the Muon step instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the SOAP step of a "
@@ -127,6 +211,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.muon:
+        return bench_muon(args, soap, torch, sg)
     wl = sg.workload(2)
     spec = wl.matrices[0]
     m, n = spec.m, spec.n
