@@ -5,7 +5,9 @@
 // Tiling: a 256-thread workgroup (4 wave64s in a 2 x 2 arrangement) computes a
 // 128 x 128 tile of C; each wave owns a 64 x 64 sub-tile held as 2 x 2 MFMA
 // 32x32 accumulators (64 accumulation registers per lane).  K advances in slabs
-// of 16 staged through double-buffered LDS.  Both operands are kept in LDS as
+// of 16 staged through double-buffered LDS; for long K the global loads run two
+// slabs ahead in two register sets, with every load issued unconditionally at
+// a clamped address so that the waits cover exactly the slab being stored.  Both operands are kept in LDS as
 // [x][k] rows (x = output row or column, k contiguous, padded to 20 floats so
 // that 16-byte reads of 16 consecutive lanes fall in distinct banks); a lane
 // then fetches the 8 k-values it feeds to 8 consecutive MFMAs with two
@@ -32,6 +34,7 @@ constexpr int TILE_FLOATS = 128 * LDSK;  // one operand tile in LDS
 constexpr int NTHREADS = 256;
 constexpr int SHORT_K = 512;    // products with at most this much K per slice use the rank-k kernel
 constexpr int GROUP_M = 8;
+
 
 enum { MODE_GENERAL = 0, MODE_SYRK = 1, MODE_ADAM = 2 };
 
@@ -63,6 +66,12 @@ template <bool KCONTIG, int VEC>
 struct SlabLoader {
   float r[8];
 
+  // Every load is issued unconditionally at an address clamped into the
+  // matrix, and values outside it are replaced by zero afterwards: with no
+  // branch around the loads the compiler can wait for exactly the loads a
+  // store needs, which the two-slab prefetch of the long-K loop relies on.
+  // Requires X >= 1, K >= 1 (and the VEC == 4 preconditions: K % 4 == 0 for
+  // k-contiguous, X even for x-contiguous operands).
   __device__ __forceinline__ void load(const float *__restrict__ base, int64_t ld, int x0,
                                        int k0, int X, int K, int tid) {
 #pragma unroll
@@ -71,14 +80,18 @@ struct SlabLoader {
       if (KCONTIG) {
         const int x = x0 + (idx >> 2);
         const int k = k0 + 4 * (idx & 3);
+        const int64_t row = (int64_t)min(x, X - 1) * ld;
         if (VEC == 4) {
-          float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (x < X && k < K) v = *reinterpret_cast<const float4 *>(base + (int64_t)x * ld + k);
-          r[4 * s + 0] = v.x; r[4 * s + 1] = v.y; r[4 * s + 2] = v.z; r[4 * s + 3] = v.w;
+          const float4 v = *reinterpret_cast<const float4 *>(base + row + min(k, K - 4));
+          const bool ok = x < X && k < K;
+          r[4 * s + 0] = ok ? v.x : 0.f; r[4 * s + 1] = ok ? v.y : 0.f;
+          r[4 * s + 2] = ok ? v.z : 0.f; r[4 * s + 3] = ok ? v.w : 0.f;
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            r[4 * s + e] = (x < X && k + e < K) ? base[(int64_t)x * ld + k + e] : 0.f;
+          for (int e = 0; e < 4; ++e) {
+            const float v = base[row + min(k + e, K - 1)];
+            r[4 * s + e] = (x < X && k + e < K) ? v : 0.f;
+          }
         }
       } else if (VEC == 4) {
         // x-contiguous with 8-byte loads: thread -> (k-quad, x pair); the
@@ -87,20 +100,25 @@ struct SlabLoader {
         if (s == 0) {
           const int x = x0 + 2 * (tid & 63);
           const int k = k0 + 4 * (tid >> 6);
+          const int xc = min(x, X - 2);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            float2 v = make_float2(0.f, 0.f);
-            if (x < X && k + e < K) v = *reinterpret_cast<const float2 *>(base + (int64_t)(k + e) * ld + x);
-            r[e] = v.x;
-            r[4 + e] = v.y;
+            const float2 v =
+                *reinterpret_cast<const float2 *>(base + (int64_t)min(k + e, K - 1) * ld + xc);
+            const bool ok = x < X && k + e < K;
+            r[e] = ok ? v.x : 0.f;
+            r[4 + e] = ok ? v.y : 0.f;
           }
         }
       } else {
         const int x = x0 + (idx & 127);
         const int k = k0 + 4 * (idx >> 7);
+        const int xc = min(x, X - 1);
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          r[4 * s + e] = (x < X && k + e < K) ? base[(int64_t)(k + e) * ld + x] : 0.f;
+        for (int e = 0; e < 4; ++e) {
+          const float v = base[(int64_t)min(k + e, K - 1) * ld + xc];
+          r[4 * s + e] = (x < X && k + e < K) ? v : 0.f;
+        }
       }
     }
   }
@@ -199,23 +217,8 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   const int kbeg = blockIdx.y * p.kslice;
   const int kend = min(p.K, kbeg + p.kslice);
   const int nk = (kend - kbeg + BK - 1) / BK;
-  la.load(A, p.lda, m0, kbeg, p.M, kend, tid);
-  if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, kbeg, p.M, kend, tid);
-  lb.load(B, p.ldb, n0, kbeg, p.N, kend, tid);
-  la.store(buf(0, 0), tid);
-  if (MODE == MODE_ADAM) la2.store(buf(0, 1), tid);
-  lb.store(buf(0, NA), tid);
-  __syncthreads();
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int k0 = kbeg + (kt + 1) * BK;
-      la.load(A, p.lda, m0, k0, p.M, kend, tid);
-      if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, k0, p.M, kend, tid);
-      lb.load(B, p.ldb, n0, k0, p.N, kend, tid);
-    }
+  // One K slab from LDS buffer `cur` into the accumulators.
+  auto compute = [&](int cur) {
     float fb[2][8];
     read_frag(buf(cur, NA), wn * 64 + xl, h, fb[0]);
     read_frag(buf(cur, NA), wn * 64 + 32 + xl, h, fb[1]);
@@ -233,12 +236,75 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
             acc[a][i][j] =
                 __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[a][i][j], 0, 0, 0);
     }
-    if (more) {
-      la.store(buf(cur ^ 1, 0), tid);
-      if (MODE == MODE_ADAM) la2.store(buf(cur ^ 1, 1), tid);
-      lb.store(buf(cur ^ 1, NA), tid);
+  };
+
+  if constexpr (!SHORTK) {
+    // Long K: global loads run two slabs ahead of the matrix cores (two
+    // register sets), so a slab's loads have two slabs of MFMA work to land.
+    SlabLoader<TA == 0, VEC> lc, lc2;
+    SlabLoader<TB == 1, VEC> ld;
+    auto load_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TA == 0, VEC> &xa2,
+                        SlabLoader<TB == 1, VEC> &xb, int kt) {
+      const int k0 = kbeg + kt * BK;
+      xa.load(A, p.lda, m0, k0, p.M, kend, tid);
+      if (MODE == MODE_ADAM) xa2.load(A2, p.lda, m0, k0, p.M, kend, tid);
+      xb.load(B, p.ldb, n0, k0, p.N, kend, tid);
+    };
+    auto store_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TA == 0, VEC> &xa2,
+                         SlabLoader<TB == 1, VEC> &xb, int stage) {
+      xa.store(buf(stage, 0), tid);
+      if (MODE == MODE_ADAM) xa2.store(buf(stage, 1), tid);
+      xb.store(buf(stage, NA), tid);
+    };
+    // slab kt is computed from LDS while the register set `held` carries
+    // slab kt+1 (stored to the other buffer after the MFMAs) and `next`
+    // receives slab kt+2.
+    auto body = [&](int kt, SlabLoader<TA == 0, VEC> &ha, SlabLoader<TA == 0, VEC> &ha2,
+                    SlabLoader<TB == 1, VEC> &hb, SlabLoader<TA == 0, VEC> &na,
+                    SlabLoader<TA == 0, VEC> &na2, SlabLoader<TB == 1, VEC> &nb) {
+      const int cur = kt & 1;
+      load_set(na, na2, nb, kt + 2);   // past the end: clamped loads, all zero
+      compute(cur);
+      if (kt + 1 < nk) store_set(ha, ha2, hb, cur ^ 1);
+      __syncthreads();
+    };
+    if (nk > 0) {
+      load_set(lc, lc2, ld, 0);
+      store_set(lc, lc2, ld, 0);
+      load_set(la, la2, lb, 1);
     }
     __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      body(kt, la, la2, lb, lc, lc2, ld);
+      if (kt + 1 < nk) body(kt + 1, lc, lc2, ld, la, la2, lb);
+    }
+  } else {
+    if (nk > 0) {
+      la.load(A, p.lda, m0, kbeg, p.M, kend, tid);
+      if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, kbeg, p.M, kend, tid);
+      lb.load(B, p.ldb, n0, kbeg, p.N, kend, tid);
+      la.store(buf(0, 0), tid);
+      if (MODE == MODE_ADAM) la2.store(buf(0, 1), tid);
+      lb.store(buf(0, NA), tid);
+    }
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int cur = kt & 1;
+      const bool more = kt + 1 < nk;
+      if (more) {
+        const int k0 = kbeg + (kt + 1) * BK;
+        la.load(A, p.lda, m0, k0, p.M, kend, tid);
+        if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, k0, p.M, kend, tid);
+        lb.load(B, p.ldb, n0, k0, p.N, kend, tid);
+      }
+      compute(cur);
+      if (more) {
+        la.store(buf(cur ^ 1, 0), tid);
+        if (MODE == MODE_ADAM) la2.store(buf(cur ^ 1, 1), tid);
+        lb.store(buf(cur ^ 1, NA), tid);
+      }
+      __syncthreads();
+    }
   }
 
   // Epilogue.  Accumulator register r of block (i, j) holds
