@@ -7,7 +7,7 @@ are generated and copied to HBM before the timed region.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
                     [--calibration-copy-mib N] [--kl] [--refresh-every F] [--stale]
-                    [--muon]
+                    [--muon] [--workload {1,3,4}] [--group]
 
 --kl times the KL-SOAP step instead (soap_kl_step, beta_kron 0.95): the
 factors are accumulated by the KL-Shampoo rule, the rest of the step is the
@@ -17,7 +17,12 @@ factors before the step's gradient (the ablation of Section 5.4.1).  --muon
 times the Muon step of Algorithm 1 on the same weight instead (16
 Newton-Schulz iterations; the paper's PolarExpress coefficients are not
 printed, so the Taylor quintic (15/8, -5/4, 3/8) stands in: the cost does
-not depend on the values).
+not depend on the values).  --workload 1 / 3 / 4 time the SOAP step on the
+other workloads instead: the 4096 x 4096 attention projection, the bank of 64
+experts of 2048 x 768 through soap_step_batched, and the 24-layer model (96
+matrices of four shapes; one soap_step per matrix from one host loop, or with
+--group one soap_step_batched per shape).  These reuse one gradient per
+matrix for every step.
 
 Prints ONE JSON line.  `value` is steps/s of the whole step; `roofline`
 describes the dominant kernel (timed with HIP events on the library's stream
@@ -137,6 +142,74 @@ def bench_muon(args, soap, torch, sg):
     print(json.dumps(out), flush=True)
 
 
+def bench_workload(args, soap, torch, sg):
+    """Whole-workload SOAP step time on workload 1, 3 or 4 (information lines)."""
+    wl = sg.workload(args.workload)
+    specs = wl.matrices
+    groups = {}
+    for sp in specs:
+        groups.setdefault((sp.m, sp.n), []).append(sp)
+    scales = sg.expert_scales(0, 3, len(specs)) if args.workload == 3 else None
+    calls = []   # (state, W, G) with W, G on the device; batched states take stacked tensors
+    total_flops = sum(step_flops(sp.m, sp.n) for sp in specs)
+
+    def grad(sp, i):
+        g = next(sg.make_matrix_stream(sp, args.workload, 1))
+        return g * np.float32(scales[i]) if scales is not None else g
+
+    if args.workload == 3 or args.group:
+        for (m, n), sps in groups.items():
+            idx = [specs.index(sp) for sp in sps]
+            W = torch.from_numpy(np.stack([sg.initial_weight(sp, args.workload) for sp in sps])).cuda()
+            G = torch.from_numpy(np.stack([grad(sp, i) for sp, i in zip(sps, idx)])).cuda()
+            st = soap.SoapState(m, n, batch=len(sps))
+            calls.append((st, W, G))
+    else:
+        shared = {}
+        for i, sp in enumerate(specs):
+            key = (sp.m, sp.n)
+            if key not in shared:
+                shared[key] = soap.SoapState(sp.m, sp.n)
+            st = shared[key]
+            own = soap.SoapState.__new__(soap.SoapState)   # state tensors per matrix, shared workspace
+            own.__dict__.update(st.__dict__)
+            kw = dict(dtype=torch.float32, device="cuda")
+            own.L = torch.empty((sp.m, sp.m), **kw); own.R = torch.empty((sp.n, sp.n), **kw)
+            own.Q_L = torch.empty((sp.m, sp.m), **kw); own.Q_R = torch.empty((sp.n, sp.n), **kw)
+            own.M = torch.empty((sp.m, sp.n), **kw); own.V = torch.empty((sp.m, sp.n), **kw)
+            soap.soap_init_state(1, sp.m, sp.n, own.L, own.R, own.Q_L, own.Q_R, own.M, own.V)
+            calls.append((own, torch.from_numpy(sg.initial_weight(sp, args.workload)).cuda(),
+                          torch.from_numpy(grad(sp, i)).cuda()))
+    stream = torch.cuda.current_stream()
+    for t in range(1, args.warmup + 1):
+        for st, W, G in calls:
+            st.step(W, G, t, **HP)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(1, args.steps + 1):
+        for st, W, G in calls:
+            st.step(W, G, args.warmup + t, stream=stream, **HP)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    value = args.steps / elapsed
+    desc = {1: "soap_step on one 4096x4096 fp32 weight (attention projection)",
+            3: "soap_step_batched on 64 experts of 2048x768 (one call)",
+            4: "the 24-layer dense model (hidden 2048, FFN 8192): 96 matrices, "
+               + ("one soap_step_batched per shape" if args.group else "one soap_step per matrix")}
+    out = {
+        "metric": "SOAP steps/s of the whole workload (1 GPU)", "value": value, "unit": "steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": 1e3 * elapsed / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded low-rank + noise gradients; one gradient per matrix reused)",
+        "config": {"workload": desc[args.workload], "matrices": len(specs),
+                   "shapes": sorted(groups.keys()), "parallelism": "none (1 GPU)"},
+        "step_tflops": total_flops * value / 1e12,
+        "step_frac_of_fp32_mfma_peak": total_flops * value / 1e12 / PEAK_FP32_MFMA_TFLOPS,
+    }
+    print(json.dumps(out), flush=True)
+
+
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "power_product_R_4096x14336_traffic.json")
 GEMM_SOURCE = os.path.join(ROOT, "paper_2607_20548_amd", "csrc", "gemm.hip")
 
@@ -198,6 +271,9 @@ def main():
     ap.add_argument("--refresh-every", type=int, default=1)
     ap.add_argument("--stale", action="store_true")
     ap.add_argument("--muon", action="store_true", help="time the Muon step instead")
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4])
+    ap.add_argument("--group", action="store_true",
+                    help="workload 4: one batched call per shape instead of one call per matrix")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the SOAP step of a "
@@ -213,6 +289,8 @@ def main():
     torch.cuda.set_device(0)
     if args.muon:
         return bench_muon(args, soap, torch, sg)
+    if args.workload != 2:
+        return bench_workload(args, soap, torch, sg)
     wl = sg.workload(2)
     spec = wl.matrices[0]
     m, n = spec.m, spec.n
