@@ -67,11 +67,15 @@ struct SlabLoader {
   float r[8];
 
   // Every load is issued unconditionally at an address clamped into the
-  // matrix, and values outside it are replaced by zero afterwards: with no
-  // branch around the loads the compiler can wait for exactly the loads a
-  // store needs, which the two-slab prefetch of the long-K loop relies on.
-  // Requires X >= 1, K >= 1 (and the VEC == 4 preconditions: K % 4 == 0 for
-  // k-contiguous, X even for x-contiguous operands).
+  // matrix: with no branch around the loads the compiler can wait for exactly
+  // the loads a store needs, which the two-slab prefetch of the long-K loop
+  // relies on.  With VEC == 4 the values are used as loaded: rows x >= X only
+  // reach output rows or columns that are never written, and k-values past
+  // the end of K are zeroed by store() (kvalid), right before they go to LDS,
+  // so that nothing consumes a loaded register early.  The scalar path
+  // (VEC == 1) masks both at load time.  Requires X >= 1, K >= 1 (and the
+  // VEC == 4 preconditions: K % 4 == 0 for k-contiguous, X even for
+  // x-contiguous operands).
   __device__ __forceinline__ void load(const float *__restrict__ base, int64_t ld, int x0,
                                        int k0, int X, int K, int tid) {
 #pragma unroll
@@ -83,9 +87,7 @@ struct SlabLoader {
         const int64_t row = (int64_t)min(x, X - 1) * ld;
         if (VEC == 4) {
           const float4 v = *reinterpret_cast<const float4 *>(base + row + min(k, K - 4));
-          const bool ok = x < X && k < K;
-          r[4 * s + 0] = ok ? v.x : 0.f; r[4 * s + 1] = ok ? v.y : 0.f;
-          r[4 * s + 2] = ok ? v.z : 0.f; r[4 * s + 3] = ok ? v.w : 0.f;
+          r[4 * s + 0] = v.x; r[4 * s + 1] = v.y; r[4 * s + 2] = v.z; r[4 * s + 3] = v.w;
         } else {
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
@@ -96,18 +98,19 @@ struct SlabLoader {
       } else if (VEC == 4) {
         // x-contiguous with 8-byte loads: thread -> (k-quad, x pair); the
         // 4 x 2 block is transposed in registers (r[0..3] = column x,
-        // r[4..7] = column x+1).  Needs an even x extent and leading dimension.
+        // r[4..7] = column x+1).  Needs an even x extent and leading
+        // dimension.  k is uniform within a wave, so the row address is
+        // formed on the scalar unit and each lane adds its column offset.
         if (s == 0) {
           const int x = x0 + 2 * (tid & 63);
-          const int k = k0 + 4 * (tid >> 6);
-          const int xc = min(x, X - 2);
+          const int k = k0 + 4 * __builtin_amdgcn_readfirstlane(tid >> 6);
+          const unsigned xc = (unsigned)min(x, X - 2);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float2 v =
-                *reinterpret_cast<const float2 *>(base + (int64_t)min(k + e, K - 1) * ld + xc);
-            const bool ok = x < X && k + e < K;
-            r[e] = ok ? v.x : 0.f;
-            r[4 + e] = ok ? v.y : 0.f;
+            const float *rowp = base + (int64_t)min(k + e, K - 1) * ld;
+            const float2 v = *reinterpret_cast<const float2 *>(rowp + xc);
+            r[e] = v.x;
+            r[4 + e] = v.y;
           }
         }
       } else {
@@ -123,7 +126,25 @@ struct SlabLoader {
     }
   }
 
-  __device__ __forceinline__ void store(float *lds, int tid) const {
+  // Writes the slab to LDS as [x][k] rows; kvalid = number of k-values of
+  // this slab inside K (BK except in the last, ragged slab).
+  __device__ __forceinline__ void store(float *lds, int tid, int kvalid) {
+    if (VEC == 4 && kvalid < BK) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int idx = tid + NTHREADS * s;
+        const int kl = KCONTIG ? 4 * (idx & 3) : 4 * (tid >> 6);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (KCONTIG) {
+            if (kl >= kvalid) r[4 * s + e] = 0.f;   // K % 4 == 0: whole quads
+          } else if (s == 0 && kl + e >= kvalid) {
+            r[e] = 0.f;
+            r[4 + e] = 0.f;
+          }
+        }
+      }
+    }
     if (!KCONTIG && VEC == 4) {
       const int xl = 2 * (tid & 63), kq = tid >> 6;
       *reinterpret_cast<float4 *>(lds + xl * LDSK + 4 * kq) = make_float4(r[0], r[1], r[2], r[3]);
@@ -251,10 +272,11 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
       xb.load(B, p.ldb, n0, k0, p.N, kend, tid);
     };
     auto store_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TA == 0, VEC> &xa2,
-                         SlabLoader<TB == 1, VEC> &xb, int stage) {
-      xa.store(buf(stage, 0), tid);
-      if (MODE == MODE_ADAM) xa2.store(buf(stage, 1), tid);
-      xb.store(buf(stage, NA), tid);
+                         SlabLoader<TB == 1, VEC> &xb, int stage, int kt) {
+      const int kvalid = min(BK, kend - (kbeg + kt * BK));
+      xa.store(buf(stage, 0), tid, kvalid);
+      if (MODE == MODE_ADAM) xa2.store(buf(stage, 1), tid, kvalid);
+      xb.store(buf(stage, NA), tid, kvalid);
     };
     // slab kt is computed from LDS while the register set `held` carries
     // slab kt+1 (stored to the other buffer after the MFMAs) and `next`
@@ -265,12 +287,12 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
       const int cur = kt & 1;
       load_set(na, na2, nb, kt + 2);   // past the end: clamped loads, all zero
       compute(cur);
-      if (kt + 1 < nk) store_set(ha, ha2, hb, cur ^ 1);
+      if (kt + 1 < nk) store_set(ha, ha2, hb, cur ^ 1, kt + 1);
       __syncthreads();
     };
     if (nk > 0) {
       load_set(lc, lc2, ld, 0);
-      store_set(lc, lc2, ld, 0);
+      store_set(lc, lc2, ld, 0, 0);
       load_set(la, la2, lb, 1);
     }
     __syncthreads();
@@ -283,9 +305,10 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
       la.load(A, p.lda, m0, kbeg, p.M, kend, tid);
       if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, kbeg, p.M, kend, tid);
       lb.load(B, p.ldb, n0, kbeg, p.N, kend, tid);
-      la.store(buf(0, 0), tid);
-      if (MODE == MODE_ADAM) la2.store(buf(0, 1), tid);
-      lb.store(buf(0, NA), tid);
+      const int kvalid = min(BK, kend - kbeg);
+      la.store(buf(0, 0), tid, kvalid);
+      if (MODE == MODE_ADAM) la2.store(buf(0, 1), tid, kvalid);
+      lb.store(buf(0, NA), tid, kvalid);
     }
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
@@ -299,9 +322,10 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
       }
       compute(cur);
       if (more) {
-        la.store(buf(cur ^ 1, 0), tid);
-        if (MODE == MODE_ADAM) la2.store(buf(cur ^ 1, 1), tid);
-        lb.store(buf(cur ^ 1, NA), tid);
+        const int kvalid = min(BK, kend - (kbeg + (kt + 1) * BK));
+        la.store(buf(cur ^ 1, 0), tid, kvalid);
+        if (MODE == MODE_ADAM) la2.store(buf(cur ^ 1, 1), tid, kvalid);
+        lb.store(buf(cur ^ 1, NA), tid, kvalid);
       }
       __syncthreads();
     }
