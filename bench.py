@@ -42,6 +42,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix peak (256 CU x 256 flop/clk x 2.4 GHz)
+PEAK_BF16_MFMA_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak (datasheet, no sparsity)
 PEAK_HBM_GBS = 8000.0
 HP = dict(beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3, weight_decay=0.1)
 BETA_KRON = 0.95   # KL-Shampoo accumulation coefficient (hyperparameter table of Section 5.4)
@@ -83,15 +84,16 @@ def bench_muon(args, soap, torch, sg):
     W = torch.from_numpy(sg.initial_weight(spec, 2)).cuda()
     state = soap.MuonState(m, n)
     stream = torch.cuda.current_stream()
+    bf = bool(args.bf16)
     for t in range(args.warmup):
-        state.step(W, grads[t], MUON_COEFFS, **MUON_HP)
+        state.step(W, grads[t], MUON_COEFFS, bf16=bf, **MUON_HP)
     torch.cuda.synchronize()
     soap.soap_timing_reset()
     soap.soap_timing_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(args.steps):
-        state.step(W, grads[args.warmup + t], MUON_COEFFS, stream=stream, **MUON_HP)
+        state.step(W, grads[args.warmup + t], MUON_COEFFS, bf16=bf, stream=stream, **MUON_HP)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     soap.soap_timing_enable(False)
@@ -105,22 +107,24 @@ def bench_muon(args, soap, torch, sg):
     achieved = ns_fl / (ns_ms * 1e-3) / 1e12
     F = muon_step_flops(m, n)
     value = args.steps / elapsed
+    peak = PEAK_BF16_MFMA_TFLOPS if bf else PEAK_FP32_MFMA_TFLOPS
     out = {
         "metric": "Muon steps/s per weight shape + achieved MFMA TFLOPS fraction (1 GPU)",
         "value": value, "unit": "steps/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": 1e3 * elapsed / args.steps,
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 (Newton-Schulz), f32 (rest)" if bf else "f32",
         "data": "synthetic (seeded low-rank + noise gradients, rank 128, 10% noise)",
         "config": {"workload": f"soap_muon_step on one {m}x{n} fp32 weight (MLP up-projection), "
-                               f"16 Newton-Schulz iterations in fp32",
+                               f"16 Newton-Schulz iterations in {'bf16' if bf else 'fp32'}",
                    "m": m, "n": n, "rank": spec.rank, "global_batch": 1, "seq_len": None,
                    "parallelism": "none (1 GPU)"},
         "step_tflops": F * value / 1e12,
         "step_frac_of_fp32_mfma_peak": F * value / 1e12 / PEAK_FP32_MFMA_TFLOPS,
         "roofline": {"bound": "mfma", "kernel": "muon_newton_schulz (SYRK + two GEMMs per "
                                                 "iteration)",
-                     "achieved": achieved, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": None,
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
                      "avg_launch_ms": ns_ms / ns_n},
         "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
     }
@@ -271,6 +275,8 @@ def main():
     ap.add_argument("--refresh-every", type=int, default=1)
     ap.add_argument("--stale", action="store_true")
     ap.add_argument("--muon", action="store_true", help="time the Muon step instead")
+    ap.add_argument("--bf16", action="store_true",
+                    help="with --muon: Newton-Schulz in bfloat16 (the paper's precision)")
     ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4])
     ap.add_argument("--group", action="store_true",
                     help="workload 4: one batched call per shape instead of one call per matrix")

@@ -162,8 +162,15 @@ int soap_kl_step_batched(int64_t batch, float *param, const float *grad, float *
  * caller supplies the schedule.  param, grad, M are device pointers in the
  * layout of soap_step (grad read only, param and M updated); beta1 in [0, 1),
  * lr and weight_decay finite and >= 0, eps finite and > 0, n_iters in
- * [0, 1024], flags 0.  The products run in fp32 on the matrix cores.
+ * [0, 1024].  flags 0: the products run in fp32 on the matrix cores.
+ * flags SOAP_MUON_BF16: the Newton-Schulz iterations run in bfloat16, the
+ * paper's precision for them (its discussion of orthogonalisation accuracy
+ * in the conclusion): X_0, every A, B and X are bfloat16, each product
+ * accumulated in fp32 on the bf16 matrix cores and rounded once to nearest
+ * (ties to even); the momentum, the norm and the weight update stay fp32.
+ * It needs m and n multiples of 8 (SOAP_ERR_SHAPE otherwise).
  * Ownership, streams and errors as for soap_step. */
+enum { SOAP_MUON_BF16 = 1u << 0 };
 size_t soap_muon_workspace_bytes(int64_t batch, int64_t m, int64_t n);
 int soap_muon_step(float *param, const float *grad, float *M, int64_t m, int64_t n, float beta1,
                    float lr, float weight_decay, float eps, const float *coeffs, int64_t n_iters,

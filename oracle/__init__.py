@@ -18,4 +18,4 @@ from .soap_oracle import (  # noqa: F401
     soap_step_batched, eigenvalue_estimates, kl_factor_update, kl_factors, kl_soap_step,
     kl_soap_step_batched, refresh_due,
 )
-from .muon_oracle import newton_schulz, muon_step  # noqa: F401
+from .muon_oracle import newton_schulz, muon_step, round_bf16  # noqa: F401

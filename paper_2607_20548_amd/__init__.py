@@ -28,6 +28,7 @@ SOAP_ERR_HIP = -7
 SOAP_FLAG_NO_BIAS_CORRECTION = 1
 SOAP_FLAG_SKIP_REFRESH = 2
 SOAP_FLAG_STALE_REFRESH = 4
+SOAP_MUON_BF16 = 1
 SOAP_MAX_DIM = 16384
 
 EXPORTED = [
@@ -353,14 +354,16 @@ class MuonState:
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
 
     def step(self, param, grad, coeffs, beta1=0.9, lr=1e-3, weight_decay=0.1, eps=1e-7,
-             stream=None) -> None:
-        """coeffs: a sequence of (a, b, c) Newton-Schulz triples, one per iteration."""
+             bf16=False, stream=None) -> None:
+        """coeffs: a sequence of (a, b, c) Newton-Schulz triples, one per iteration.
+        bf16: Newton-Schulz in bfloat16 (SOAP_MUON_BF16)."""
         flat = [float(x) for abc in coeffs for x in abc]
         n_iters = len(flat) // 3
+        flags = SOAP_MUON_BF16 if bf16 else 0
         if self.batch == 1:
             soap_muon_step(param, grad, self.M, self.m, self.n, beta1, lr, weight_decay, eps, flat,
-                           n_iters, 0, self.workspace, self.ws_bytes, stream)
+                           n_iters, flags, self.workspace, self.ws_bytes, stream)
         else:
             soap_muon_step_batched(self.batch, param, grad, self.M, self.m, self.n, beta1, lr,
-                                   weight_decay, eps, flat, n_iters, 0, self.workspace,
+                                   weight_decay, eps, flat, n_iters, flags, self.workspace,
                                    self.ws_bytes, stream)

@@ -102,6 +102,45 @@ hipError_t launch_muon_normalise(const float *M, float *X, int64_t batch, int64_
 // W <- alpha W + beta X over `count` floats.
 hipError_t launch_axpby(float *W, const float *X, int64_t count, float alpha, float beta,
                         hipStream_t s);
+// inv[b] = 1 / max(||M_b||_F, eps) only (norm in double, fixed order).
+hipError_t launch_muon_norm_inv(const float *M, int64_t batch, int64_t count, float eps,
+                                double *part, float *inv, hipStream_t s);
+
+// ---------------------------------------------------- bfloat16 products
+// C = round_bf16(alpha * P Q^T + beta * D) for `batch` products (element
+// strides sP, sQ, sD, sC, sCt), bfloat16 stored as uint16_t, row-major:
+// P is M x K (rows k-contiguous, leading dimension ldp), Q is N x K, D and C
+// are M x N.  D may be null (beta ignored).  syrk: M == N, P == Q, only the
+// tiles on or below the diagonal are computed and C is written mirrored.
+// Ct, if not null, receives C^T (N x M, leading dimension ldct).  Needs
+// K, ldp, ldq multiples of 8, ldct a multiple of 4 and 16-byte aligned
+// P, Q (else hipErrorInvalidValue).  The sum runs in fp32 on the matrix
+// cores; C is rounded once, to nearest with ties to even.
+struct BfGemmDesc {
+  int64_t M = 0, N = 0, K = 0;
+  const uint16_t *P = nullptr;
+  int64_t ldp = 0, sP = 0;
+  const uint16_t *Q = nullptr;
+  int64_t ldq = 0, sQ = 0;
+  const uint16_t *D = nullptr;
+  int64_t ldd = 0, sD = 0;
+  uint16_t *C = nullptr;
+  int64_t ldc = 0, sC = 0;
+  uint16_t *Ct = nullptr;
+  int64_t ldct = 0, sCt = 0;
+  float alpha = 1.f, beta = 0.f;
+  int64_t batch = 1;
+  bool syrk = false;
+};
+hipError_t launch_gemm_bf16_nt(const BfGemmDesc &d, hipStream_t s);
+// Xo = round_bf16(inv[b] * S_b) (rows x cols; S_b read transposed, i.e. as a
+// cols x rows fp32 matrix, when trans) and Xt = Xo^T, per batch entry b.
+hipError_t launch_bf16_scale_both(const float *S, int64_t batch, int64_t rows, int64_t cols,
+                                  bool trans, const float *inv, uint16_t *Xo, uint16_t *Xt,
+                                  hipStream_t s);
+// W <- alpha W + beta X over `count` values (X bfloat16).
+hipError_t launch_axpby_bf16(float *W, const uint16_t *X, int64_t count, float alpha, float beta,
+                             hipStream_t s);
 
 // ----------------------------------------------------------------- QR
 // Blocked Householder QR of `batch` n x n matrices A, each given TRANSPOSED:

@@ -91,6 +91,18 @@ hipError_t launch_muon_normalise(const float *M, float *X, int64_t batch, int64_
   return hipGetLastError();
 }
 
+hipError_t launch_muon_norm_inv(const float *M, int64_t batch, int64_t count, float eps,
+                                double *part, float *inv, hipStream_t s) {
+  if (batch <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(norm_partial, dim3(NR_BLOCKS, (unsigned)batch), dim3(NR_THREADS), 0, s, M,
+                     count, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(norm_finish, dim3((unsigned)((batch + 63) / 64)), dim3(64), 0, s, part,
+                     batch, eps, inv);
+  return hipGetLastError();
+}
+
 hipError_t launch_axpby(float *W, const float *X, int64_t count, float alpha, float beta,
                         hipStream_t s) {
   if (count <= 0) return hipSuccess;

@@ -730,6 +730,71 @@ MuonLayout muon_layout(int64_t batch, int64_t m, int64_t n) {
 
 constexpr int64_t kMuonMaxIters = 1024;
 
+// Newton-Schulz in bfloat16 (SOAP_MUON_BF16), after the momentum update:
+// X, A and B are bfloat16, each product accumulated in fp32 on the matrix
+// cores and rounded once.  The iterate of the d x e problem (d = min(m, n))
+// is kept in both layouts, X (d x e) and X^T (e x d), so that every product
+// reads k-contiguous rows: A = X X^T and B = b A + c A A^T (A symmetric) as
+// one-triangle products, X <- a X + B X as (B, X^T) with both layouts of the
+// result written.  The workspace of the fp32 form holds these buffers.
+int muon_ns_bf16(int64_t batch, float *param, const float *M, int64_t m, int64_t n, float lr,
+                 float wd, float eps, const float *coeffs, int64_t iters, char *w,
+                 const MuonLayout &lay, hipStream_t s) {
+  const bool tall = m > n;
+  const int64_t d = tall ? n : m, e2 = tall ? m : n;
+  const int64_t mn = m * n, dd = d * d;
+  uint16_t *X = reinterpret_cast<uint16_t *>(w + lay.x), *Xt = X + batch * mn;
+  uint16_t *Y = reinterpret_cast<uint16_t *>(w + lay.xn), *Yt = Y + batch * mn;
+  uint16_t *A = reinterpret_cast<uint16_t *>(w + lay.a), *B = A + batch * dd;
+  float *inv = reinterpret_cast<float *>(w + lay.inv);
+  const double Bt = (double)batch, dd_ = (double)d, ee = (double)e2;
+  hipError_t e;
+  {  // X_0 = round(M / max(||M||_F, eps)) as d x e (M^T when tall) and its transpose
+    StageScope sc(ST_MUON_NORMALISE, 0.0, s);
+    if ((e = soap::launch_muon_norm_inv(M, batch, mn, eps, reinterpret_cast<double *>(w + lay.part),
+                                        inv, s)) != hipSuccess)
+      return hip_fail(e, "normalise");
+    if ((e = soap::launch_bf16_scale_both(M, batch, d, e2, tall, inv, X, Xt, s)) != hipSuccess)
+      return hip_fail(e, "normalise (bf16)");
+  }
+  for (int64_t it = 0; it < iters; ++it) {
+    const float a = coeffs[3 * it], b = coeffs[3 * it + 1], c = coeffs[3 * it + 2];
+    StageScope sc(ST_MUON_NEWTON_SCHULZ,
+                  Bt * (dd_ * (dd_ + 1) * ee + (c != 0.f ? 2.0 * dd_ * dd_ * dd_ : 0.0) +
+                        2.0 * dd_ * dd_ * ee), s);
+    soap::BfGemmDesc g;   // A = X X^T
+    g.M = d; g.N = d; g.K = e2; g.P = X; g.ldp = e2; g.sP = mn; g.Q = X; g.ldq = e2; g.sQ = mn;
+    g.C = A; g.ldc = d; g.sC = dd; g.batch = batch; g.syrk = true;
+    if ((e = soap::launch_gemm_bf16_nt(g, s)) != hipSuccess) return hip_fail(e, "Newton-Schulz A (bf16)");
+    const uint16_t *Bop = A;
+    float alpha_b = b;
+    if (c != 0.f) {       // B = b A + c A A^T
+      soap::BfGemmDesc h;
+      h.M = d; h.N = d; h.K = d; h.P = A; h.ldp = d; h.sP = dd; h.Q = A; h.ldq = d; h.sQ = dd;
+      h.D = A; h.ldd = d; h.sD = dd; h.C = B; h.ldc = d; h.sC = dd;
+      h.alpha = c; h.beta = b; h.batch = batch; h.syrk = true;
+      if ((e = soap::launch_gemm_bf16_nt(h, s)) != hipSuccess) return hip_fail(e, "Newton-Schulz B (bf16)");
+      Bop = B;
+      alpha_b = 1.f;
+    }
+    soap::BfGemmDesc x;   // X <- a X + B X, both layouts
+    x.M = d; x.N = e2; x.K = d; x.P = Bop; x.ldp = d; x.sP = dd; x.Q = Xt; x.ldq = d; x.sQ = mn;
+    x.D = X; x.ldd = e2; x.sD = mn; x.C = Y; x.ldc = e2; x.sC = mn;
+    x.Ct = Yt; x.ldct = d; x.sCt = mn; x.alpha = alpha_b; x.beta = a; x.batch = batch;
+    if ((e = soap::launch_gemm_bf16_nt(x, s)) != hipSuccess) return hip_fail(e, "Newton-Schulz X (bf16)");
+    std::swap(X, Y);
+    std::swap(Xt, Yt);
+  }
+  {  // W <- (1 - lr wd) W - lr sqrt(max(m, n)) X_n, X_n in the m x n layout
+    StageScope sc(ST_MUON_UPDATE, 0.0, s);
+    const float scale = (float)std::sqrt((double)std::max(m, n));
+    if ((e = soap::launch_axpby_bf16(param, tall ? Xt : X, batch * mn, 1.f - lr * wd, -lr * scale,
+                                     s)) != hipSuccess)
+      return hip_fail(e, "update");
+  }
+  return ok();
+}
+
 // One Muon step (Algorithm 1) on `batch` m x n matrices.  The Newton-Schulz
 // polynomial acts on singular values only, so its Gram matrix is formed on
 // the smaller side: A = X X^T (m x m) with X <- a X + B X when m <= n, and
@@ -762,7 +827,12 @@ int muon_impl(int64_t batch, float *param, const float *grad, float *M, int64_t 
   for (int64_t i = 0; i < 3 * iters; ++i)
     if (!std::isfinite(coeffs[i]))
       return fail(SOAP_ERR_HPARAM, "coefficient %lld is not finite", (long long)i);
-  if (flags != 0) return fail(SOAP_ERR_HPARAM, "unknown flag bits 0x%x", flags);
+  if ((flags & ~(uint32_t)SOAP_MUON_BF16) != 0)
+    return fail(SOAP_ERR_HPARAM, "unknown flag bits 0x%x", flags);
+  const bool bf16 = (flags & SOAP_MUON_BF16) != 0;
+  if (bf16 && (m % 8 != 0 || n % 8 != 0))
+    return fail(SOAP_ERR_SHAPE, "SOAP_MUON_BF16 needs m and n multiples of 8 (m=%lld n=%lld)",
+                (long long)m, (long long)n);
   const MuonLayout lay = muon_layout(batch, m, n);
   if (ws_bytes < lay.total)
     return fail(SOAP_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", ws_bytes, lay.total);
@@ -788,6 +858,7 @@ int muon_impl(int64_t batch, float *param, const float *grad, float *M, int64_t 
     if ((e = soap::launch_momentum(M, grad, batch * mn, beta1, s)) != hipSuccess)
       return hip_fail(e, "momentum");
   }
+  if (bf16) return muon_ns_bf16(batch, param, M, m, n, lr, wd, eps, coeffs, iters, w, lay, s);
   {  // X_0 = M / max(||M||_F, eps)
     StageScope sc(ST_MUON_NORMALISE, 0.0, s);
     if ((e = soap::launch_muon_normalise(M, X, batch, mn, eps,

@@ -197,7 +197,8 @@ def test_muon_validation(L):
     assert call(eps=0.0) == soap.SOAP_ERR_HPARAM
     assert call(it=-1) == soap.SOAP_ERR_HPARAM
     assert call(it=2000) == soap.SOAP_ERR_HPARAM
-    assert call(flags=1) == soap.SOAP_ERR_HPARAM
+    assert call(flags=2) == soap.SOAP_ERR_HPARAM
+    assert call(flags=soap.SOAP_MUON_BF16) == soap.SOAP_ERR_SHAPE    # n = 12: not a multiple of 8
     assert call(wsb=ws - 1) == soap.SOAP_ERR_WORKSPACE
     assert call(grad=P + 16) == soap.SOAP_ERR_ALIAS
     assert call(M=M + 4) == soap.SOAP_ERR_ALIGN

@@ -100,3 +100,77 @@ def test_momentum_beta_on_old_buffer():
     M0, G = rng.standard_normal((3, 4)), rng.standard_normal((3, 4))
     _, M = oracle.muon_step(np.zeros((3, 4)), M0, G, 0.9, 0.0, 0.0, 1e-7, [])
     assert rel(M, 0.9 * M0 + 0.1 * G) <= 1e-15
+
+
+# ---- bfloat16 Newton-Schulz (the paper's precision for the iterations) ----
+
+def _bf16_by_bits(x32):
+    """Round-to-nearest-even to bfloat16 on the fp32 bit pattern: add 0x7FFF
+    plus the lowest kept bit, keep the upper 16 bits (NaN passed through)."""
+    u = np.asarray(x32, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    out = r.astype(np.uint32).view(np.float32).astype(np.float64)
+    return np.where(np.isnan(x32), np.nan, out)
+
+
+def test_round_bf16_worked_values():
+    r = oracle.round_bf16
+    assert r(1.0) == 1.0
+    assert r(1 + 2.0 ** -8) == 1.0                    # tie: to the even neighbour 1
+    assert r(1 + 3 * 2.0 ** -8) == 1 + 2.0 ** -6      # tie: up to the even mantissa
+    assert r(1 + 2.0 ** -8 + 2.0 ** -30) == 1 + 2.0 ** -7
+    assert r(1 / 3) == 0.333984375                    # 0x3EAB
+    assert r(-2.0 ** -133) == -2.0 ** -133            # smallest subnormal
+    assert r(2.0 ** -134) == 0.0                      # half the smallest subnormal: tie to 0
+    assert np.isinf(r(3.5e38)) and np.isnan(r(np.nan))
+
+
+def test_round_bf16_matches_bit_definition_and_torch():
+    import torch
+    rng = np.random.default_rng(3)
+    x = np.concatenate([
+        rng.standard_normal(20000) * 10.0 ** rng.integers(-30, 30, 20000),
+        (1 + (2 * rng.integers(0, 127, 2000) + 1) * 2.0 ** -8) * 2.0 ** rng.integers(-20, 20, 2000),
+        rng.uniform(-1, 1, 2000) * 2.0 ** -126,        # subnormal range
+        [0.0, -0.0, 2.0 ** -133, 3.0e38, -3.3e38]]).astype(np.float32)
+    ours = oracle.round_bf16(x.astype(np.float64))
+    assert np.array_equal(ours, _bf16_by_bits(x))
+    tb = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(ours, tb)
+
+
+def _ns_fp32_accumulate(M, coeffs, eps):
+    """The hardware model: products and linear combinations in fp32 on
+    bfloat16 operands, each result rounded once to bfloat16 (torch's
+    conversion)."""
+    import torch
+    bf = lambda t: t.to(torch.bfloat16).to(torch.float32)
+    Mt = torch.from_numpy(M.astype(np.float32))
+    X = bf(Mt / max(float(np.linalg.norm(M)), eps))
+    for a, b, c in coeffs:
+        A = bf(X @ X.T)
+        B = bf(b * A + c * (A @ A))
+        X = bf(a * X + B @ X)
+    return X.double().numpy()
+
+
+@pytest.mark.parametrize("m,n", [(24, 40), (40, 24), (32, 32)])
+def test_bf16_newton_schulz_matches_fp32_accumulating_model(m, n):
+    """The oracle (exact operation, one rounding) and the fp32-accumulating
+    model round differently only next to rounding boundaries; over 16 quintic
+    steps that keeps them within a few bfloat16 units in Frobenius norm."""
+    rng = np.random.default_rng(m * 100 + n)
+    M = rng.standard_normal((m, n))
+    coeffs = [QUINTIC] * 16
+    if m > n:   # the library orthogonalises the transpose of a tall matrix
+        ours = oracle.newton_schulz(M.T, coeffs, 1e-7, "bf16").T
+        model = _ns_fp32_accumulate(M.T, coeffs, 1e-7).T
+    else:
+        ours = oracle.newton_schulz(M, coeffs, 1e-7, "bf16")
+        model = _ns_fp32_accumulate(M, coeffs, 1e-7)
+    assert np.array_equal(oracle.round_bf16(ours), ours)     # every entry is a bfloat16 value
+    assert rel(ours, model) <= 8 * 2.0 ** -8
+    exact = oracle.newton_schulz(M.T if m > n else M, coeffs, 1e-7)
+    exact = exact.T if m > n else exact
+    assert rel(ours, exact) <= 0.1                           # bfloat16 noise, not a different map
+    assert rel(ours, exact) > 1e-4                           # ... and the rounding did happen
