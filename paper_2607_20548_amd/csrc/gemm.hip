@@ -42,7 +42,6 @@ struct KParams {
   int M, N, K;
   const float *A;
   int64_t lda, sA;
-  const float *A2;
   const float *B;
   int64_t ldb, sB;
   float *C;
@@ -200,8 +199,7 @@ __device__ __forceinline__ void tile_coords(const KParams &p, int t, int &tm, in
 template <int TA, int TB, int VEC, int MODE, int TAG, int MINB, bool PERSIST = false>
 __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   constexpr bool SHORTK = MINB > 1;
-  constexpr int NA = (MODE == MODE_ADAM) ? 2 : 1;
-  __shared__ __attribute__((aligned(16))) float lds[2 * (NA + 1) * TILE_FLOATS];
+  __shared__ __attribute__((aligned(16))) float lds[2 * 2 * TILE_FLOATS];
 
   // One tile per workgroup; PERSIST: a loop over tiles when the grid was
   // capped (the caller limited the compute units this product may hold).
@@ -210,7 +208,6 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   tile_coords<MODE>(p, tile, tm, tn);
   const int64_t bz = blockIdx.z;
   const float *A = p.A + bz * p.sA;
-  const float *A2 = (MODE == MODE_ADAM) ? p.A2 + bz * p.sA : nullptr;
   const float *B = p.B + bz * p.sB;
   const int m0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x;
@@ -220,95 +217,82 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
 
   // op(A) rows are x = i: k-contiguous when TA == 0.  op(B) columns are x = j:
   // k-contiguous when TB == 1.
-  SlabLoader<TA == 0, VEC> la, la2;
+  SlabLoader<TA == 0, VEC> la;
   SlabLoader<TB == 1, VEC> lb;
 
-  v16f acc[NA][2][2];
+  v16f acc[2][2];
 #pragma unroll
-  for (int a = 0; a < NA; ++a)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[a][i][j][r] = 0.f;
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  auto buf = [&](int stage, int which) { return lds + (stage * (NA + 1) + which) * TILE_FLOATS; };
+  auto buf = [&](int stage, int which) { return lds + (stage * 2 + which) * TILE_FLOATS; };
 
   const int kbeg = blockIdx.y * p.kslice;
   const int kend = min(p.K, kbeg + p.kslice);
   const int nk = (kend - kbeg + BK - 1) / BK;
   // One K slab from LDS buffer `cur` into the accumulators.
   auto compute = [&](int cur) {
-    float fb[2][8];
-    read_frag(buf(cur, NA), wn * 64 + xl, h, fb[0]);
-    read_frag(buf(cur, NA), wn * 64 + 32 + xl, h, fb[1]);
+    float fa[2][8], fb[2][8];
+    read_frag(buf(cur, 1), wn * 64 + xl, h, fb[0]);
+    read_frag(buf(cur, 1), wn * 64 + 32 + xl, h, fb[1]);
+    read_frag(buf(cur, 0), wm * 64 + xl, h, fa[0]);
+    read_frag(buf(cur, 0), wm * 64 + 32 + xl, h, fa[1]);
 #pragma unroll
-    for (int a = 0; a < NA; ++a) {
-      float fa[2][8];
-      read_frag(buf(cur, a), wm * 64 + xl, h, fa[0]);
-      read_frag(buf(cur, a), wm * 64 + 32 + xl, h, fa[1]);
+    for (int s = 0; s < 8; ++s)
 #pragma unroll
-      for (int s = 0; s < 8; ++s)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[a][i][j] =
-                __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[a][i][j], 0, 0, 0);
-    }
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
   };
 
   if constexpr (!SHORTK) {
     // Long K: global loads run two slabs ahead of the matrix cores (two
     // register sets), so a slab's loads have two slabs of MFMA work to land.
-    SlabLoader<TA == 0, VEC> lc, lc2;
+    SlabLoader<TA == 0, VEC> lc;
     SlabLoader<TB == 1, VEC> ld;
-    auto load_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TA == 0, VEC> &xa2,
-                        SlabLoader<TB == 1, VEC> &xb, int kt) {
+    auto load_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TB == 1, VEC> &xb, int kt) {
       const int k0 = kbeg + kt * BK;
       xa.load(A, p.lda, m0, k0, p.M, kend, tid);
-      if (MODE == MODE_ADAM) xa2.load(A2, p.lda, m0, k0, p.M, kend, tid);
       xb.load(B, p.ldb, n0, k0, p.N, kend, tid);
     };
-    auto store_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TA == 0, VEC> &xa2,
-                         SlabLoader<TB == 1, VEC> &xb, int stage, int kt) {
+    auto store_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TB == 1, VEC> &xb, int stage,
+                         int kt) {
       const int kvalid = min(BK, kend - (kbeg + kt * BK));
       xa.store(buf(stage, 0), tid, kvalid);
-      if (MODE == MODE_ADAM) xa2.store(buf(stage, 1), tid, kvalid);
-      xb.store(buf(stage, NA), tid, kvalid);
+      xb.store(buf(stage, 1), tid, kvalid);
     };
     // slab kt is computed from LDS while the register set `held` carries
     // slab kt+1 (stored to the other buffer after the MFMAs) and `next`
     // receives slab kt+2.
-    auto body = [&](int kt, SlabLoader<TA == 0, VEC> &ha, SlabLoader<TA == 0, VEC> &ha2,
-                    SlabLoader<TB == 1, VEC> &hb, SlabLoader<TA == 0, VEC> &na,
-                    SlabLoader<TA == 0, VEC> &na2, SlabLoader<TB == 1, VEC> &nb) {
+    auto body = [&](int kt, SlabLoader<TA == 0, VEC> &ha, SlabLoader<TB == 1, VEC> &hb,
+                    SlabLoader<TA == 0, VEC> &na, SlabLoader<TB == 1, VEC> &nb) {
       const int cur = kt & 1;
-      load_set(na, na2, nb, kt + 2);   // past the end: clamped loads, all zero
+      load_set(na, nb, kt + 2);   // past the end: clamped loads, all zero
       compute(cur);
-      if (kt + 1 < nk) store_set(ha, ha2, hb, cur ^ 1, kt + 1);
+      if (kt + 1 < nk) store_set(ha, hb, cur ^ 1, kt + 1);
       __syncthreads();
     };
     if (nk > 0) {
-      load_set(lc, lc2, ld, 0);
-      store_set(lc, lc2, ld, 0, 0);
-      load_set(la, la2, lb, 1);
+      load_set(lc, ld, 0);
+      store_set(lc, ld, 0, 0);
+      load_set(la, lb, 1);
     }
     __syncthreads();
     for (int kt = 0; kt < nk; kt += 2) {
-      body(kt, la, la2, lb, lc, lc2, ld);
-      if (kt + 1 < nk) body(kt + 1, lc, lc2, ld, la, la2, lb);
+      body(kt, la, lb, lc, ld);
+      if (kt + 1 < nk) body(kt + 1, lc, ld, la, lb);
     }
   } else {
     if (nk > 0) {
       la.load(A, p.lda, m0, kbeg, p.M, kend, tid);
-      if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, kbeg, p.M, kend, tid);
       lb.load(B, p.ldb, n0, kbeg, p.N, kend, tid);
       const int kvalid = min(BK, kend - kbeg);
       la.store(buf(0, 0), tid, kvalid);
-      if (MODE == MODE_ADAM) la2.store(buf(0, 1), tid, kvalid);
-      lb.store(buf(0, NA), tid, kvalid);
+      lb.store(buf(0, 1), tid, kvalid);
     }
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
@@ -317,15 +301,13 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
       if (more) {
         const int k0 = kbeg + (kt + 1) * BK;
         la.load(A, p.lda, m0, k0, p.M, kend, tid);
-        if (MODE == MODE_ADAM) la2.load(A2, p.lda, m0, k0, p.M, kend, tid);
         lb.load(B, p.ldb, n0, k0, p.N, kend, tid);
       }
       compute(cur);
       if (more) {
         const int kvalid = min(BK, kend - (kbeg + (kt + 1) * BK));
         la.store(buf(cur ^ 1, 0), tid, kvalid);
-        if (MODE == MODE_ADAM) la2.store(buf(cur ^ 1, 1), tid, kvalid);
-        lb.store(buf(cur ^ 1, NA), tid, kvalid);
+        lb.store(buf(cur ^ 1, 1), tid, kvalid);
       }
       __syncthreads();
     }
@@ -363,9 +345,9 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
           if (row >= p.M || col >= p.N) continue;
           const int64_t off = (int64_t)row * p.ldc + col;
           if (P) {
-            P[(int64_t)row * p.N + col] = acc[0][i][j][r];
+            P[(int64_t)row * p.N + col] = acc[i][j][r];
           } else {
-            float v = p.alpha * acc[0][i][j][r];
+            float v = p.alpha * acc[i][j][r];
             if (p.beta != 0.f) v += p.beta * cv[r];
             C[off] = v;
           }
@@ -383,22 +365,25 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
           if (row >= p.M || col >= p.N) continue;
           const int64_t off = (int64_t)row * p.ldc + col;
           if (MODE == MODE_GENERAL && P) {
-            P[(int64_t)row * p.N + col] = acc[0][i][j][r];
+            P[(int64_t)row * p.N + col] = acc[i][j][r];
           } else if (MODE == MODE_GENERAL) {
-            float v = p.alpha * acc[0][i][j][r];
+            float v = p.alpha * acc[i][j][r];
             if (p.beta != 0.f) v += p.beta * C[off];
             C[off] = v;
           } else if (MODE == MODE_SYRK) {
             if (row < col) continue;  // the mirror of (col,row) is written by its owner
-            const float v = (p.beta != 0.f ? p.beta * C[off] : 0.f) + p.alpha * acc[0][i][j][r];
+            const float v = (p.beta != 0.f ? p.beta * C[off] : 0.f) + p.alpha * acc[i][j][r];
             C[off] = v;
             if (row != col) C[(int64_t)col * p.ldc + row] = v;
-          } else {
-            const float g = acc[0][i][j][r];
-            const float mm = acc[1][i][j][r];
-            const float v = p.b2 * V[off] + (1.f - p.b2) * g * g;
-            V[off] = v;
-            Nout[off] = (mm / p.c1) / (sqrtf(v / p.c2) + p.eps);
+          } else if ((r & 1) == 0) {
+            // rows 2i, 2i+1 of the interleaved operand are G' and M' of
+            // output row i; they sit in registers r, r+1 of the same lane
+            const float g = acc[i][j][r];
+            const float mm = acc[i][j][r + 1];
+            const int64_t o = (int64_t)(row >> 1) * p.ldc + col;
+            const float v = p.b2 * V[o] + (1.f - p.b2) * g * g;
+            V[o] = v;
+            Nout[o] = (mm / p.c1) / (sqrtf(v / p.c2) + p.eps);
           }
         }
       }
@@ -526,7 +511,6 @@ KParams make_params(const GemmDesc &d) {
   KParams kp{};
   kp.M = (int)d.M; kp.N = (int)d.N; kp.K = (int)d.K;
   kp.A = d.A; kp.lda = d.lda; kp.sA = d.sA;
-  kp.A2 = nullptr;
   kp.B = d.B; kp.ldb = d.ldb; kp.sB = d.sB;
   kp.C = d.C; kp.ldc = d.ldc; kp.sC = d.sC;
   kp.alpha = d.alpha; kp.beta = d.beta;
@@ -549,12 +533,12 @@ KParams make_params(const GemmDesc &d) {
 // leading dimension and batch stride, 8-byte aligned base).
 bool aligned8(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
-bool vec_ok_for(const GemmDesc &d, const float *A2) {
+bool vec_ok_for(const GemmDesc &d) {
   bool ok = true;
   if (d.trans_a == 0)
-    ok = ok && d.K % 4 == 0 && d.lda % 4 == 0 && d.sA % 4 == 0 && aligned16(d.A) && (!A2 || aligned16(A2));
+    ok = ok && d.K % 4 == 0 && d.lda % 4 == 0 && d.sA % 4 == 0 && aligned16(d.A);
   else
-    ok = ok && d.M % 2 == 0 && d.lda % 2 == 0 && d.sA % 2 == 0 && aligned8(d.A) && (!A2 || aligned8(A2));
+    ok = ok && d.M % 2 == 0 && d.lda % 2 == 0 && d.sA % 2 == 0 && aligned8(d.A);
   if (d.trans_b == 1)
     ok = ok && d.K % 4 == 0 && d.ldb % 4 == 0 && d.sB % 4 == 0 && aligned16(d.B);
   else
@@ -577,24 +561,24 @@ int choose_splitk(int64_t M, int64_t N, int64_t K, int64_t batch, int max_split)
 hipError_t launch_gemm(const GemmDesc &d, hipStream_t s) {
   if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
   KParams kp = make_params(d);
-  return dispatch<MODE_GENERAL>(d, kp, s, vec_ok_for(d, nullptr));
+  return dispatch<MODE_GENERAL>(d, kp, s, vec_ok_for(d));
 }
 
 hipError_t launch_syrk_ema(const GemmDesc &d, hipStream_t s) {
   if (d.M <= 0 || d.batch <= 0) return hipSuccess;
   KParams kp = make_params(d);
   kp.ntiles = kp.tiles_m * (kp.tiles_m + 1) / 2;
-  return dispatch<MODE_SYRK>(d, kp, s, vec_ok_for(d, nullptr));
+  return dispatch<MODE_SYRK>(d, kp, s, vec_ok_for(d));
 }
 
 hipError_t launch_gemm_adam(const GemmDesc &d, const AdamEpi &e, hipStream_t s) {
   if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
+  if (d.M % 2 != 0 || d.trans_a != 0) return hipErrorInvalidValue;
   KParams kp = make_params(d);
-  kp.A2 = e.A2;
   kp.V = e.V;
   kp.Nout = e.Nout;
   kp.b2 = e.b2; kp.c1 = e.c1; kp.c2 = e.c2; kp.eps = e.eps;
-  return dispatch<MODE_ADAM>(d, kp, s, vec_ok_for(d, e.A2));
+  return dispatch<MODE_ADAM>(d, kp, s, vec_ok_for(d));
 }
 
 }  // namespace soap

@@ -53,13 +53,14 @@ hipError_t launch_gemm(const GemmDesc &d, hipStream_t s);
 // lower triangle.  max_wg caps it like a GEMM for the layouts (0, 1) and (1, 0).
 hipError_t launch_syrk_ema(const GemmDesc &d, hipStream_t s);
 
-// Fused second rotation + Adam in the eigenbasis.  With op(A) = T_G and
-// op(A2) = T_M (same layout/strides), op(B) = Q_R:
-//   G' = T_G Q_R,  M' = T_M Q_R,  V <- b2 V + (1-b2) G'^2,
-//   Nout = (M'/c1) / (sqrt(V/c2) + eps).
-// V and Nout use the leading dimension / stride of C in the descriptor.
+// Fused second rotation + Adam in the eigenbasis.  op(A) (trans_a = 0,
+// d.M = 2 m rows) holds T_G and T_M interleaved by rows: row 2i is row i of
+// T_G, row 2i+1 row i of T_M.  With op(B) = Q_R one product gives
+//   G' = T_G Q_R,  M' = T_M Q_R  (rows 2i, 2i+1 of the result), and the
+// epilogue does  V <- b2 V + (1-b2) G'^2,  Nout = (M'/c1) / (sqrt(V/c2) + eps)
+// on the m x n outputs, which use the leading dimension and batch stride of
+// C in the descriptor.  d.M odd or trans_a != 0: hipErrorInvalidValue.
 struct AdamEpi {
-  const float *A2 = nullptr;
   float *V = nullptr;
   float *Nout = nullptr;
   float b2 = 0.f, c1 = 1.f, c2 = 1.f, eps = 0.f;

@@ -178,8 +178,8 @@ StepLayout step_layout(int64_t batch, int64_t m, int64_t n, bool kl) {
   size_t o = 0;
   L.al = o; o = align256(o + f * batch * m * m);
   L.ar = o; o = align256(o + f * batch * n * n);
-  L.tg = o; o = align256(o + f * batch * m * n);
-  L.tm = o; o = align256(o + f * batch * m * n);
+  L.tg = o; o = align256(o + f * batch * m * n);   // T_G, T_M: adjacent, so that the
+  L.tm = o; o = align256(o + f * batch * m * n);   // row-interleaved pair fits over both
   L.nb = o; o = align256(o + f * batch * m * n);
   if (kl) {
     L.kz = o; o = align256(o + f * batch * m * n);
@@ -668,9 +668,11 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     soap::GemmDesc d;
     d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
     d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
-    d.C = TG; d.ldc = n; d.sC = mn; d.batch = batch; d.max_wg = kSideWorkgroups;
+    // T_G and T_M interleaved by rows over the T_G and T_M buffers (adjacent,
+    // 2 m n floats per matrix): row 2i = T_G row i, row 2i+1 = T_M row i.
+    d.C = TG; d.ldc = 2 * n; d.sC = 2 * mn; d.batch = batch; d.max_wg = kSideWorkgroups;
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in G");
-    d.B = M; d.C = TM;
+    d.B = M; d.C = TG + n;
     if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
   }
   if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
@@ -681,13 +683,13 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
       return hip_fail(e, "QR R");
   }
   if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
-  {  // G' = T_G Q_R, M' = T_M Q_R, then Adam in the eigenbasis
+  {  // G' = T_G Q_R, M' = T_M Q_R (one product over the interleaved rows), then Adam
     StageScope sc(ST_ROT_IN_R_ADAM, B * 4.0 * md * nd * nd, s);
     soap::GemmDesc d;
-    d.M = m; d.N = n; d.K = n; d.A = TG; d.lda = n; d.sA = mn; d.B = QR; d.ldb = n; d.sB = nn;
-    d.C = nullptr; d.ldc = n; d.sC = mn; d.batch = batch;
+    d.M = 2 * m; d.N = n; d.K = n; d.A = TG; d.lda = n; d.sA = 2 * mn; d.B = QR; d.ldb = n;
+    d.sB = nn; d.C = nullptr; d.ldc = n; d.sC = mn; d.batch = batch;
     soap::AdamEpi ae;
-    ae.A2 = TM; ae.V = V; ae.Nout = NN; ae.b2 = beta2; ae.c1 = c1; ae.c2 = c2; ae.eps = eps;
+    ae.V = V; ae.Nout = NN; ae.b2 = beta2; ae.c1 = c1; ae.c2 = c2; ae.eps = eps;
     if ((e = soap::launch_gemm_adam(d, ae, s)) != hipSuccess) return hip_fail(e, "rotate in + Adam");
   }
   {  // T2 = Q_L N (into T_G, which is dead now)
