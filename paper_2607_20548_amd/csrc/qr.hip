@@ -934,14 +934,15 @@ __global__ __launch_bounds__(256) void qr_zero_above_blocks_kernel(float *At, in
 //   [[T_a, T_ab], [0, T_b]]; T_ab was written in place by the caller.
 __global__ __launch_bounds__(256) void qr_assemble_pair_t_kernel(float *TP, int64_t sTP,
                                                                  const float *Ta, const float *Tb,
-                                                                 int64_t sT) {
+                                                                 int64_t sT, int w, int ldab) {
+  // TP is 2w x 2w (row-major); Ta, Tb are w x w with leading dimension ldab.
   float *P = TP + (int64_t)blockIdx.y * sTP;
   const float *A = Ta + (int64_t)blockIdx.y * sT, *B = Tb + (int64_t)blockIdx.y * sT;
-  for (int e = blockIdx.x * 256 + threadIdx.x; e < 4 * NB * NB; e += gridDim.x * 256) {
-    const int r = e / (2 * NB), c = e % (2 * NB);
-    if (r < NB && c < NB) P[e] = A[r * NB + c];
-    else if (r >= NB && c < NB) P[e] = 0.f;
-    else if (r >= NB) P[e] = B[(r - NB) * NB + (c - NB)];
+  for (int e = blockIdx.x * 256 + threadIdx.x; e < 4 * w * w; e += gridDim.x * 256) {
+    const int r = e / (2 * w), c = e % (2 * w);
+    if (r < w && c < w) P[e] = A[r * ldab + c];
+    else if (r >= w && c < w) P[e] = 0.f;
+    else if (r >= w) P[e] = B[(r - w) * ldab + (c - w)];
   }
 }
 
@@ -979,10 +980,11 @@ struct QrLayout {
   int64_t n, nob;
   bool block;          // outer blocks factored by qr_block_kernel (else the panel path)
   size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, x_off, total;
-  size_t tp_off, sx_off, skp_off;
+  size_t tp_off, sx_off, skp_off, tq_off, sq_off;
   int64_t sT, sWbuf, sSk, sPart, sWi;
-  int64_t np;          // pairs of full outer blocks (Q is formed by pairs)
-  int64_t sTP, sSx, sSkp;
+  int64_t np;          // pairs of full outer blocks
+  int64_t nq;          // quads (pairs of full pairs): Q is formed by quads
+  int64_t sTP, sSx, sSkp, sTQ, sSq;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -996,11 +998,14 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   const int64_t P = (n + RCH - 1) / RCH;
   L.sT = L.nob * NB * NB;
   L.np = (n / NB) / 2;
-  L.sWbuf = (int64_t)2 * NB * n;
+  L.nq = L.np / 2;
+  L.sWbuf = (int64_t)4 * NB * n;
   L.sSk = (int64_t)MAX_SPLIT * 2 * NB * n;
   L.sTP = L.np * 4 * NB * NB;
   L.sSx = L.np * 2 * NB * NB;
   L.sSkp = (int64_t)64 * NB * NB;
+  L.sTQ = L.nq * 16 * NB * NB;
+  L.sSq = L.nq * 8 * NB * NB;
   L.sPart = P * PART_STRIDE;
   L.sWi = (int64_t)MAX_B * NB;
   size_t o = 0;
@@ -1016,6 +1021,8 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.tp_off = o;   o = align256(o + sizeof(float) * batch * L.sTP);
   L.sx_off = o;   o = align256(o + sizeof(float) * batch * L.sSx);
   L.skp_off = o;  o = align256(o + sizeof(float) * batch * L.sSkp);
+  L.tq_off = o;   o = align256(o + sizeof(float) * batch * L.sTQ);
+  L.sq_off = o;   o = align256(o + sizeof(float) * batch * L.sSq);
   // The resident-block path needs every workgroup of a launch resident at
   // once: at most BK_MAX_WG workgroups (two such launches, one per factor,
   // may run together on the 256 compute units).
@@ -1090,7 +1097,7 @@ struct QrCtx {
   float *Tb, *Wb, *W2, *Sk, *Pt, *Wi, *dsign, *betas;
   unsigned *cnt;
   unsigned long long *xch;
-  float *TP, *Sx, *Skp;
+  float *TP, *Sx, *Skp, *TQ, *Sq;
 };
 
 hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
@@ -1221,7 +1228,48 @@ hipError_t pair_t(const QrCtx &x, int64_t p, hipStream_t st) {
   gt.C = TP + NB; gt.ldc = 2 * NB; gt.sC = x.L.sTP; gt.alpha = -1.f; gt.batch = x.batch;
   SOAP_TRY(launch_gemm(gt, st));
   hipLaunchKernelGGL(qr_assemble_pair_t_kernel, dim3(64, (unsigned)x.batch), dim3(256), 0, st, TP,
-                     x.L.sTP, Ta, Tbk, x.L.sT);
+                     x.L.sTP, Ta, Tbk, x.L.sT, NB, NB);
+  return hipGetLastError();
+}
+
+// T of quad q (full pairs a = 2q, b = 2q+1), on stream st, from the pair
+// T's: S = Y_a^T Y_b, X = T_a S, T_ab = -X T_b, then the diagonal blocks.
+// Y_b's second block still holds R entries above its diagonal block (the
+// factorization is running), so S is formed block by block of Y_b, each over
+// the rows where that block's reflectors live: S[:, 0:NB] over rows >= c_b1,
+// S[:, NB:2NB] over rows >= c_b2.  Reads only At rows of the quad at columns
+// >= c_b1, which the concurrent trailing update does not touch.
+hipError_t quad_t(const QrCtx &x, int64_t q, hipStream_t st) {
+  const int64_t n = x.n, ca = 4 * q * NB, cb1 = ca + 2 * NB, cb2 = cb1 + NB;
+  const int64_t W = 2 * NB;
+  float *S = x.Sq + q * 2 * W * W, *X = S + W * W;
+  const float *Ta = x.TP + (2 * q) * 4 * NB * NB, *Tbq = Ta + 4 * NB * NB;
+  float *TQ = x.TQ + q * 4 * W * W;
+  for (int half = 0; half < 2; ++half) {   // S[:, half NB : (half+1) NB]
+    const int64_t cr = half ? cb2 : cb1;
+    GemmDesc gs;  // S[i][j] = sum_r At[ca+i][r] At[cr+j][r], r in [cr, n)
+    gs.trans_a = 0; gs.trans_b = 1; gs.M = W; gs.N = NB; gs.K = n - cr;
+    gs.A = x.At + ca * n + cr; gs.lda = n; gs.sA = x.sA;
+    gs.B = x.At + cr * n + cr; gs.ldb = n; gs.sB = x.sA;
+    gs.C = S + half * NB; gs.ldc = W; gs.sC = x.L.sSq; gs.batch = x.batch;
+    gs.splitk = narrow_split(W, NB, n - cr, x.batch, x.batch * x.L.sSkp);
+    gs.part = x.Skp;
+    SOAP_TRY(launch_gemm(gs, st));
+  }
+  GemmDesc gx;  // X = T_a S
+  gx.M = W; gx.N = W; gx.K = W;
+  gx.A = Ta; gx.lda = W; gx.sA = x.L.sTP;
+  gx.B = S; gx.ldb = W; gx.sB = x.L.sSq;
+  gx.C = X; gx.ldc = W; gx.sC = x.L.sSq; gx.batch = x.batch;
+  SOAP_TRY(launch_gemm(gx, st));
+  GemmDesc gt;  // T_ab = -X T_b
+  gt.M = W; gt.N = W; gt.K = W;
+  gt.A = X; gt.lda = W; gt.sA = x.L.sSq;
+  gt.B = Tbq; gt.ldb = W; gt.sB = x.L.sTP;
+  gt.C = TQ + W; gt.ldc = 2 * W; gt.sC = x.L.sTQ; gt.alpha = -1.f; gt.batch = x.batch;
+  SOAP_TRY(launch_gemm(gt, st));
+  hipLaunchKernelGGL(qr_assemble_pair_t_kernel, dim3(64, (unsigned)x.batch), dim3(256), 0, st, TQ,
+                     x.L.sTQ, Ta, Tbq, x.L.sTP, (int)W, (int)W);
   return hipGetLastError();
 }
 
@@ -1236,7 +1284,8 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
   g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
   g1.B = x.Q + c * n + c; g1.ldb = n; g1.sB = x.sA;
   g1.C = x.Wb; g1.ldc = Kr; g1.sC = x.L.sWbuf; g1.batch = x.batch;
-  g1.splitk = choose_splitk(w, Kr, Kr, x.batch, MAX_SPLIT);
+  // the partial buffer holds MAX_SPLIT slices of 2 NB x n
+  g1.splitk = choose_splitk(w, Kr, Kr, x.batch, (int)(MAX_SPLIT * 2 * NB / std::max<int64_t>(w, 2 * NB)));
   g1.part = x.Sk;
   SOAP_TRY(launch_gemm(g1, s));
   GemmDesc g2;  // W2 = T W
@@ -1277,6 +1326,8 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   x.TP = reinterpret_cast<float *>(base + x.L.tp_off);
   x.Sx = reinterpret_cast<float *>(base + x.L.sx_off);
   x.Skp = reinterpret_cast<float *>(base + x.L.skp_off);
+  x.TQ = reinterpret_cast<float *>(base + x.L.tq_off);
+  x.Sq = reinterpret_cast<float *>(base + x.L.sq_off);
   const int64_t nob = x.L.nob, np = x.L.np;
 
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
@@ -1308,7 +1359,9 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     SOAP_TRY(hipEventRecord(ev_panel, sp));
     if ((ob + 1) % 2 == 1 && (ob + 1) / 2 < np) {               // pair (ob, ob+1) complete
       SOAP_TRY(hipStreamWaitEvent(st, ev_panel, 0));
-      SOAP_TRY(pair_t(x, (ob + 1) / 2, st));
+      const int64_t p = (ob + 1) / 2;
+      SOAP_TRY(pair_t(x, p, st));
+      if (p % 2 == 1 && p / 2 < x.L.nq) SOAP_TRY(quad_t(x, p / 2, st));   // quad (p-1, p)
     }
     SOAP_TRY(trailing_update(x, ob, cend2, n, s));              // far: the rest
     SOAP_TRY(hipStreamWaitEvent(s, ev_panel, 0));               // block ob+1 factored
@@ -1340,14 +1393,19 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
                        x.ni, x.sA);
     SOAP_TRY(hipGetLastError());
   }
-  // Blocks past the last full pair one by one (backwards), then the pairs as
-  // rank-2NB updates.
+  // Backwards: the blocks past the last full pair one by one, the pairs
+  // past the last full quad as rank-2NB updates, then the quads as rank-4NB
+  // updates (longer K per product: the rank-512 update runs nearer the
+  // matrix cores' rate than the rank-256 one).
+  const int64_t nq = x.L.nq;
   for (int64_t ob = nob - 1; ob >= 2 * np; --ob) {
     const int64_t c = ob * NB;
     SOAP_TRY(q_update(x, c, std::min<int64_t>(n, c + NB) - c, x.Tb + ob * NB * NB, NB, x.L.sT, s));
   }
-  for (int64_t p = np - 1; p >= 0; --p)
+  for (int64_t p = np - 1; p >= 2 * nq; --p)
     SOAP_TRY(q_update(x, 2 * p * NB, 2 * NB, x.TP + p * 4 * NB * NB, 2 * NB, x.L.sTP, s));
+  for (int64_t q = nq - 1; q >= 0; --q)
+    SOAP_TRY(q_update(x, 4 * q * NB, 4 * NB, x.TQ + q * 16 * NB * NB, 4 * NB, x.L.sTQ, s));
   return hipSuccess;
 }
 
