@@ -980,16 +980,21 @@ struct QrLayout {
   int64_t n, nob;
   bool block;          // outer blocks factored by qr_block_kernel (else the panel path)
   size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, x_off, total;
-  size_t tp_off, sx_off, skp_off, tq_off, sq_off;
+  size_t tp_off, sx_off, skp_off, tq_off, sq_off, to_off, so_off;
   int64_t sT, sWbuf, sSk, sPart, sWi;
   int64_t np;          // pairs of full outer blocks
-  int64_t nq;          // quads (pairs of full pairs): Q is formed by quads
-  int64_t sTP, sSx, sSkp, sTQ, sSq;
+  int64_t nq;          // quads (pairs of full pairs)
+  int64_t no;          // octs (pairs of full quads), for n >= OCT_MIN_N
+  int64_t sTP, sSx, sSkp, sTQ, sSq, sTO, sSo;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 constexpr int MAX_SPLIT = 8;
+// From this size on, Q is formed by rank-1024 updates (octs of blocks): the
+// longer K brings the update near the long-K products' rate, which outweighs
+// the coarser trapezoid (1.5 w / n more flops than the block-level count).
+constexpr int64_t OCT_MIN_N = 8192;
 
 QrLayout qr_layout(int64_t batch, int64_t n) {
   QrLayout L{};
@@ -999,13 +1004,16 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.sT = L.nob * NB * NB;
   L.np = (n / NB) / 2;
   L.nq = L.np / 2;
-  L.sWbuf = (int64_t)4 * NB * n;
+  L.no = (n >= OCT_MIN_N) ? L.nq / 2 : 0;
+  L.sWbuf = (int64_t)(L.no > 0 ? 8 : 4) * NB * n;
   L.sSk = (int64_t)MAX_SPLIT * 2 * NB * n;
   L.sTP = L.np * 4 * NB * NB;
   L.sSx = L.np * 2 * NB * NB;
   L.sSkp = (int64_t)64 * NB * NB;
   L.sTQ = L.nq * 16 * NB * NB;
   L.sSq = L.nq * 8 * NB * NB;
+  L.sTO = L.no * 64 * NB * NB;
+  L.sSo = L.no * 32 * NB * NB;
   L.sPart = P * PART_STRIDE;
   L.sWi = (int64_t)MAX_B * NB;
   size_t o = 0;
@@ -1023,6 +1031,8 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.skp_off = o;  o = align256(o + sizeof(float) * batch * L.sSkp);
   L.tq_off = o;   o = align256(o + sizeof(float) * batch * L.sTQ);
   L.sq_off = o;   o = align256(o + sizeof(float) * batch * L.sSq);
+  L.to_off = o;   o = align256(o + sizeof(float) * batch * L.sTO);
+  L.so_off = o;   o = align256(o + sizeof(float) * batch * L.sSo);
   // The resident-block path needs every workgroup of a launch resident at
   // once: at most BK_MAX_WG workgroups (two such launches, one per factor,
   // may run together on the 256 compute units).
@@ -1097,7 +1107,7 @@ struct QrCtx {
   float *Tb, *Wb, *W2, *Sk, *Pt, *Wi, *dsign, *betas;
   unsigned *cnt;
   unsigned long long *xch;
-  float *TP, *Sx, *Skp, *TQ, *Sq;
+  float *TP, *Sx, *Skp, *TQ, *Sq, *TO, *So;
 };
 
 hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
@@ -1232,44 +1242,50 @@ hipError_t pair_t(const QrCtx &x, int64_t p, hipStream_t st) {
   return hipGetLastError();
 }
 
-// T of quad q (full pairs a = 2q, b = 2q+1), on stream st, from the pair
-// T's: S = Y_a^T Y_b, X = T_a S, T_ab = -X T_b, then the diagonal blocks.
-// Y_b's second block still holds R entries above its diagonal block (the
+// T of group g at level lv (lv = 2: quads, pairs of full pairs; lv = 3:
+// octs, pairs of full quads), on stream st, from the T's of its halves a, b
+// (level lv - 1, hw = NB 2^(lv-1) reflectors each): S = Y_a^T Y_b,
+// X = T_a S, T_ab = -X T_b, then the diagonal blocks.  The blocks of Y_b
+// after its first still hold R entries above their diagonal blocks (the
 // factorization is running), so S is formed block by block of Y_b, each over
-// the rows where that block's reflectors live: S[:, 0:NB] over rows >= c_b1,
-// S[:, NB:2NB] over rows >= c_b2.  Reads only At rows of the quad at columns
-// >= c_b1, which the concurrent trailing update does not touch.
-hipError_t quad_t(const QrCtx &x, int64_t q, hipStream_t st) {
-  const int64_t n = x.n, ca = 4 * q * NB, cb1 = ca + 2 * NB, cb2 = cb1 + NB;
-  const int64_t W = 2 * NB;
-  float *S = x.Sq + q * 2 * W * W, *X = S + W * W;
-  const float *Ta = x.TP + (2 * q) * 4 * NB * NB, *Tbq = Ta + 4 * NB * NB;
-  float *TQ = x.TQ + q * 4 * W * W;
-  for (int half = 0; half < 2; ++half) {   // S[:, half NB : (half+1) NB]
-    const int64_t cr = half ? cb2 : cb1;
-    GemmDesc gs;  // S[i][j] = sum_r At[ca+i][r] At[cr+j][r], r in [cr, n)
-    gs.trans_a = 0; gs.trans_b = 1; gs.M = W; gs.N = NB; gs.K = n - cr;
+// the rows where that block's reflectors live.  Reads only At rows of the
+// group at columns >= c_b, which the concurrent trailing update does not
+// touch.
+hipError_t merge_t(const QrCtx &x, int lv, int64_t g, hipStream_t st) {
+  const int64_t n = x.n, hw = (int64_t)NB << (lv - 1), W = 2 * hw;
+  const int64_t ca = g * W, cb = ca + hw;
+  float *Tlo = lv == 2 ? x.TP : x.TQ, *Thi = lv == 2 ? x.TQ : x.TO;
+  float *Sg = lv == 2 ? x.Sq : x.So;
+  const int64_t sLo = lv == 2 ? x.L.sTP : x.L.sTQ, sHi = lv == 2 ? x.L.sTQ : x.L.sTO;
+  const int64_t sS = lv == 2 ? x.L.sSq : x.L.sSo;
+  float *S = Sg + g * 2 * hw * hw, *X = S + hw * hw;
+  const float *Ta = Tlo + (2 * g) * hw * hw, *Tbg = Ta + hw * hw;
+  float *TG = Thi + g * W * W;
+  for (int64_t j = 0; j < hw / NB; ++j) {   // S[:, j NB : (j+1) NB]
+    const int64_t cr = cb + j * NB;
+    GemmDesc gs;  // S[i][jj] = sum_r At[ca+i][r] At[cr+jj][r], r in [cr, n)
+    gs.trans_a = 0; gs.trans_b = 1; gs.M = hw; gs.N = NB; gs.K = n - cr;
     gs.A = x.At + ca * n + cr; gs.lda = n; gs.sA = x.sA;
     gs.B = x.At + cr * n + cr; gs.ldb = n; gs.sB = x.sA;
-    gs.C = S + half * NB; gs.ldc = W; gs.sC = x.L.sSq; gs.batch = x.batch;
-    gs.splitk = narrow_split(W, NB, n - cr, x.batch, x.batch * x.L.sSkp);
+    gs.C = S + j * NB; gs.ldc = hw; gs.sC = sS; gs.batch = x.batch;
+    gs.splitk = narrow_split(hw, NB, n - cr, x.batch, x.batch * x.L.sSkp);
     gs.part = x.Skp;
     SOAP_TRY(launch_gemm(gs, st));
   }
   GemmDesc gx;  // X = T_a S
-  gx.M = W; gx.N = W; gx.K = W;
-  gx.A = Ta; gx.lda = W; gx.sA = x.L.sTP;
-  gx.B = S; gx.ldb = W; gx.sB = x.L.sSq;
-  gx.C = X; gx.ldc = W; gx.sC = x.L.sSq; gx.batch = x.batch;
+  gx.M = hw; gx.N = hw; gx.K = hw;
+  gx.A = Ta; gx.lda = hw; gx.sA = sLo;
+  gx.B = S; gx.ldb = hw; gx.sB = sS;
+  gx.C = X; gx.ldc = hw; gx.sC = sS; gx.batch = x.batch;
   SOAP_TRY(launch_gemm(gx, st));
   GemmDesc gt;  // T_ab = -X T_b
-  gt.M = W; gt.N = W; gt.K = W;
-  gt.A = X; gt.lda = W; gt.sA = x.L.sSq;
-  gt.B = Tbq; gt.ldb = W; gt.sB = x.L.sTP;
-  gt.C = TQ + W; gt.ldc = 2 * W; gt.sC = x.L.sTQ; gt.alpha = -1.f; gt.batch = x.batch;
+  gt.M = hw; gt.N = hw; gt.K = hw;
+  gt.A = X; gt.lda = hw; gt.sA = sS;
+  gt.B = Tbg; gt.ldb = hw; gt.sB = sLo;
+  gt.C = TG + hw; gt.ldc = W; gt.sC = sHi; gt.alpha = -1.f; gt.batch = x.batch;
   SOAP_TRY(launch_gemm(gt, st));
-  hipLaunchKernelGGL(qr_assemble_pair_t_kernel, dim3(64, (unsigned)x.batch), dim3(256), 0, st, TQ,
-                     x.L.sTQ, Ta, Tbq, x.L.sTP, (int)W, (int)W);
+  hipLaunchKernelGGL(qr_assemble_pair_t_kernel, dim3(64, (unsigned)x.batch), dim3(256), 0, st, TG,
+                     sHi, Ta, Tbg, sLo, (int)hw, (int)hw);
   return hipGetLastError();
 }
 
@@ -1328,6 +1344,8 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   x.Skp = reinterpret_cast<float *>(base + x.L.skp_off);
   x.TQ = reinterpret_cast<float *>(base + x.L.tq_off);
   x.Sq = reinterpret_cast<float *>(base + x.L.sq_off);
+  x.TO = reinterpret_cast<float *>(base + x.L.to_off);
+  x.So = reinterpret_cast<float *>(base + x.L.so_off);
   const int64_t nob = x.L.nob, np = x.L.np;
 
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
@@ -1361,7 +1379,11 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
       SOAP_TRY(hipStreamWaitEvent(st, ev_panel, 0));
       const int64_t p = (ob + 1) / 2;
       SOAP_TRY(pair_t(x, p, st));
-      if (p % 2 == 1 && p / 2 < x.L.nq) SOAP_TRY(quad_t(x, p / 2, st));   // quad (p-1, p)
+      if (p % 2 == 1 && p / 2 < x.L.nq) {                  // quad (p-1, p) complete
+        const int64_t q = p / 2;
+        SOAP_TRY(merge_t(x, 2, q, st));
+        if (q % 2 == 1 && q / 2 < x.L.no) SOAP_TRY(merge_t(x, 3, q / 2, st));   // oct (q-1, q)
+      }
     }
     SOAP_TRY(trailing_update(x, ob, cend2, n, s));              // far: the rest
     SOAP_TRY(hipStreamWaitEvent(s, ev_panel, 0));               // block ob+1 factored
@@ -1393,19 +1415,21 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
                        x.ni, x.sA);
     SOAP_TRY(hipGetLastError());
   }
-  // Backwards: the blocks past the last full pair one by one, the pairs
-  // past the last full quad as rank-2NB updates, then the quads as rank-4NB
-  // updates (longer K per product: the rank-512 update runs nearer the
-  // matrix cores' rate than the rank-256 one).
-  const int64_t nq = x.L.nq;
+  // Backwards: the blocks past the last full pair one by one, then the
+  // pairs, quads and octs past the last full group of the next size as
+  // rank-2NB, 4NB and 8NB updates (longer K per product: the update runs
+  // nearer the matrix cores' rate than with rank 256).
+  const int64_t nq = x.L.nq, no = x.L.no;
   for (int64_t ob = nob - 1; ob >= 2 * np; --ob) {
     const int64_t c = ob * NB;
     SOAP_TRY(q_update(x, c, std::min<int64_t>(n, c + NB) - c, x.Tb + ob * NB * NB, NB, x.L.sT, s));
   }
   for (int64_t p = np - 1; p >= 2 * nq; --p)
     SOAP_TRY(q_update(x, 2 * p * NB, 2 * NB, x.TP + p * 4 * NB * NB, 2 * NB, x.L.sTP, s));
-  for (int64_t q = nq - 1; q >= 0; --q)
+  for (int64_t q = nq - 1; q >= 2 * no; --q)
     SOAP_TRY(q_update(x, 4 * q * NB, 4 * NB, x.TQ + q * 16 * NB * NB, 4 * NB, x.L.sTQ, s));
+  for (int64_t o8 = no - 1; o8 >= 0; --o8)
+    SOAP_TRY(q_update(x, 8 * o8 * NB, 8 * NB, x.TO + o8 * 64 * NB * NB, 8 * NB, x.L.sTO, s));
   return hipSuccess;
 }
 

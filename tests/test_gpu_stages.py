@@ -143,6 +143,32 @@ def test_qr_q_only_matches_oracle(n):
     assert np.linalg.norm(Q.T @ Q - np.eye(n)) / np.sqrt(n) <= 1e-5
 
 
+def test_qr_large_residuals_rank1024_q_formation():
+    """n = 8576 = 67 blocks: Q formed by rank-1024 updates (8 octs) plus a
+    leftover pair and block; residuals computed in fp64 on the GPU."""
+    import paper_2607_20548_amd as soap
+    import torch
+    n = 8576
+    g = torch.Generator(device="cuda").manual_seed(21)
+    A = (torch.eye(n, device="cuda") + 0.1 * torch.randn((n, n), device="cuda", generator=g) / n ** 0.5)
+    Q = torch.empty((n, n), device="cuda")
+    R = torch.empty((n, n), device="cuda")
+    wsb = soap.soap_qr_workspace_bytes(n)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    soap.soap_qr_f32(n, A, Q, R, ws, wsb)
+    Q2 = torch.empty_like(Q)
+    soap.soap_qr_f32(n, A, Q2, None, ws, wsb)
+    torch.cuda.synchronize()
+    assert torch.equal(Q, Q2)
+    Qd, Rd, Ad = Q.double(), R.double(), A.double()
+    orth = (torch.linalg.norm(Qd.T @ Qd - torch.eye(n, device="cuda", dtype=torch.float64)) / n ** 0.5).item()
+    rec = (torch.linalg.norm(Qd @ Rd - Ad) / torch.linalg.norm(Ad)).item()
+    log(f"qr n={n}: orth {orth:.2e} rec {rec:.2e}")
+    assert orth <= 1e-5 and rec <= 1e-5
+    assert torch.equal(torch.tril(R, -1), torch.zeros_like(R))
+    assert bool((torch.diagonal(R) >= 0).all())
+
+
 def test_qr_random_gaussian_residuals():
     """Ill-conditioned (Gaussian) input: Q is less determined, residuals still tiny."""
     import paper_2607_20548_amd as soap
