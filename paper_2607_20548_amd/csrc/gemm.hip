@@ -499,7 +499,7 @@ hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) 
   }
 #undef SOAP_LAUNCH
   hipError_t err = hipGetLastError();
-  if (err != hipSuccess || S == 1) return err;
+  if (err != hipSuccess || S == 1 || d.partials_only) return err;
   int64_t mn = d.M * d.N;
   unsigned gx = (unsigned)std::min<int64_t>((mn + 255) / 256, 2048);
   hipLaunchKernelGGL(splitk_reduce, dim3(gx, (unsigned)d.batch), dim3(256), 0, s, kp.part, S,

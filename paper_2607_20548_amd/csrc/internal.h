@@ -30,6 +30,9 @@ struct GemmDesc {
   // summed in a fixed order by a second kernel.
   int splitk = 1;
   float *part = nullptr;
+  // With split-K: leave the partials in `part` for the caller to reduce
+  // (C is not written).
+  bool partials_only = false;
   // Distinct kernel symbol for profiling (0 = shared GEMM; 1, 2 = the power
   // products L Q_L and R Q_R), so that a trace can attribute time per stage.
   int tag = 0;

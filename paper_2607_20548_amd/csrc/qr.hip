@@ -946,6 +946,81 @@ __global__ __launch_bounds__(256) void qr_assemble_pair_t_kernel(float *TP, int6
   }
 }
 
+// Near update, second product: W2 = T^T W with W = sum_s part[s] (the S
+// split-K partials of W = Y^T A_next, each nb x Nt row-major, summed in slice
+// order) and T the block's nb x nb upper-triangular factor (row-major, leading
+// dimension NB).  One workgroup per 8 columns of W2: it sums its columns of
+// the partials into LDS, stages T, and forms its 8 columns of T^T W (k in
+// increasing order).  Replaces a reduction pass and a one-tile GEMM on the
+// factorization's critical path.
+__global__ __launch_bounds__(256) void qr_near_reduce_tt_kernel(const float *__restrict__ part,
+                                                                int S, int nb, int Nt,
+                                                                const float *__restrict__ T,
+                                                                int64_t sT, float *__restrict__ W2,
+                                                                int64_t sW) {
+  __shared__ float Ts[NB][NB + 1];
+  __shared__ float Ws[NB][8];
+  const int64_t bz = blockIdx.y;
+  const int t = threadIdx.x;
+  const int j0 = blockIdx.x * 8;
+  const float *Tb = T + bz * sT;
+  if (nb == NB && (reinterpret_cast<uintptr_t>(Tb) & 15u) == 0) {   // 16 float4 per thread
+    const float4 *T4 = reinterpret_cast<const float4 *>(Tb);
+    float4 tv[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) tv[q] = T4[t + 256 * q];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int e4 = t + 256 * q, k = e4 / (NB / 4), i = 4 * (e4 % (NB / 4));
+      Ts[k][i] = tv[q].x; Ts[k][i + 1] = tv[q].y; Ts[k][i + 2] = tv[q].z; Ts[k][i + 3] = tv[q].w;
+    }
+  } else {
+    for (int e = t; e < NB * NB; e += 256) {
+      const int k = e / NB, i = e % NB;
+      Ts[k][i] = (k < nb && i < nb) ? Tb[k * NB + i] : 0.f;
+    }
+  }
+  const int64_t slice = (int64_t)nb * Nt;
+  const float *pb = part + bz * S * slice;
+  // Four entries per thread, slices in order; loads issued eight slices at a
+  // time so that their latencies overlap.
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  int64_t off[4];
+  bool ok[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = t + 256 * q, k = e >> 3, j = j0 + (e & 7);
+    ok[q] = k < nb && j < Nt;
+    off[q] = ok[q] ? (int64_t)k * Nt + j : 0;
+  }
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    float v[8][4];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        v[u][q] = (s0 + u < S && ok[q]) ? pb[(int64_t)(s0 + u) * slice + off[q]] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[q] += v[u][q];
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = t + 256 * q;
+    Ws[e >> 3][e & 7] = acc[q];
+  }
+  __syncthreads();
+  float *Wb = W2 + bz * sW;
+  for (int e = t; e < NB * 8; e += 256) {
+    const int i = e >> 3, c = e & 7, j = j0 + c;
+    if (i >= nb || j >= Nt) continue;
+    float acc = 0.f;
+    for (int k = 0; k < nb; ++k) acc += Ts[k][i] * Ws[k][c];
+    Wb[(int64_t)i * Nt + j] = acc;
+  }
+}
+
 // Q <- diag(d) for each matrix of the batch.
 __global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *dsign, int n,
                                                         int64_t sA) {
@@ -1189,14 +1264,22 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   g1.splitk = (Nt <= NB) ? narrow_split(nb, Nt, Kr, x.batch, x.batch * x.L.sSk)
                           : choose_splitk(nb, Nt, Kr, x.batch, MAX_SPLIT);
   g1.part = x.Sk;
+  const bool fused = Nt <= NB && g1.splitk > 1;   // the near update (critical path)
+  g1.partials_only = fused;
   SOAP_TRY(launch_gemm(g1, s));
+  if (fused) {   // W2 = T^T (sum of the partials) in one pass
+    hipLaunchKernelGGL(qr_near_reduce_tt_kernel, dim3((unsigned)((Nt + 7) / 8), (unsigned)x.batch),
+                       dim3(256), 0, s, x.Sk, g1.splitk, (int)nb, (int)Nt, Tob, x.L.sT, x.W2,
+                       x.L.sWbuf);
+    SOAP_TRY(hipGetLastError());
+  }
   // W2 = T^T W
   GemmDesc g2;
   g2.trans_a = 1; g2.trans_b = 0; g2.M = nb; g2.N = Nt; g2.K = nb;
   g2.A = Tob; g2.lda = NB; g2.sA = x.L.sT;
   g2.B = x.Wb; g2.ldb = Nt; g2.sB = x.L.sWbuf;
   g2.C = x.W2; g2.ldc = Nt; g2.sC = x.L.sWbuf; g2.batch = x.batch;
-  SOAP_TRY(launch_gemm(g2, s));
+  if (!fused) SOAP_TRY(launch_gemm(g2, s));
   // At[j0+j][c+k] -= sum_i W2[i][j] Y[k][i]
   GemmDesc g3;
   g3.trans_a = 1; g3.trans_b = 0; g3.M = Nt; g3.N = Kr; g3.K = nb;
