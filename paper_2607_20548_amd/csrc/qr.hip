@@ -493,23 +493,25 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
 // c + g*BK_ROWS .. c + (g+1)*BK_ROWS - 1 of the block in registers: the four
 // lanes 4q..4q+3 of wave w own column k = 8q + w (so every wave keeps the
 // same number of active columns as the factorization advances) and lane part
-// holds the local rows 16 i + 4 part + e (i < BK_R/4, e < 4).  Per column j:
-//   * the pivot column is broadcast through LDS and every thread forms the
-//     partial dot of its column with the pivot below the diagonal row;
+// holds the local rows 16 i + 4 part + e (i < BK_R/4, e < 4).  The columns
+// are taken in rounds of two (see the loop for the one-column rounds).  Per
+// round:
+//   * the two pivot columns are broadcast through LDS and every thread forms
+//     the partial dots of its column with both, below their diagonal rows;
 //   * the partials are summed grid-wide in two hops through global memory.
 //     Every value travels as a 64-bit item (value bits | generation << 32)
 //     written and read with agent-scope atomics, so a reader recognises a
-//     fresh value by its generation (global column index + 1) and needs no
-//     barrier or flag: each workgroup posts its partials of all columns (one
-//     contiguous row of items); one wave of the owner of each chunk of 8
-//     columns (workgroup 1 + chunk mod (P-1)) sums the P partials of each of
-//     its columns in a fixed order, reads the diagonal-row values from
-//     workgroup 0, and forwards both into a private copy for every workgroup
+//     fresh value by its generation (round index + 1 past the block's first
+//     column) and needs no barrier or flag: each workgroup posts its partials
+//     of all columns (contiguous rows of items); one wave of the owner of each
+//     chunk of 8 columns (workgroup 1 + chunk mod (P-1)) sums the P partials of
+//     each of its columns in a fixed order, reads the diagonal-row values from
+//     workgroup 0, and forwards them into a private copy for every workgroup
 //     (so that no cache line is polled by more than one workgroup); every
 //     workgroup reads the totals it needs from its copy, so all of them apply
-//     bit-identical reflectors.  Items are double-buffered by column parity:
-//     no workgroup can get two columns ahead of a reader;
-//   * every thread updates its own column.
+//     bit-identical reflectors.  Items are double-buffered by round parity:
+//     no workgroup can get two rounds ahead of a reader;
+//   * every thread applies both reflectors to its own column.
 // Workgroup 0 holds the block's diagonal rows: its pivot broadcast is zero at
 // and above the diagonal row (so its dot products need no masks), it posts
 // the diagonal-row values, and it keeps S = strict upper part of Y^T Y,
@@ -527,18 +529,22 @@ constexpr int BK_WAVES = BK_THREADS / 64;
 constexpr int BK_PARTS = 4;                     // threads per column
 constexpr int BK_R = 64;                        // rows per thread
 constexpr int BK_ROWS = BK_PARTS * BK_R;        // rows per workgroup
-constexpr int BK_MAX_ITEMS = 16;                // partials summed per owner thread
-constexpr int BK_MAX_P = BK_PARTS * BK_MAX_ITEMS;   // workgroups per matrix (n <= 16384)
+constexpr int BK_MAX_P = 64;                    // workgroups per matrix (n <= 16384);
+                                                // an owner lane sums at most 8 partials
 constexpr int BK_MAX_WG = 96;                   // workgroups per launch
 constexpr unsigned BK_SPIN_LIMIT = 1u << 22;
 constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (spreads banks)
-// exchange area per matrix, in 64-bit items: partials [2][BK_MAX_P][NB],
-// diagonal-row values of workgroup 0 [2][NB], per-reader copies of
-// (total, diagonal-row value) [BK_MAX_P][2][NB][2] (4 KiB per reader), abort flag
+// A round takes two columns when H_j leaves column j+1 at least this fraction
+// of its squared norm (rows j+1.. after H_j against rows j.. before it).
+constexpr float BK_PAIR_TAU = 0.0625f;
+// exchange area per matrix, in 64-bit items, all by round parity: partials
+// [2][2 sums][BK_MAX_P][NB], values of workgroup 0 in the diagonal rows j, j+1
+// [2][2][NB], per-reader copies of (D, A, E, B) [BK_MAX_P][2][NB][4] (8 KiB
+// per reader), abort flag
 constexpr int64_t BK_XD = 0;
-constexpr int64_t BK_XA = 2 * NB * BK_MAX_P;
-constexpr int64_t BK_XC = BK_XA + 2 * NB;
-constexpr int64_t BK_XABORT = BK_XC + (int64_t)BK_MAX_P * 2 * NB * 2;
+constexpr int64_t BK_XA = 2 * 2 * (int64_t)BK_MAX_P * NB;
+constexpr int64_t BK_XC = BK_XA + 2 * 2 * NB;
+constexpr int64_t BK_XABORT = BK_XC + (int64_t)BK_MAX_P * 2 * NB * 4;
 constexpr int64_t BK_XSTRIDE = BK_XABORT + 32;
 
 struct BlockParams {
@@ -581,33 +587,6 @@ __device__ __forceinline__ bool bk_give_up(unsigned &spins, unsigned *abort_flag
   return false;
 }
 
-// Owner hop: waits for generation `gen` of the partials p[0], p[stride], ...,
-// p[stride (cnt-1)] (re-reading only those not yet current) and returns their
-// sum in order.  false: aborted.
-__device__ __forceinline__ bool bk_sum_partials(const unsigned long long *p, int stride, int cnt,
-                                                unsigned gen, unsigned *abort_flag, float &sum) {
-  float v[BK_MAX_ITEMS];
-  unsigned pending = (cnt >= 32) ? ~0u : ((1u << cnt) - 1u);
-  unsigned spins = 0;
-  for (;;) {
-#pragma unroll
-    for (int u = 0; u < BK_MAX_ITEMS; ++u)
-      if (pending & (1u << u)) {
-        const unsigned long long it = bk_get(p + (int64_t)stride * u);
-        v[u] = __uint_as_float((unsigned)it);
-        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << u);
-      }
-    if (pending == 0u) break;
-    if (bk_give_up(spins, abort_flag)) return false;
-  }
-  float s = 0.f;
-#pragma unroll
-  for (int u = 0; u < BK_MAX_ITEMS; ++u)
-    if (u < cnt) s += v[u];
-  sum = s;
-  return true;
-}
-
 // Reader hop: waits for generation `gen` of the items at p and (if q is not
 // null) q.  false: aborted.
 __device__ __forceinline__ bool bk_read2(const unsigned long long *p, const unsigned long long *q,
@@ -631,6 +610,64 @@ __device__ __forceinline__ bool bk_read2(const unsigned long long *p, const unsi
   }
 }
 
+// Owner hop for two sums: waits for generation `gen` of the partials
+// p[stride u] and q[stride u], u < cnt <= 8 (re-reading only those not yet
+// current), and returns both sums in index order.  false: aborted.
+__device__ __forceinline__ bool bk_sum_partials2(const unsigned long long *p,
+                                                 const unsigned long long *q, int stride, int cnt,
+                                                 unsigned gen, unsigned *abort_flag, float &sp,
+                                                 float &sq) {
+  float v[8], w[8];
+  const unsigned m = (1u << cnt) - 1u;
+  unsigned pending = m | (m << 8);
+  unsigned spins = 0;
+  for (;;) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (pending & (1u << u)) {
+        const unsigned long long it = bk_get(p + (int64_t)stride * u);
+        v[u] = __uint_as_float((unsigned)it);
+        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << u);
+      }
+      if (pending & (1u << (u + 8))) {
+        const unsigned long long it = bk_get(q + (int64_t)stride * u);
+        w[u] = __uint_as_float((unsigned)it);
+        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << (u + 8));
+      }
+    }
+    if (pending == 0u) break;
+    if (bk_give_up(spins, abort_flag)) return false;
+  }
+  float s = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+    if (u < cnt) {
+      s += v[u];
+      s2 += w[u];
+    }
+  sp = s;
+  sq = s2;
+  return true;
+}
+
+// Householder reflector of a column with diagonal value x0 and tail sum of
+// squares st (the larfg convention above): beta, 1 / v0 and the R diagonal.
+// st == 0: the column is already triangular, H = I.
+__device__ __forceinline__ void bk_reflector(float x0, float st, float &bet, float &inv_v0,
+                                             float &rjj) {
+  if (st == 0.f) {
+    bet = 0.f;
+    inv_v0 = 0.f;
+    rjj = x0;
+  } else {
+    const float sigma = sqrtf(x0 * x0 + st);
+    const float v0 = (x0 >= 0.f) ? (x0 + sigma) : (x0 - sigma);
+    bet = 2.f * v0 * v0 / (st + v0 * v0);
+    inv_v0 = 1.f / v0;
+    rjj = (x0 >= 0.f) ? -sigma : sigma;
+  }
+}
+
 template <int R>
 __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   constexpr int NI = R / 4;
@@ -638,8 +675,8 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   // register groups i that can hold one of the diagonal rows 0..NB-1 of
   // workgroup 0 (local row 16 i + 4 part + e < NB); only these need masks
   constexpr int NIM = (NB / 16 < NI) ? NB / 16 : NI;
-  __shared__ float px[2][RS];            // pivot column, by column parity
-  __shared__ float pv[2][2];             // pivot tail sum of squares and diagonal value
+  __shared__ float px[2][2][RS];         // pivot columns j, j+1, by round parity
+  __shared__ float pv[2][8];             // their totals, by round parity
   __shared__ float bs[NB];               // beta_j (workgroup 0)
   __shared__ float Ss[NB * BK_TSTR];     // S (workgroup 0), row-major
   __shared__ float Ts[NB * BK_TSTR];     // T (workgroup 0), row-major
@@ -671,21 +708,39 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   bool alive = true;
   const int nchunk = (nb + 7) / 8;
 
-  for (int j = 0; j < nb; ++j) {
-    const int par = j & 1;
-    const unsigned gen = (unsigned)(c + j + 1);
-    if (k == j) {
+  // Rounds of one or two columns.  A round broadcasts pivot column j (its
+  // tail below the diagonal row j) and, if there is one, column j+1 (its tail
+  // below row j+1); every thread forms the dots of its column with both, and
+  // one grid-wide exchange gives every column
+  //   D = sum_{r>j} a_r x_r,  E = sum_{r>j+1} a_r y_r,  A = a_j,  B = a_{j+1}.
+  // Reflector j comes from (D_j, A_j) as in a one-column step.  The effect of
+  // H_j on column j+1 and on the dots with it follows from these sums (the
+  // 2 x 2 Gram correction below), so reflector j+1 and the update of every
+  // later column by H_j H_{j+1} need no second exchange.  When H_j removes
+  // most of column j+1 (its norm from row j+1 down falls below a quarter of
+  // its norm from row j down) the corrected sums would lose digits to
+  // cancellation: the round then applies H_j alone and the next round starts
+  // at column j+1.  Every workgroup takes this decision from the same totals
+  // with the same arithmetic, so all of them follow the same rounds.
+  int j = 0;
+  for (int round = 0; j < nb; ++round) {
+    const int par = round & 1;
+    const unsigned gen = (unsigned)(c + round + 1);   // rounds <= columns: unique per call
+    const bool two = j + 1 < nb;
+    if (k == j || (two && k == j + 1)) {
+      float *dst = px[par][k - j];
 #pragma unroll
       for (int i = 0; i < NI; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int lr = 16 * i + 4 * part + e;
-          px[par][lr] = (w0 && i < NIM && lr <= j) ? 0.f : a[i][e];
+          dst[lr] = (w0 && i < NIM && lr <= k) ? 0.f : a[i][e];
         }
     }
     __syncthreads();
-    const float *x = px[par];
-    float d = 0.f, av = 0.f;
+    const float *x = px[par][0];
+    const float *y = px[par][1];
+    float d = 0.f, ev = 0.f, av0 = 0.f, av1 = 0.f;
     if (col) {
       float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -693,92 +748,172 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) acc[e] += a[i][e] * x[16 * i + 4 * part + e];
       d = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-      if (w0) {   // value of the diagonal row j
+      if (two) {
+        float acc2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc2[e] += a[i][e] * y[16 * i + 4 * part + e];
+        ev = (acc2[0] + acc2[1]) + (acc2[2] + acc2[3]);
+      }
+      if (w0) {   // values of the diagonal rows j and j+1
 #pragma unroll
         for (int i = 0; i < NIM; ++i)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) av = (16 * i + 4 * part + e == j) ? a[i][e] : av;
+          for (int e = 0; e < 4; ++e) {
+            const int lr = 16 * i + 4 * part + e;
+            av0 = (lr == j) ? a[i][e] : av0;
+            av1 = (lr == j + 1) ? a[i][e] : av1;
+          }
       }
     }
     d += __shfl_xor(d, 1);
     d += __shfl_xor(d, 2);
-    av += __shfl_xor(av, 1);
-    av += __shfl_xor(av, 2);
-    float D = d, A = av;
+    ev += __shfl_xor(ev, 1);
+    ev += __shfl_xor(ev, 2);
+    av0 += __shfl_xor(av0, 1);
+    av0 += __shfl_xor(av0, 2);
+    av1 += __shfl_xor(av1, 1);
+    av1 += __shfl_xor(av1, 2);
+    float D = d, E = ev, A = av0, B = av1;
     if (P > 1) {
-      unsigned long long *xa = X + BK_XA + par * NB;
+      unsigned long long *xa = X + BK_XA + (int64_t)par * 2 * NB;   // [row j, row j+1][NB]
       const int lead = lane & ~3;              // lane of part 0 of this column
-      if (col && part == 0) bk_put(X + BK_XD + ((int64_t)par * BK_MAX_P + g) * NB + k, d, gen);
-      if (w0 && col && part == 1) bk_put(xa + k, av, gen);
+      if (col && part == 0) bk_put(X + BK_XD + (((int64_t)par * 2 + 0) * BK_MAX_P + g) * NB + k, d, gen);
+      if (col && part == 2) bk_put(X + BK_XD + (((int64_t)par * 2 + 1) * BK_MAX_P + g) * NB + k, ev, gen);
+      if (w0 && col && part == 1) bk_put(xa + k, av0, gen);
+      if (w0 && col && part == 3) bk_put(xa + NB + k, av1, gen);
       // owner hop: chunk ch (columns 8ch..8ch+7) belongs to one wave of
       // workgroup 1 + ch mod (P-1); lane (u, c8) sums the partials of
-      // workgroups u, u+8, ... of column 8ch+c8, then the wave adds across u.
-      // (wave w of workgroup g >= 1 owns chunks g-1 + (P-1)(w + 8m), m >= 0)
+      // workgroups u, u+8, ... of column 8ch+c8 (both sums), then the wave
+      // adds across u.  (wave w of workgroup g >= 1 owns chunks
+      // g-1 + (P-1)(w + 8m), m >= 0)
       for (int ch = g - 1 + (P - 1) * wave; g > 0 && ch < nchunk; ch += (P - 1) * BK_WAVES) {
         const int c8 = lane & 7, u = lane >> 3, kc = 8 * ch + c8;
-        float s = 0.f, aval = 0.f, unused = 0.f;
+        float s = 0.f, s2 = 0.f, aval = 0.f, bval = 0.f;
         const int cnt = (P - u + 7) / 8;
         if (kc < nb && alive)
-          alive = bk_sum_partials(X + BK_XD + ((int64_t)par * BK_MAX_P + u) * NB + kc, 8 * NB, cnt,
-                                  gen, abort_flag, s);
+          alive = bk_sum_partials2(X + BK_XD + (((int64_t)par * 2 + 0) * BK_MAX_P + u) * NB + kc,
+                                   X + BK_XD + (((int64_t)par * 2 + 1) * BK_MAX_P + u) * NB + kc,
+                                   8 * NB, cnt, gen, abort_flag, s, s2);
         s += __shfl_xor(s, 8);
         s += __shfl_xor(s, 16);
         s += __shfl_xor(s, 32);
-        if (kc < nb && u == 0 && alive) alive = bk_read2(xa + kc, nullptr, gen, abort_flag, aval, unused);
+        s2 += __shfl_xor(s2, 8);
+        s2 += __shfl_xor(s2, 16);
+        s2 += __shfl_xor(s2, 32);
+        if (kc < nb && u == 0 && alive) alive = bk_read2(xa + kc, xa + NB + kc, gen, abort_flag, aval, bval);
         aval = __shfl(aval, c8);
+        bval = __shfl(bval, c8);
         if (kc < nb)
           for (int r = u; r < P; r += 8) {
-            unsigned long long *cp = X + BK_XC + (((int64_t)r * 2 + par) * NB + kc) * 2;
+            unsigned long long *cp = X + BK_XC + (((int64_t)r * 2 + par) * NB + kc) * 4;
             bk_put(cp, s, gen);
             bk_put(cp + 1, aval, gen);
+            bk_put(cp + 2, s2, gen);
+            bk_put(cp + 3, bval, gen);
           }
       }
-      if (col && (w0 || k >= j)) {             // reader hop (one lane per column)
-        const unsigned long long *cp = X + BK_XC + (((int64_t)g * 2 + par) * NB + k) * 2;
-        float tot = 0.f, aa = 0.f;
-        if (part == 0 && alive) alive = bk_read2(cp, w0 ? nullptr : cp + 1, gen, abort_flag, tot, aa);
-        D = __shfl(tot, lead);
-        aa = __shfl(aa, lead);
-        if (!w0) A = aa;
+      if (col && (w0 || k >= j)) {             // reader hop (two lanes per column)
+        const unsigned long long *cp = X + BK_XC + (((int64_t)g * 2 + par) * NB + k) * 4;
+        float v0 = 0.f, v1 = 0.f;
+        if (part < 2 && alive)
+          alive = bk_read2(cp + 2 * part, w0 ? nullptr : cp + 2 * part + 1, gen, abort_flag, v0, v1);
+        D = __shfl(v0, lead);
+        E = __shfl(v0, lead + 1);
+        const float aa = __shfl(v1, lead), bb = __shfl(v1, lead + 1);
+        if (!w0) {
+          A = aa;
+          B = bb;
+        }
       }
     }
-    if (k == j && part == 0) {
-      pv[par][0] = D;
-      pv[par][1] = A;
+    if (part == 0) {
+      if (k == j) {
+        pv[par][0] = D;
+        pv[par][1] = A;
+        pv[par][2] = B;
+      } else if (two && k == j + 1) {
+        pv[par][3] = D;
+        pv[par][4] = A;
+        pv[par][5] = B;
+        pv[par][6] = E;
+      }
     }
     __syncthreads();
-    const float st = pv[par][0], x0 = pv[par][1];
+    const float st = pv[par][0], x0 = pv[par][1], Bj = pv[par][2];
     float bet, inv_v0, rjj;
-    if (st == 0.f) {          // already triangular: H = I
-      bet = 0.f;
-      inv_v0 = 0.f;
-      rjj = x0;
-    } else {
-      const float sigma = sqrtf(x0 * x0 + st);
-      const float v0 = (x0 >= 0.f) ? (x0 + sigma) : (x0 - sigma);
-      bet = 2.f * v0 * v0 / (st + v0 * v0);
-      inv_v0 = 1.f / v0;
-      rjj = (x0 >= 0.f) ? -sigma : sigma;
+    bk_reflector(x0, st, bet, inv_v0, rjj);
+    // Column j+1 after H_j: f1 = beta_j v_j^T a_{j+1}, its diagonal value
+    // x0b and tail sum of squares stb from the sums; sxy and sxx are the dots
+    // of x with y and with itself below row j+1.
+    bool pair = false;
+    float fs1 = 0.f, sxy = 0.f, sxx = 0.f, f1 = 0.f;
+    float bet2 = 0.f, inv_v02 = 0.f, rjj2 = 0.f;
+    if (two) {
+      const float D1 = pv[par][3], A1 = pv[par][4], B1 = pv[par][5], E1 = pv[par][6];
+      f1 = bet * (A1 + D1 * inv_v0);
+      fs1 = f1 * inv_v0;
+      sxy = D1 - B1 * Bj;
+      sxx = st - Bj * Bj;
+      const float x0b = B1 - fs1 * Bj;
+      const float stb = E1 - 2.f * fs1 * sxy + fs1 * fs1 * sxx;
+      const float ref = A1 * A1 + B1 * B1 + E1;
+      pair = stb >= 0.f && x0b * x0b + stb >= BK_PAIR_TAU * ref;
+      if (pair) bk_reflector(x0b, stb, bet2, inv_v02, rjj2);
     }
-    if (col && k > j) {
-      // a -= f v with v = [1 at the diagonal row; x / v0 below it]; in
-      // workgroup 0 the broadcast x is zero at and above the diagonal row
+    const int jl = pair ? j + 1 : j;           // last column of this round
+    if (col && k > jl) {
       const float f = bet * (A + D * inv_v0);
       const float fs = f * inv_v0;
-      if (w0) {
+      if (pair) {
+        // H_j H_{j+1} at once: a -= fs x + fsp (y - fs1 x) below row j+1,
+        // with fsp from the dot of the updated column and updated pivot.
+        const float ak1 = B - fs * Bj;
+        const float dp = E - fs1 * (D - B * Bj) - fs * sxy + fs * fs1 * sxx;
+        const float fp = bet2 * (ak1 + dp * inv_v02);
+        const float fsp = fp * inv_v02;
+        const float c1 = fs - fsp * fs1;
+        if (w0) {
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
+          for (int i = 0; i < NI; ++i)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int lr = 16 * i + 4 * part + e;
-            a[i][e] = fmaf(-fs, x[lr], a[i][e]);
-            if (i < NIM) a[i][e] -= (lr == j) ? f : 0.f;
-          }
+            for (int e = 0; e < 4; ++e) {
+              const int lr = 16 * i + 4 * part + e;
+              float v = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
+              if (i < NIM) {
+                v = (lr == j) ? a[i][e] - f : v;
+                v = (lr == j + 1) ? a[i][e] - fs * Bj - fp : v;
+              }
+              a[i][e] = v;
+            }
+        } else {
+#pragma unroll
+          for (int i = 0; i < NI; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int lr = 16 * i + 4 * part + e;
+              a[i][e] = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
+            }
+        }
       } else {
+        // a -= f v with v = [1 at the diagonal row; x / v0 below it]; in
+        // workgroup 0 the broadcast x is zero at and above the diagonal row
+        if (w0) {
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
+          for (int i = 0; i < NI; ++i)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[16 * i + 4 * part + e], a[i][e]);
+            for (int e = 0; e < 4; ++e) {
+              const int lr = 16 * i + 4 * part + e;
+              a[i][e] = fmaf(-fs, x[lr], a[i][e]);
+              if (i < NIM) a[i][e] -= (lr == j) ? f : 0.f;
+            }
+        } else {
+#pragma unroll
+          for (int i = 0; i < NI; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[16 * i + 4 * part + e], a[i][e]);
+        }
       }
     } else if (k == j) {
       if (w0) {
@@ -798,17 +933,53 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) a[i][e] *= inv_v0;
       }
+    } else if (pair && k == j + 1) {
+      // column j+1: H_j, then its own reflector (R entry in row j, R
+      // diagonal in row j+1, v below)
+      if (w0) {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int lr = 16 * i + 4 * part + e;
+            const float v = fmaf(-fs1, x[lr], a[i][e]) * inv_v02;
+            if (i < NIM)
+              a[i][e] = (lr > j + 1) ? v : ((lr == j + 1) ? rjj2 : ((lr == j) ? a[i][e] - f1 : a[i][e]));
+            else
+              a[i][e] = v;
+          }
+      } else {
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            a[i][e] = fmaf(-fs1, x[16 * i + 4 * part + e], a[i][e]) * inv_v02;
+      }
     }
     if (w0) {
-      if (col && k < j && part == 0) Ss[k * BK_TSTR + j] = A + D * inv_v0;
+      // S[l][j] = y_l^T v_j for the stored reflectors l < j, and for pairs
+      // S[l][j+1] = y_l^T v_{j+1} (l <= j), from the same sums
+      if (col && part == 0) {
+        if (k < j) {
+          Ss[k * BK_TSTR + j] = A + D * inv_v0;
+          if (pair) Ss[k * BK_TSTR + j + 1] = B + inv_v02 * (E - fs1 * (D - B * Bj));
+        } else if (pair && k == j) {
+          Ss[j * BK_TSTR + j + 1] = Bj * inv_v0 + inv_v0 * inv_v02 * (sxy - fs1 * sxx);
+        }
+      }
       if (t == 0) {
         bs[j] = bet;
         p.beta[bz * n + c + j] = bet;
         p.dsign[bz * n + c + j] = (rjj < 0.f) ? -1.f : 1.f;
+        if (pair) {
+          bs[j + 1] = bet2;
+          p.beta[bz * n + c + j + 1] = bet2;
+          p.dsign[bz * n + c + j + 1] = (rjj2 < 0.f) ? -1.f : 1.f;
+        }
       }
     }
+    j = jl + 1;
   }
-
   // Write Y (zeros above its diagonal, ones on it) and the R entries of the
   // block's diagonal rows.  An aborted exchange poisons the block.
   const bool bad =

@@ -143,6 +143,37 @@ def test_qr_q_only_matches_oracle(n):
     assert np.linalg.norm(Q.T @ Q - np.eye(n)) / np.sqrt(n) <= 1e-5
 
 
+@pytest.mark.parametrize("n", [300, 640])
+def test_qr_nearly_dependent_neighbour_columns(n):
+    """Every third column is 1.5 x its left neighbour plus 5% of a fresh
+    direction: the reflector of the left column removes most of it, so the
+    block factorization takes that column in a round of its own (no
+    two-column round), at every alignment.  Q against the oracle and the
+    residuals at the usual bar."""
+    import paper_2607_20548_amd as soap
+    import oracle
+    import torch
+    log(f"qr nearly dependent n={n}")
+    B = _well_conditioned(n, 3).astype(np.float64)
+    A = B.copy()
+    for j in range(0, n - 1, 3):
+        A[:, j + 1] = 1.5 * A[:, j] + 0.05 * B[:, j + 1]
+    A = A.astype(np.float32)
+    Qd = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    Rd = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    wsb = soap.soap_qr_workspace_bytes(n)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    soap.soap_qr_f32(n, dev(A), Qd, Rd, ws, wsb)
+    Q, R = host(Qd), host(Rd)
+    A64 = A.astype(np.float64)
+    Qo = oracle.householder_qr(A64)
+    assert column_signs_agree(Q, Qo)
+    assert rel(Q, Qo) <= 1e-4
+    assert np.linalg.norm(Q @ R - A64) / np.linalg.norm(A64) <= 1e-5
+    assert np.linalg.norm(Q.T @ Q - np.eye(n)) / np.sqrt(n) <= 1e-5
+    assert np.all(np.tril(R, -1) == 0) and np.all(np.diag(R) >= 0)
+
+
 def test_qr_large_residuals_rank1024_q_formation():
     """n = 8576 = 67 blocks: Q formed by rank-1024 updates (8 octs) plus a
     leftover pair and block; residuals computed in fp64 on the GPU."""
