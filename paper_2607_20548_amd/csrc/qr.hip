@@ -490,25 +490,23 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
 // ------------------------------------------------ resident-block factorization
 // One launch factors a whole outer block (rows c..n-1, nb <= NB columns) with
 // the same reflectors as the panel path.  Workgroup g keeps rows
-// c + g*BK_ROWS .. c + (g+1)*BK_ROWS - 1 of the block in registers: the four
-// lanes 4q..4q+3 of wave w own column k = 8q + w (so every wave keeps the
+// c + g*BK_ROWS .. c + (g+1)*BK_ROWS - 1 of the block in registers: the eight
+// lanes 8q..8q+7 of wave w own column k = 16q + w (so every wave keeps the
 // same number of active columns as the factorization advances) and lane part
-// holds the local rows 16 i + 4 part + e (i < BK_R/4, e < 4).  The columns
+// holds the local rows 32 i + 4 part + e (i < BK_R/4, e < 4): 32 values per
+// lane and four waves per SIMD to hide the latency of each round.  The columns
 // are taken in rounds of two (see the loop for the one-column rounds).  Per
 // round:
 //   * the two pivot columns are broadcast through LDS and every thread forms
 //     the partial dots of its column with both, below their diagonal rows;
-//   * the partials are summed grid-wide in two hops through global memory.
+//   * the partials are summed grid-wide in one hop through global memory.
 //     Every value travels as a 64-bit item (value bits | generation << 32)
 //     written and read with agent-scope atomics, so a reader recognises a
 //     fresh value by its generation (round index + 1 past the block's first
 //     column) and needs no barrier or flag: each workgroup posts its partials
-//     of all columns (contiguous rows of items); one wave of the owner of each
-//     chunk of 8 columns (workgroup 1 + chunk mod (P-1)) sums the P partials of
-//     each of its columns in a fixed order, reads the diagonal-row values from
-//     workgroup 0, and forwards them into a private copy for every workgroup
-//     (so that no cache line is polled by more than one workgroup); every
-//     workgroup reads the totals it needs from its copy, so all of them apply
+//     of all columns (contiguous rows of items) and workgroup 0 the
+//     diagonal-row values; every workgroup then reads the P partials of each
+//     column it needs and sums them in one fixed order, so all of them apply
 //     bit-identical reflectors.  Items are double-buffered by round parity:
 //     no workgroup can get two rounds ahead of a reader;
 //   * every thread applies both reflectors to its own column.
@@ -524,11 +522,12 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
 // to BK_MAX_WG workgroups.  Waits are bounded: one that exceeds BK_SPIN_LIMIT
 // polls raises a per-matrix abort flag, after which every wait returns at
 // once and the block is written as NaN, so the kernel always ends.
-constexpr int BK_THREADS = 512;
+constexpr int BK_THREADS = 1024;
 constexpr int BK_WAVES = BK_THREADS / 64;
-constexpr int BK_PARTS = 4;                     // threads per column
-constexpr int BK_R = 64;                        // rows per thread
+constexpr int BK_PARTS = 8;                     // threads per column
+constexpr int BK_R = 32;                        // rows per thread
 constexpr int BK_ROWS = BK_PARTS * BK_R;        // rows per workgroup
+constexpr int BK_LI = 4 * BK_PARTS;             // local-row stride of a thread's register groups
 constexpr int BK_MAX_P = 64;                    // workgroups per matrix (n <= 16384);
                                                 // an owner lane sums at most 8 partials
 constexpr int BK_MAX_WG = 96;                   // workgroups per launch
@@ -538,13 +537,12 @@ constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (sp
 // of its squared norm (rows j+1.. after H_j against rows j.. before it).
 constexpr float BK_PAIR_TAU = 0.0625f;
 // exchange area per matrix, in 64-bit items, all by round parity: partials
-// [2][2 sums][BK_MAX_P][NB], values of workgroup 0 in the diagonal rows j, j+1
-// [2][2][NB], per-reader copies of (D, A, E, B) [BK_MAX_P][2][NB][4] (8 KiB
-// per reader), abort flag
+// [2][2 sums][BK_MAX_P][NB] and values of workgroup 0 in the diagonal rows j,
+// j+1 [2][2][NB], column k at position (k mod 8) * 16 + k / 8 (the columns of
+// one wave are contiguous), then the abort flag
 constexpr int64_t BK_XD = 0;
 constexpr int64_t BK_XA = 2 * 2 * (int64_t)BK_MAX_P * NB;
-constexpr int64_t BK_XC = BK_XA + 2 * 2 * NB;
-constexpr int64_t BK_XABORT = BK_XC + (int64_t)BK_MAX_P * 2 * NB * 4;
+constexpr int64_t BK_XABORT = BK_XA + 2 * 2 * NB;
 constexpr int64_t BK_XSTRIDE = BK_XABORT + 32;
 
 struct BlockParams {
@@ -587,66 +585,38 @@ __device__ __forceinline__ bool bk_give_up(unsigned &spins, unsigned *abort_flag
   return false;
 }
 
-// Reader hop: waits for generation `gen` of the items at p and (if q is not
-// null) q.  false: aborted.
-__device__ __forceinline__ bool bk_read2(const unsigned long long *p, const unsigned long long *q,
-                                         unsigned gen, unsigned *abort_flag, float &vp,
-                                         float &vq) {
-  unsigned spins = 0;
-  bool hp = false, hq = (q == nullptr);
-  for (;;) {
-    if (!hp) {
-      const unsigned long long a = bk_get(p);
-      vp = __uint_as_float((unsigned)a);
-      hp = (unsigned)(a >> 32) == gen;
-    }
-    if (!hq) {
-      const unsigned long long b = bk_get(q);
-      vq = __uint_as_float((unsigned)b);
-      hq = (unsigned)(b >> 32) == gen;
-    }
-    if (hp && hq) return true;
-    if (bk_give_up(spins, abort_flag)) return false;
-  }
-}
-
-// Owner hop for two sums: waits for generation `gen` of the partials
-// p[stride u] and q[stride u], u < cnt <= 8 (re-reading only those not yet
-// current), and returns both sums in index order.  false: aborted.
-__device__ __forceinline__ bool bk_sum_partials2(const unsigned long long *p,
-                                                 const unsigned long long *q, int stride, int cnt,
-                                                 unsigned gen, unsigned *abort_flag, float &sp,
-                                                 float &sq) {
-  float v[8], w[8];
-  const unsigned m = (1u << cnt) - 1u;
-  unsigned pending = m | (m << 8);
+// Waits for generation `gen` of the items p[stride i], i < cnt <= 16, and
+// (if x is not null) of the item x, re-reading only those not yet current;
+// returns the sum of the first in index order and the value of x.  false:
+// aborted.
+__device__ __forceinline__ bool bk_gather(const unsigned long long *p, int stride, int cnt,
+                                          const unsigned long long *x, unsigned gen,
+                                          unsigned *abort_flag, float &sum, float &xv) {
+  float v[16];
+  unsigned pending = (1u << cnt) - 1u;
+  bool hx = (x == nullptr);
   unsigned spins = 0;
   for (;;) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (pending & (1u << u)) {
-        const unsigned long long it = bk_get(p + (int64_t)stride * u);
-        v[u] = __uint_as_float((unsigned)it);
-        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << u);
+    for (int i = 0; i < 16; ++i)
+      if (pending & (1u << i)) {
+        const unsigned long long it = bk_get(p + (int64_t)stride * i);
+        v[i] = __uint_as_float((unsigned)it);
+        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << i);
       }
-      if (pending & (1u << (u + 8))) {
-        const unsigned long long it = bk_get(q + (int64_t)stride * u);
-        w[u] = __uint_as_float((unsigned)it);
-        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << (u + 8));
-      }
+    if (!hx) {
+      const unsigned long long it = bk_get(x);
+      xv = __uint_as_float((unsigned)it);
+      hx = (unsigned)(it >> 32) == gen;
     }
-    if (pending == 0u) break;
+    if (pending == 0u && hx) break;
     if (bk_give_up(spins, abort_flag)) return false;
   }
-  float s = 0.f, s2 = 0.f;
+  float s = 0.f;
 #pragma unroll
-  for (int u = 0; u < 8; ++u)
-    if (u < cnt) {
-      s += v[u];
-      s2 += w[u];
-    }
-  sp = s;
-  sq = s2;
+  for (int i = 0; i < 16; ++i)
+    if (i < cnt) s += v[i];
+  sum = s;
   return true;
 }
 
@@ -673,8 +643,8 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   constexpr int NI = R / 4;
   constexpr int RS = BK_PARTS * R;
   // register groups i that can hold one of the diagonal rows 0..NB-1 of
-  // workgroup 0 (local row 16 i + 4 part + e < NB); only these need masks
-  constexpr int NIM = (NB / 16 < NI) ? NB / 16 : NI;
+  // workgroup 0 (local row BK_LI i + 4 part + e < NB); only these need masks
+  constexpr int NIM = (NB / BK_LI < NI) ? NB / BK_LI : NI;
   __shared__ float px[2][2][RS];         // pivot columns j, j+1, by round parity
   __shared__ float pv[2][8];             // their totals, by round parity
   __shared__ float bs[NB];               // beta_j (workgroup 0)
@@ -683,8 +653,8 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
 
   const int g = blockIdx.x;
   const int64_t bz = blockIdx.y;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, part = t & 3;
-  const int k = 8 * (lane >> 2) + wave;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, part = t & (BK_PARTS - 1);
+  const int k = BK_WAVES * (lane / BK_PARTS) + wave;
   const int n = p.n, c = p.c, nb = p.nb, P = p.P;
   const unsigned un = (unsigned)n;     // n*n < 2^31
   float *At = p.At + bz * p.sA;
@@ -701,12 +671,11 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
     for (int i = 0; i < NI; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int row = r0 + 16 * i + 4 * part + e;
+        const int row = r0 + BK_LI * i + 4 * part + e;
         a[i][e] = (col && row < n) ? src[row] : 0.f;
       }
   }
   bool alive = true;
-  const int nchunk = (nb + 7) / 8;
 
   // Rounds of one or two columns.  A round broadcasts pivot column j (its
   // tail below the diagonal row j) and, if there is one, column j+1 (its tail
@@ -733,7 +702,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       for (int i = 0; i < NI; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int lr = 16 * i + 4 * part + e;
+          const int lr = BK_LI * i + 4 * part + e;
           dst[lr] = (w0 && i < NIM && lr <= k) ? 0.f : a[i][e];
         }
     }
@@ -746,14 +715,14 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
 #pragma unroll
       for (int i = 0; i < NI; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] += a[i][e] * x[16 * i + 4 * part + e];
+        for (int e = 0; e < 4; ++e) acc[e] += a[i][e] * x[BK_LI * i + 4 * part + e];
       d = (acc[0] + acc[1]) + (acc[2] + acc[3]);
       if (two) {
         float acc2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < NI; ++i)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc2[e] += a[i][e] * y[16 * i + 4 * part + e];
+          for (int e = 0; e < 4; ++e) acc2[e] += a[i][e] * y[BK_LI * i + 4 * part + e];
         ev = (acc2[0] + acc2[1]) + (acc2[2] + acc2[3]);
       }
       if (w0) {   // values of the diagonal rows j and j+1
@@ -761,67 +730,45 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         for (int i = 0; i < NIM; ++i)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int lr = 16 * i + 4 * part + e;
+            const int lr = BK_LI * i + 4 * part + e;
             av0 = (lr == j) ? a[i][e] : av0;
             av1 = (lr == j + 1) ? a[i][e] : av1;
           }
       }
     }
-    d += __shfl_xor(d, 1);
-    d += __shfl_xor(d, 2);
-    ev += __shfl_xor(ev, 1);
-    ev += __shfl_xor(ev, 2);
-    av0 += __shfl_xor(av0, 1);
-    av0 += __shfl_xor(av0, 2);
-    av1 += __shfl_xor(av1, 1);
-    av1 += __shfl_xor(av1, 2);
+#pragma unroll
+    for (int msk = 1; msk < BK_PARTS; msk <<= 1) {
+      d += __shfl_xor(d, msk);
+      ev += __shfl_xor(ev, msk);
+      av0 += __shfl_xor(av0, msk);
+      av1 += __shfl_xor(av1, msk);
+    }
     float D = d, E = ev, A = av0, B = av1;
     if (P > 1) {
-      unsigned long long *xa = X + BK_XA + (int64_t)par * 2 * NB;   // [row j, row j+1][NB]
-      const int lead = lane & ~3;              // lane of part 0 of this column
-      if (col && part == 0) bk_put(X + BK_XD + (((int64_t)par * 2 + 0) * BK_MAX_P + g) * NB + k, d, gen);
-      if (col && part == 2) bk_put(X + BK_XD + (((int64_t)par * 2 + 1) * BK_MAX_P + g) * NB + k, ev, gen);
-      if (w0 && col && part == 1) bk_put(xa + k, av0, gen);
-      if (w0 && col && part == 3) bk_put(xa + NB + k, av1, gen);
-      // owner hop: chunk ch (columns 8ch..8ch+7) belongs to one wave of
-      // workgroup 1 + ch mod (P-1); lane (u, c8) sums the partials of
-      // workgroups u, u+8, ... of column 8ch+c8 (both sums), then the wave
-      // adds across u.  (wave w of workgroup g >= 1 owns chunks
-      // g-1 + (P-1)(w + 8m), m >= 0)
-      for (int ch = g - 1 + (P - 1) * wave; g > 0 && ch < nchunk; ch += (P - 1) * BK_WAVES) {
-        const int c8 = lane & 7, u = lane >> 3, kc = 8 * ch + c8;
-        float s = 0.f, s2 = 0.f, aval = 0.f, bval = 0.f;
-        const int cnt = (P - u + 7) / 8;
-        if (kc < nb && alive)
-          alive = bk_sum_partials2(X + BK_XD + (((int64_t)par * 2 + 0) * BK_MAX_P + u) * NB + kc,
-                                   X + BK_XD + (((int64_t)par * 2 + 1) * BK_MAX_P + u) * NB + kc,
-                                   8 * NB, cnt, gen, abort_flag, s, s2);
-        s += __shfl_xor(s, 8);
-        s += __shfl_xor(s, 16);
-        s += __shfl_xor(s, 32);
-        s2 += __shfl_xor(s2, 8);
-        s2 += __shfl_xor(s2, 16);
-        s2 += __shfl_xor(s2, 32);
-        if (kc < nb && u == 0 && alive) alive = bk_read2(xa + kc, xa + NB + kc, gen, abort_flag, aval, bval);
-        aval = __shfl(aval, c8);
-        bval = __shfl(bval, c8);
-        if (kc < nb)
-          for (int r = u; r < P; r += 8) {
-            unsigned long long *cp = X + BK_XC + (((int64_t)r * 2 + par) * NB + kc) * 4;
-            bk_put(cp, s, gen);
-            bk_put(cp + 1, aval, gen);
-            bk_put(cp + 2, s2, gen);
-            bk_put(cp + 3, bval, gen);
-          }
-      }
-      if (col && (w0 || k >= j)) {             // reader hop (two lanes per column)
-        const unsigned long long *cp = X + BK_XC + (((int64_t)g * 2 + par) * NB + k) * 4;
-        float v0 = 0.f, v1 = 0.f;
-        if (part < 2 && alive)
-          alive = bk_read2(cp + 2 * part, w0 ? nullptr : cp + 2 * part + 1, gen, abort_flag, v0, v1);
-        D = __shfl(v0, lead);
-        E = __shfl(v0, lead + 1);
-        const float aa = __shfl(v1, lead), bb = __shfl(v1, lead + 1);
+      // One hop: every workgroup posts its partials, then every workgroup
+      // reads the P partials of each column it needs and sums them in the
+      // same order, so all of them hold bit-identical totals.  Lanes 0..3 of
+      // a column sum the D partials of the workgroups u = part mod 4, lanes
+      // 4..7 those of E; lanes 3 and 7 also fetch A and B from workgroup 0.
+      const int64_t pk = (int64_t)(wave * (64 / BK_PARTS) + lane / BK_PARTS);   // position of column k
+      const int lead = lane & ~(BK_PARTS - 1);  // lane of part 0 of this column
+      const int q = part >> 2, u0 = part & 3;
+      if (col && (part == 0 || part == 4))
+        bk_put(X + BK_XD + (((int64_t)par * 2 + q) * BK_MAX_P + g) * NB + pk, q ? ev : d, gen);
+      if (w0 && col && (part == 1 || part == 5))
+        bk_put(X + BK_XA + ((int64_t)par * 2 + q) * NB + pk, q ? av1 : av0, gen);
+      if (col && (w0 || k >= j)) {
+        float ssum = 0.f, xv = 0.f;
+        if (alive)
+          alive = bk_gather(X + BK_XD + (((int64_t)par * 2 + q) * BK_MAX_P + u0) * NB + pk, 4 * NB,
+                            (P - u0 + 3) / 4,
+                            (!w0 && u0 == 3) ? X + BK_XA + ((int64_t)par * 2 + q) * NB + pk : nullptr,
+                            gen, abort_flag, ssum, xv);
+        D = (__shfl(ssum, lead) + __shfl(ssum, lead + 1)) +
+            (__shfl(ssum, lead + 2) + __shfl(ssum, lead + 3));
+        E = (__shfl(ssum, lead + 4) + __shfl(ssum, lead + 5)) +
+            (__shfl(ssum, lead + 6) + __shfl(ssum, lead + 7));
+        const float aa = __shfl(xv, lead + 3), bb = __shfl(xv, lead + 7);
         if (!w0) {
           A = aa;
           B = bb;
@@ -879,7 +826,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
           for (int i = 0; i < NI; ++i)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const int lr = 16 * i + 4 * part + e;
+              const int lr = BK_LI * i + 4 * part + e;
               float v = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
               if (i < NIM) {
                 v = (lr == j) ? a[i][e] - f : v;
@@ -892,7 +839,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
           for (int i = 0; i < NI; ++i)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const int lr = 16 * i + 4 * part + e;
+              const int lr = BK_LI * i + 4 * part + e;
               a[i][e] = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
             }
         }
@@ -904,7 +851,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
           for (int i = 0; i < NI; ++i)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-              const int lr = 16 * i + 4 * part + e;
+              const int lr = BK_LI * i + 4 * part + e;
               a[i][e] = fmaf(-fs, x[lr], a[i][e]);
               if (i < NIM) a[i][e] -= (lr == j) ? f : 0.f;
             }
@@ -912,7 +859,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
 #pragma unroll
           for (int i = 0; i < NI; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[16 * i + 4 * part + e], a[i][e]);
+            for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[BK_LI * i + 4 * part + e], a[i][e]);
         }
       }
     } else if (k == j) {
@@ -921,7 +868,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         for (int i = 0; i < NI; ++i)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int lr = 16 * i + 4 * part + e;
+            const int lr = BK_LI * i + 4 * part + e;
             if (i < NIM)
               a[i][e] = (lr > j) ? a[i][e] * inv_v0 : ((lr == j) ? rjj : a[i][e]);
             else
@@ -941,7 +888,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         for (int i = 0; i < NI; ++i)
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int lr = 16 * i + 4 * part + e;
+            const int lr = BK_LI * i + 4 * part + e;
             const float v = fmaf(-fs1, x[lr], a[i][e]) * inv_v02;
             if (i < NIM)
               a[i][e] = (lr > j + 1) ? v : ((lr == j + 1) ? rjj2 : ((lr == j) ? a[i][e] - f1 : a[i][e]));
@@ -953,7 +900,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         for (int i = 0; i < NI; ++i)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            a[i][e] = fmaf(-fs1, x[16 * i + 4 * part + e], a[i][e]) * inv_v02;
+            a[i][e] = fmaf(-fs1, x[BK_LI * i + 4 * part + e], a[i][e]) * inv_v02;
       }
     }
     if (w0) {
@@ -992,7 +939,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
     for (int i = 0; i < NI; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int lr = 16 * i + 4 * part + e;
+        const int lr = BK_LI * i + 4 * part + e;
         const int row = r0 + lr;
         if (row < n) {
           float v = a[i][e];
@@ -1020,8 +967,8 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
     for (int j = k; j < jend; ++j) {
       float s = 0.f;
       for (int l = k + part; l < j; l += BK_PARTS) s += trow[l] * Ss[l * BK_TSTR + j];
-      s += __shfl_xor(s, 1);
-      s += __shfl_xor(s, 2);
+#pragma unroll
+      for (int msk = 1; msk < BK_PARTS; msk <<= 1) s += __shfl_xor(s, msk);
       __builtin_amdgcn_wave_barrier();
       if (part == 0) trow[j] = (j == k) ? bs[j] : -bs[j] * s;
       __builtin_amdgcn_wave_barrier();
@@ -1029,38 +976,28 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   }
   __syncthreads();
   if (col) {
-    const int lead = lane & ~3;
+    const int lead = lane & ~(BK_PARTS - 1);
     for (int J = J0 + 1; 8 * J < nb; ++J) {
-      // X[c] = sum_{l=k}^{8J-1} T[k][l] S[l][8J+c]; lane part forms c = part, part+4
-      const int c0 = 8 * J + part, c1 = c0 + 4;
-      float x0a = 0.f, x0b = 0.f, x1a = 0.f, x1b = 0.f;
+      // X[c] = sum_{l=k}^{8J-1} T[k][l] S[l][8J+c]; lane part forms c = part
+      const int c0 = 8 * J + part;
+      float x0a = 0.f, x0b = 0.f;
       int l = k;
       for (; l + 1 < 8 * J; l += 2) {
-        const float t0 = trow[l], t1 = trow[l + 1];
-        x0a += t0 * Ss[l * BK_TSTR + c0];
-        x1a += t0 * Ss[l * BK_TSTR + c1];
-        x0b += t1 * Ss[(l + 1) * BK_TSTR + c0];
-        x1b += t1 * Ss[(l + 1) * BK_TSTR + c1];
+        x0a += trow[l] * Ss[l * BK_TSTR + c0];
+        x0b += trow[l + 1] * Ss[(l + 1) * BK_TSTR + c0];
       }
-      if (l < 8 * J) {
-        const float t0 = trow[l];
-        x0a += t0 * Ss[l * BK_TSTR + c0];
-        x1a += t0 * Ss[l * BK_TSTR + c1];
-      }
+      if (l < 8 * J) x0a += trow[l] * Ss[l * BK_TSTR + c0];
       // columns past nb of S were never written: keep them out of X
-      const float xa = (c0 < nb) ? x0a + x0b : 0.f, xb = (c1 < nb) ? x1a + x1b : 0.f;
-      // T[k][8J+q] = -sum_c X[c] T_JJ[c][q],  X[c] from lane lead + (c & 3)
-      float r0 = 0.f, r1 = 0.f;
+      const float xa = (c0 < nb) ? x0a + x0b : 0.f;
+      // T[k][8J+q] = -sum_c X[c] T_JJ[c][q],  X[c] from lane lead + c
+      float r0 = 0.f;
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) {
-        const float xc = __shfl((cc < 4) ? xa : xb, lead + (cc & 3));
-        const float *tjj = Ts + (8 * J + cc) * BK_TSTR + 8 * J;
-        r0 += xc * tjj[part];
-        r1 += xc * tjj[part + 4];
+        const float xc = __shfl(xa, lead + cc);
+        r0 += xc * Ts[(8 * J + cc) * BK_TSTR + 8 * J + part];
       }
       __builtin_amdgcn_wave_barrier();
       if (c0 < nb) trow[c0] = -r0;
-      if (c1 < nb) trow[c1] = -r1;
       __builtin_amdgcn_wave_barrier();
     }
   }
