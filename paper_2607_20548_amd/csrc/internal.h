@@ -4,6 +4,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <functional>
+
 #include <cstddef>
 #include <cstdint>
 
@@ -155,11 +157,18 @@ hipError_t launch_axpby_bf16(float *W, const uint16_t *X, int64_t count, float a
 // block factorizations run on stream sp and the T matrices of block pairs on
 // stream st (both joined back into s with events; st may equal sp).
 // If q_free is not null, s waits for it before Q is first written (Q may
-// still be read by work on other streams until then).
+// still be read by work on other streams until then).  If at_mid is set it
+// is called once, when the host loop over the outer blocks reaches block
+// mid_frac * (number of outer blocks) (or at the end of the factorization),
+// right after recording `mid` on s (if not null), so that the caller can
+// enqueue work that waits for that event: the factorization's later blocks
+// leave most of the GPU idle.
 size_t qr_workspace_bytes(int64_t batch, int64_t n);
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
-                                hipStream_t st, hipEvent_t q_free = nullptr);
+                                hipStream_t st, hipEvent_t q_free = nullptr,
+                                hipEvent_t mid = nullptr, float mid_frac = 0.5f,
+                                const std::function<hipError_t()> &at_mid = {});
 // dst = src^T for one n x n row-major matrix.
 hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t s);
 

@@ -527,9 +527,16 @@ constexpr int BK_WAVES = BK_THREADS / 64;
 constexpr int BK_PARTS = 8;                     // threads per column
 constexpr int BK_R = 32;                        // rows per thread
 constexpr int BK_ROWS = BK_PARTS * BK_R;        // rows per workgroup
+// Blocks with few rows take half as many rows per thread (twice the
+// workgroups): the work of each round halves while the exchange grows by P
+// items per column (measured on 14336 x 14336: faster up to about 32
+// workgroups, slower from about 40 on).
+constexpr int BK_R_SMALL = 16;
+constexpr int BK_ROWS_SMALL = BK_PARTS * BK_R_SMALL;
+constexpr int BK_SMALL_MAX_P = 32;
 constexpr int BK_LI = 4 * BK_PARTS;             // local-row stride of a thread's register groups
 constexpr int BK_MAX_P = 64;                    // workgroups per matrix (n <= 16384);
-                                                // an owner lane sums at most 8 partials
+                                                // a reader lane sums at most 16 partials
 constexpr int BK_MAX_WG = 96;                   // workgroups per launch
 constexpr unsigned BK_SPIN_LIMIT = 1u << 22;
 constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (spreads banks)
@@ -1310,11 +1317,17 @@ hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
   if (!x.L.block) return panel_phase(x, ob, s);
   const int c = (int)(ob * NB);
   const int nb = (int)std::min<int64_t>(NB, x.n - c);
-  const int P = (int)((x.n - c + BK_ROWS - 1) / BK_ROWS);
+  const int Ps = (int)((x.n - c + BK_ROWS_SMALL - 1) / BK_ROWS_SMALL);
+  const bool small = Ps <= BK_SMALL_MAX_P && Ps * x.batch <= BK_MAX_WG;
+  const int P = small ? Ps : (int)((x.n - c + BK_ROWS - 1) / BK_ROWS);
   BlockParams bp{x.At, x.sA, x.ni, c, nb, x.Tb + ob * NB * NB, x.L.sT, x.Rf, x.dsign, x.betas,
                  x.xch, P};
-  hipLaunchKernelGGL((qr_block_kernel<BK_R>), dim3((unsigned)P, (unsigned)x.batch),
-                     dim3(BK_THREADS), 0, s, bp);
+  if (small)
+    hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL>), dim3((unsigned)P, (unsigned)x.batch),
+                       dim3(BK_THREADS), 0, s, bp);
+  else
+    hipLaunchKernelGGL((qr_block_kernel<BK_R>), dim3((unsigned)P, (unsigned)x.batch),
+                       dim3(BK_THREADS), 0, s, bp);
   return hipGetLastError();
 }
 
@@ -1514,7 +1527,8 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
 
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
-                                hipStream_t st, hipEvent_t q_free) {
+                                hipStream_t st, hipEvent_t q_free, hipEvent_t mid,
+                                float mid_frac, const std::function<hipError_t()> &at_mid) {
   QrCtx x;
   x.L = qr_layout(batch, n);
   if (ws_bytes < x.L.total) return hipErrorInvalidValue;
@@ -1554,8 +1568,15 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   SOAP_TRY(t_events.get(&ev));
   SOAP_TRY(hipEventRecord(ev, sp));
   SOAP_TRY(hipStreamWaitEvent(s, ev, 0));        // block 0 factored
+  const int64_t mid_ob = (int64_t)(mid_frac * (float)nob);
+  bool mid_done = (mid == nullptr && !at_mid);
   for (int64_t ob = 0; ob < nob; ++ob) {
     const int64_t cend = std::min<int64_t>(n, (ob + 1) * NB);
+    if (!mid_done && ob >= mid_ob) {
+      if (mid) SOAP_TRY(hipEventRecord(mid, s));
+      if (at_mid) SOAP_TRY(at_mid());
+      mid_done = true;
+    }
     if (cend >= n) break;
     const int64_t cend2 = std::min<int64_t>(n, cend + NB);
     SOAP_TRY(trailing_update(x, ob, cend, cend2, s));          // near: block ob+1
@@ -1578,6 +1599,10 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     }
     SOAP_TRY(trailing_update(x, ob, cend2, n, s));              // far: the rest
     SOAP_TRY(hipStreamWaitEvent(s, ev_panel, 0));               // block ob+1 factored
+  }
+  if (!mid_done) {
+    if (mid) SOAP_TRY(hipEventRecord(mid, s));
+    if (at_mid) SOAP_TRY(at_mid());
   }
   if (np > 0) {                                                 // pair T's done
     SOAP_TRY(t_events.get(&ev));

@@ -144,6 +144,10 @@ class StageScope {
 // The T matrices of block pairs go on streams with slack: the R side's on
 // the L-side stream, the L side's on the L-side block stream.
 constexpr int N_AUX = 3;
+// Fraction of the R-side QR's outer blocks after which the rotations Q_L^T G,
+// Q_L^T M start: the factorization's later blocks leave most compute units
+// idle.
+constexpr float kRotateInFrom = 0.5f;
 // Workgroup cap of products that run beside the resident block kernels of
 // the other side's QR: 160 of the 256 compute units, leaving about 12 per XCD.
 constexpr int kSideWorkgroups = 160;
@@ -497,7 +501,7 @@ hipError_t kl_front(int64_t batch, int64_t m, int64_t n, const float *G, float *
 
 // Owns the events of one step; destroys whichever were created.
 struct StepEvents {
-  static constexpr int kCount = 5;
+  static constexpr int kCount = 7;
   hipEvent_t ev[kCount] = {};
   hipError_t create() {
     for (hipEvent_t &e : ev) {
@@ -577,7 +581,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   StepEvents evs;
   if ((e = evs.create()) != hipSuccess) return hip_fail(e, "event");
   hipEvent_t ev_fork = evs.ev[0], ev_join = evs.ev[1], ev_power = evs.ev[2];
-  hipEvent_t ev_a = evs.ev[3], ev_yr = evs.ev[4];
+  hipEvent_t ev_a = evs.ev[3], ev_yr = evs.ev[4], ev_lside = evs.ev[5], ev_mid = evs.ev[6];
   if ((e = hipEventRecord(ev_fork, s)) != hipSuccess) return hip_fail(e, "fork record");
   if ((e = hipStreamWaitEvent(sl, ev_fork, 0)) != hipSuccess) return hip_fail(e, "fork wait");
   bool defer_r = false;
@@ -661,26 +665,41 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     d.beta = beta_kron; d.batch = batch; d.max_wg = kSideWorkgroups;
     if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "KL factor R");
   }
-  {  // T_G = Q_L^T G,  T_M = Q_L^T M on the L-side stream, capped to part of the
-     // GPU: it overlaps the R-side QR, whose resident block kernels need whole
-     // compute units free.
-    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, sl);
+  if ((e = hipEventRecord(ev_lside, sl)) != hipSuccess) return hip_fail(e, "L side record");
+  // T_G = Q_L^T G,  T_M = Q_L^T M on the L side's block stream (free once the
+  // L-side QR is done), enqueued once the R-side factorization has reached
+  // its tail and capped to part of the GPU: the R-side block kernels need
+  // whole compute units free, and the far trailing updates of the first half
+  // of that factorization are on its critical path.
+  const char *rot_where = nullptr;
+  auto rotate_in_l = [&](bool after_mid) -> hipError_t {
+    hipError_t r;
+    if ((r = hipStreamWaitEvent(spl, ev_lside, 0)) != hipSuccess) { rot_where = "L side wait"; return r; }
+    if (after_mid && (r = hipStreamWaitEvent(spl, ev_mid, 0)) != hipSuccess) {
+      rot_where = "QR R mid wait";
+      return r;
+    }
+    StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, spl);
     soap::GemmDesc d;
     d.trans_a = 1; d.trans_b = 0; d.M = m; d.N = n; d.K = m;
     d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
     // T_G and T_M interleaved by rows over the T_G and T_M buffers (adjacent,
     // 2 m n floats per matrix): row 2i = T_G row i, row 2i+1 = T_M row i.
     d.C = TG; d.ldc = 2 * n; d.sC = 2 * mn; d.batch = batch; d.max_wg = kSideWorkgroups;
-    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in G");
+    if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { rot_where = "rotate in G"; return r; }
     d.B = M; d.C = TG + n;
-    if ((e = soap::launch_gemm(d, sl)) != hipSuccess) return hip_fail(e, "rotate in M");
-  }
-  if ((e = hipEventRecord(ev_join, sl)) != hipSuccess) return hip_fail(e, "join record");
+    if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { rot_where = "rotate in M"; return r; }
+    if ((r = hipEventRecord(ev_join, spl)) != hipSuccess) { rot_where = "join record"; return r; }
+    return hipSuccess;
+  };
   if (refresh) {  // Q_R = QR(A_R).Q; under KL, Q_R is written only after G Q_R has read it
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
     if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl,
-                                        kl ? ev_yr : nullptr)) != hipSuccess)
-      return hip_fail(e, "QR R");
+                                        kl ? ev_yr : nullptr, ev_mid, kRotateInFrom,
+                                        [&]() { return rotate_in_l(true); })) != hipSuccess)
+      return hip_fail(e, rot_where ? rot_where : "QR R");
+  } else if ((e = rotate_in_l(false)) != hipSuccess) {
+    return hip_fail(e, rot_where);
   }
   if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
   {  // G' = T_G Q_R, M' = T_M Q_R (one product over the interleaved rows), then Adam
