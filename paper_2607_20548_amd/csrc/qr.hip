@@ -627,6 +627,58 @@ __device__ __forceinline__ bool bk_gather(const unsigned long long *p, int strid
   return true;
 }
 
+// Lane exchanges inside the 8 lanes of a column (lanes 8q..8q+7, one half of
+// a DPP row) by DPP moves, which take no LDS round trip: bk_sum8 leaves the
+// sum of the 8 values in every lane, bk_pair4 the sums of lanes 0-3 (first)
+// and 4-7 (second), bk_bcast4 the values of lanes 3 and 7.  Additions are
+// commutative, so every lane holds bit-identical results.
+template <int CTRL>
+__device__ __forceinline__ float bk_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int DPP_XOR1 = 0xB1;         // quad_perm [1, 0, 3, 2]
+constexpr int DPP_XOR2 = 0x4E;         // quad_perm [2, 3, 0, 1]
+constexpr int DPP_LANE3 = 0xFF;        // quad_perm [3, 3, 3, 3]
+constexpr int DPP_HALF_MIRROR = 0x141; // lane i <- lane 7 - i within 8 lanes
+__device__ __forceinline__ float bk_sum4(float v) {
+  v += bk_mov<DPP_XOR1>(v);
+  return v + bk_mov<DPP_XOR2>(v);
+}
+__device__ __forceinline__ float bk_sum8(float v) {
+  v = bk_sum4(v);
+  return v + bk_mov<DPP_HALF_MIRROR>(v);
+}
+// first = sum of lanes 0-3, second = sum of lanes 4-7 (in every lane of the 8)
+__device__ __forceinline__ void bk_pair4(float v, bool low, float &first, float &second) {
+  const float q = bk_sum4(v);
+  const float o = bk_mov<DPP_HALF_MIRROR>(q);
+  first = low ? q : o;
+  second = low ? o : q;
+}
+__device__ __forceinline__ void bk_bcast4(float v, bool low, float &first, float &second) {
+  const float q = bk_mov<DPP_LANE3>(v);
+  const float o = bk_mov<DPP_HALF_MIRROR>(q);
+  first = low ? q : o;
+  second = low ? o : q;
+}
+
+// Register a[idx / 4][idx % 4] for a wave-uniform idx < 4 NQ (a compare per
+// candidate register instead of a select chain over the row indices).
+template <int NQ, int NI>
+__device__ __forceinline__ float bk_reg_get(const float (&a)[NI][4], int idx) {
+  float v = 0.f;
+#pragma unroll
+  for (int q = 0; q < 4 * NQ; ++q)
+    if (q == idx) v = a[q >> 2][q & 3];
+  return v;
+}
+template <int NQ, int NI>
+__device__ __forceinline__ void bk_reg_add(float (&a)[NI][4], int idx, float dv) {
+#pragma unroll
+  for (int q = 0; q < 4 * NQ; ++q)
+    if (q == idx) a[q >> 2][q & 3] += dv;
+}
+
 // Householder reflector of a column with diagonal value x0 and tail sum of
 // squares st (the larfg convention above): beta, 1 / v0 and the R diagonal.
 // st == 0: the column is already triangular, H = I.
@@ -639,8 +691,9 @@ __device__ __forceinline__ void bk_reflector(float x0, float st, float &bet, flo
   } else {
     const float sigma = sqrtf(x0 * x0 + st);
     const float v0 = (x0 >= 0.f) ? (x0 + sigma) : (x0 - sigma);
-    bet = 2.f * v0 * v0 / (st + v0 * v0);
-    inv_v0 = 1.f / v0;
+    // hardware reciprocals (1 ulp): these feed every column's update
+    bet = 2.f * v0 * v0 * __builtin_amdgcn_rcpf(st + v0 * v0);
+    inv_v0 = __builtin_amdgcn_rcpf(v0);
     rjj = (x0 >= 0.f) ? -sigma : sigma;
   }
 }
@@ -703,6 +756,10 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
     const int par = round & 1;
     const unsigned gen = (unsigned)(c + round + 1);   // rounds <= columns: unique per call
     const bool two = j + 1 < nb;
+    // lane part and register index (i * 4 + e) of the diagonal rows j, j+1
+    // in workgroup 0 (local row BK_LI i + 4 part + e)
+    const int pj0 = (j >> 2) & (BK_PARTS - 1), ij0 = (j / BK_LI) * 4 + (j & 3);
+    const int pj1 = ((j + 1) >> 2) & (BK_PARTS - 1), ij1 = ((j + 1) / BK_LI) * 4 + ((j + 1) & 3);
     if (k == j || (two && k == j + 1)) {
       float *dst = px[par][k - j];
 #pragma unroll
@@ -732,24 +789,15 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
           for (int e = 0; e < 4; ++e) acc2[e] += a[i][e] * y[BK_LI * i + 4 * part + e];
         ev = (acc2[0] + acc2[1]) + (acc2[2] + acc2[3]);
       }
-      if (w0) {   // values of the diagonal rows j and j+1
-#pragma unroll
-        for (int i = 0; i < NIM; ++i)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int lr = BK_LI * i + 4 * part + e;
-            av0 = (lr == j) ? a[i][e] : av0;
-            av1 = (lr == j + 1) ? a[i][e] : av1;
-          }
+      if (w0) {   // values of the diagonal rows j and j+1 (one lane each)
+        if (part == pj0) av0 = bk_reg_get<NIM>(a, ij0);
+        if (two && part == pj1) av1 = bk_reg_get<NIM>(a, ij1);
       }
     }
-#pragma unroll
-    for (int msk = 1; msk < BK_PARTS; msk <<= 1) {
-      d += __shfl_xor(d, msk);
-      ev += __shfl_xor(ev, msk);
-      av0 += __shfl_xor(av0, msk);
-      av1 += __shfl_xor(av1, msk);
-    }
+    d = bk_sum8(d);
+    ev = bk_sum8(ev);
+    av0 = bk_sum8(av0);
+    av1 = bk_sum8(av1);
     float D = d, E = ev, A = av0, B = av1;
     if (P > 1) {
       // One hop: every workgroup posts its partials, then every workgroup
@@ -758,7 +806,6 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       // a column sum the D partials of the workgroups u = part mod 4, lanes
       // 4..7 those of E; lanes 3 and 7 also fetch A and B from workgroup 0.
       const int64_t pk = (int64_t)(wave * (64 / BK_PARTS) + lane / BK_PARTS);   // position of column k
-      const int lead = lane & ~(BK_PARTS - 1);  // lane of part 0 of this column
       const int q = part >> 2, u0 = part & 3;
       if (col && (part == 0 || part == 4))
         bk_put(X + BK_XD + (((int64_t)par * 2 + q) * BK_MAX_P + g) * NB + pk, q ? ev : d, gen);
@@ -771,11 +818,9 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
                             (P - u0 + 3) / 4,
                             (!w0 && u0 == 3) ? X + BK_XA + ((int64_t)par * 2 + q) * NB + pk : nullptr,
                             gen, abort_flag, ssum, xv);
-        D = (__shfl(ssum, lead) + __shfl(ssum, lead + 1)) +
-            (__shfl(ssum, lead + 2) + __shfl(ssum, lead + 3));
-        E = (__shfl(ssum, lead + 4) + __shfl(ssum, lead + 5)) +
-            (__shfl(ssum, lead + 6) + __shfl(ssum, lead + 7));
-        const float aa = __shfl(xv, lead + 3), bb = __shfl(xv, lead + 7);
+        bk_pair4(ssum, part < 4, D, E);
+        float aa, bb;
+        bk_bcast4(xv, part < 4, aa, bb);
         if (!w0) {
           A = aa;
           B = bb;
@@ -828,46 +873,27 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         const float fp = bet2 * (ak1 + dp * inv_v02);
         const float fsp = fp * inv_v02;
         const float c1 = fs - fsp * fs1;
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int lr = BK_LI * i + 4 * part + e;
+            a[i][e] = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
+          }
+        // workgroup 0: the broadcasts are zero in rows j (x, y) and j+1 (y),
+        // where v_j = 1 and v_{j+1} = 1 instead
         if (w0) {
-#pragma unroll
-          for (int i = 0; i < NI; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int lr = BK_LI * i + 4 * part + e;
-              float v = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
-              if (i < NIM) {
-                v = (lr == j) ? a[i][e] - f : v;
-                v = (lr == j + 1) ? a[i][e] - fs * Bj - fp : v;
-              }
-              a[i][e] = v;
-            }
-        } else {
-#pragma unroll
-          for (int i = 0; i < NI; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int lr = BK_LI * i + 4 * part + e;
-              a[i][e] = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
-            }
+          if (part == pj0) bk_reg_add<NIM>(a, ij0, -f);
+          if (part == pj1) bk_reg_add<NIM>(a, ij1, -(fsp * fs1 * Bj + fp));
         }
       } else {
         // a -= f v with v = [1 at the diagonal row; x / v0 below it]; in
         // workgroup 0 the broadcast x is zero at and above the diagonal row
-        if (w0) {
 #pragma unroll
-          for (int i = 0; i < NI; ++i)
+        for (int i = 0; i < NI; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int lr = BK_LI * i + 4 * part + e;
-              a[i][e] = fmaf(-fs, x[lr], a[i][e]);
-              if (i < NIM) a[i][e] -= (lr == j) ? f : 0.f;
-            }
-        } else {
-#pragma unroll
-          for (int i = 0; i < NI; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[BK_LI * i + 4 * part + e], a[i][e]);
-        }
+          for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[BK_LI * i + 4 * part + e], a[i][e]);
+        if (w0 && part == pj0) bk_reg_add<NIM>(a, ij0, -f);   // v_j = 1 in row j
       }
     } else if (k == j) {
       if (w0) {
