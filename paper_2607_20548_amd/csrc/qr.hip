@@ -1087,14 +1087,14 @@ __global__ __launch_bounds__(256) void qr_assemble_pair_t_kernel(float *TP, int6
   }
 }
 
-// Near update, second product: W2 = T^T W with W = sum_s part[s] (the S
-// split-K partials of W = Y^T A_next, each nb x Nt row-major, summed in slice
+// Trailing update, second product: W2 = T^T W with W = sum_s part[s] (the S
+// split-K partials of W = Y^T A_trail, each nb x Nt row-major, summed in slice
 // order) and T the block's nb x nb upper-triangular factor (row-major, leading
 // dimension NB).  One workgroup per 8 columns of W2: it sums its columns of
 // the partials into LDS, stages T, and forms its 8 columns of T^T W (k in
-// increasing order).  Replaces a reduction pass and a one-tile GEMM on the
-// factorization's critical path.
-__global__ __launch_bounds__(256) void qr_near_reduce_tt_kernel(const float *__restrict__ part,
+// increasing order).  Replaces a reduction pass and a latency-bound GEMM with
+// K = nb on the factorization's critical path.
+__global__ __launch_bounds__(256) void qr_reduce_tt_kernel(const float *__restrict__ part,
                                                                 int S, int nb, int Nt,
                                                                 const float *__restrict__ T,
                                                                 int64_t sT, float *__restrict__ W2,
@@ -1411,11 +1411,14 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   g1.splitk = (Nt <= NB) ? narrow_split(nb, Nt, Kr, x.batch, x.batch * x.L.sSk)
                           : choose_splitk(nb, Nt, Kr, x.batch, MAX_SPLIT);
   g1.part = x.Sk;
-  const bool fused = Nt <= NB && g1.splitk > 1;   // the near update (critical path)
+  // split products sum their slices and form T^T W in one pass (the near
+  // update is on the critical path, and so are the far updates of the first
+  // half of a large factorization)
+  const bool fused = g1.splitk > 1;
   g1.partials_only = fused;
   SOAP_TRY(launch_gemm(g1, s));
   if (fused) {   // W2 = T^T (sum of the partials) in one pass
-    hipLaunchKernelGGL(qr_near_reduce_tt_kernel, dim3((unsigned)((Nt + 7) / 8), (unsigned)x.batch),
+    hipLaunchKernelGGL(qr_reduce_tt_kernel, dim3((unsigned)((Nt + 7) / 8), (unsigned)x.batch),
                        dim3(256), 0, s, x.Sk, g1.splitk, (int)nb, (int)Nt, Tob, x.L.sT, x.W2,
                        x.L.sWbuf);
     SOAP_TRY(hipGetLastError());
