@@ -33,6 +33,9 @@ constexpr int LDSK = BK + 4;            // padded LDS row stride in floats
 constexpr int TILE_FLOATS = 128 * LDSK;  // one operand tile in LDS
 constexpr int NTHREADS = 256;
 constexpr int SHORT_K = 512;    // products with at most this much K per slice use the rank-k kernel
+// The rank-k kernel uses the same two-slab-ahead loads as the long-K one (its
+// few slabs otherwise each wait for their loads).
+constexpr bool SHORT_PREFETCH2 = true;
 constexpr int GROUP_M = 8;
 
 
@@ -249,9 +252,9 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
   };
 
-  if constexpr (!SHORTK) {
-    // Long K: global loads run two slabs ahead of the matrix cores (two
-    // register sets), so a slab's loads have two slabs of MFMA work to land.
+  if constexpr (!SHORTK || SHORT_PREFETCH2) {
+    // Global loads run two slabs ahead of the matrix cores (two register
+    // sets), so a slab's loads have two slabs of MFMA work to land.
     SlabLoader<TA == 0, VEC> lc;
     SlabLoader<TB == 1, VEC> ld;
     auto load_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TB == 1, VEC> &xb, int kt) {
