@@ -148,6 +148,9 @@ constexpr int N_AUX = 3;
 // Q_L^T M start: the factorization's later blocks leave most compute units
 // idle.
 constexpr float kRotateInFrom = 0.5f;
+// Fraction of the R-side QR's outer blocks after which the L side's QR starts
+// when R is the larger factor.
+constexpr float kLSideFrom = 0.35f;
 // Workgroup cap of products that run beside the resident block kernels of
 // the other side's QR: 160 of the 256 compute units, leaving about 12 per XCD.
 constexpr int kSideWorkgroups = 160;
@@ -651,32 +654,50 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if ((e = hipEventRecord(ev_power, s)) != hipSuccess) return hip_fail(e, "power record");
     if ((e = hipStreamWaitEvent(sl, ev_power, 0)) != hipSuccess) return hip_fail(e, "power wait");
   }
-  if (refresh) {  // Q_L = QR(A_L).Q
-    StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
-    if ((e = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl, spl)) != hipSuccess)
-      return hip_fail(e, "QR L");
-  }
-  if (defer_r) {  // R <- bk R + (1-bk)/m Y_L^T Z_L, beside the R-side QR
-    StageScope sc(ST_KL_FACTOR_R, B * nd * (nd + 1) * md, sl);
-    soap::GemmDesc d;
-    d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
-    d.A = TG; d.lda = n; d.sA = mn; d.B = TM; d.ldb = n; d.sB = mn;
-    d.C = R; d.ldc = n; d.sC = nn; d.alpha = (float)((1.0 - (double)beta_kron) / md);
-    d.beta = beta_kron; d.batch = batch; d.max_wg = kSideWorkgroups;
-    if ((e = soap::launch_syrk_ema(d, sl)) != hipSuccess) return hip_fail(e, "KL factor R");
-  }
-  if ((e = hipEventRecord(ev_lside, sl)) != hipSuccess) return hip_fail(e, "L side record");
+  // The L side's QR, its KL factor update and the rotations Q_L^T G, Q_L^T M.
+  // When R is the larger factor (n >= 2m) they are enqueued from inside the
+  // R-side QR's host loop once it reaches a fraction of its outer blocks,
+  // right after an event recorded there: the first part of the R-side
+  // factorization has its far trailing updates on the critical path, its
+  // later blocks leave most compute units idle.  (Waits on an event recorded
+  // later in host order resolve late, hence the callback.)
+  const bool late_l = refresh && n >= 2 * m;
+  const char *side_where = nullptr;
+  auto l_side = [&](bool after_mid) -> hipError_t {
+    hipError_t r;
+    if (after_mid && (r = hipStreamWaitEvent(sl, ev_mid, 0)) != hipSuccess) {
+      side_where = "QR R mid wait";
+      return r;
+    }
+    if (refresh) {  // Q_L = QR(A_L).Q
+      StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
+      if ((r = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl,
+                                          spl)) != hipSuccess) {
+        side_where = "QR L";
+        return r;
+      }
+    }
+    if (defer_r) {  // R <- bk R + (1-bk)/m Y_L^T Z_L, beside the R-side QR
+      StageScope sc(ST_KL_FACTOR_R, B * nd * (nd + 1) * md, sl);
+      soap::GemmDesc d;
+      d.trans_a = 1; d.trans_b = 0; d.M = n; d.N = n; d.K = m;
+      d.A = TG; d.lda = n; d.sA = mn; d.B = TM; d.ldb = n; d.sB = mn;
+      d.C = R; d.ldc = n; d.sC = nn; d.alpha = (float)((1.0 - (double)beta_kron) / md);
+      d.beta = beta_kron; d.batch = batch; d.max_wg = kSideWorkgroups;
+      if ((r = soap::launch_syrk_ema(d, sl)) != hipSuccess) { side_where = "KL factor R"; return r; }
+    }
+    if ((r = hipEventRecord(ev_lside, sl)) != hipSuccess) { side_where = "L side record"; return r; }
+    return hipSuccess;
+  };
   // T_G = Q_L^T G,  T_M = Q_L^T M on the L side's block stream (free once the
-  // L-side QR is done), enqueued once the R-side factorization has reached
-  // its tail and capped to part of the GPU: the R-side block kernels need
-  // whole compute units free, and the far trailing updates of the first half
-  // of that factorization are on its critical path.
-  const char *rot_where = nullptr;
+  // L-side QR is done), capped to part of the GPU (the R-side block kernels
+  // need whole compute units free); when the L side runs early they are
+  // still held back to the R-side factorization's tail.
   auto rotate_in_l = [&](bool after_mid) -> hipError_t {
     hipError_t r;
-    if ((r = hipStreamWaitEvent(spl, ev_lside, 0)) != hipSuccess) { rot_where = "L side wait"; return r; }
+    if ((r = hipStreamWaitEvent(spl, ev_lside, 0)) != hipSuccess) { side_where = "L side wait"; return r; }
     if (after_mid && (r = hipStreamWaitEvent(spl, ev_mid, 0)) != hipSuccess) {
-      rot_where = "QR R mid wait";
+      side_where = "QR R mid wait";
       return r;
     }
     StageScope sc(ST_ROT_IN_L, B * 4.0 * md * md * nd, spl);
@@ -686,20 +707,26 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     // T_G and T_M interleaved by rows over the T_G and T_M buffers (adjacent,
     // 2 m n floats per matrix): row 2i = T_G row i, row 2i+1 = T_M row i.
     d.C = TG; d.ldc = 2 * n; d.sC = 2 * mn; d.batch = batch; d.max_wg = kSideWorkgroups;
-    if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { rot_where = "rotate in G"; return r; }
+    if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { side_where = "rotate in G"; return r; }
     d.B = M; d.C = TG + n;
-    if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { rot_where = "rotate in M"; return r; }
-    if ((r = hipEventRecord(ev_join, spl)) != hipSuccess) { rot_where = "join record"; return r; }
+    if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { side_where = "rotate in M"; return r; }
+    if ((r = hipEventRecord(ev_join, spl)) != hipSuccess) { side_where = "join record"; return r; }
     return hipSuccess;
   };
+  if (!late_l && (e = l_side(false)) != hipSuccess) return hip_fail(e, side_where);
   if (refresh) {  // Q_R = QR(A_R).Q; under KL, Q_R is written only after G Q_R has read it
     StageScope sc(ST_QR_R, B * (8.0 / 3.0) * nd * nd * nd, s);
+    auto at_mid = [&]() -> hipError_t {
+      hipError_t r;
+      if (late_l && (r = l_side(true)) != hipSuccess) return r;
+      return rotate_in_l(true);
+    };
     if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl,
-                                        kl ? ev_yr : nullptr, ev_mid, kRotateInFrom,
-                                        [&]() { return rotate_in_l(true); })) != hipSuccess)
-      return hip_fail(e, rot_where ? rot_where : "QR R");
+                                        kl ? ev_yr : nullptr, ev_mid,
+                                        late_l ? kLSideFrom : kRotateInFrom, at_mid)) != hipSuccess)
+      return hip_fail(e, side_where ? side_where : "QR R");
   } else if ((e = rotate_in_l(false)) != hipSuccess) {
-    return hip_fail(e, rot_where);
+    return hip_fail(e, side_where);
   }
   if ((e = hipStreamWaitEvent(s, ev_join, 0)) != hipSuccess) return hip_fail(e, "join wait");
   {  // G' = T_G Q_R, M' = T_M Q_R (one product over the interleaved rows), then Adam
