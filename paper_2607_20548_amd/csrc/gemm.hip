@@ -362,6 +362,20 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int col = n0 + wn * 64 + j * 32 + xl;
+        // C = alpha acc + beta C: the 16 values of C of this block are read
+        // before its stores (one memory latency per block instead of one per
+        // element); the empty asm keeps the compiler from hoisting the reads
+        // of later blocks, whose registers would cost the main loop a wave
+        // per SIMD.
+        float cv[16];
+        if (MODE == MODE_GENERAL && !P) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            cv[r] = (p.beta != 0.f && row < p.M && col < p.N) ? C[(int64_t)row * p.ldc + col] : 0.f;
+          }
+        }
+        asm volatile("" ::: "memory");
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
@@ -371,7 +385,7 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
             P[(int64_t)row * p.N + col] = acc[i][j][r];
           } else if (MODE == MODE_GENERAL) {
             float v = p.alpha * acc[i][j][r];
-            if (p.beta != 0.f) v += p.beta * C[off];
+            if (p.beta != 0.f) v += p.beta * cv[r];
             C[off] = v;
           } else if (MODE == MODE_SYRK) {
             if (row < col) continue;  // the mirror of (col,row) is written by its owner
