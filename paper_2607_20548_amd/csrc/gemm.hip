@@ -328,6 +328,69 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   // element after storing the previous one serializes 64 memory latencies).
   // Long-K products keep the register-lean element-by-element form.
   if constexpr (SHORTK) {
+   if (!P && (reinterpret_cast<uintptr_t>(C) & 15u) == 0 && (p.ldc & 3) == 0) {
+    // Rank-k updates are bound by their pass over C, so the tile goes
+    // through LDS (free after the K loop) in two halves of 64 rows and C is
+    // read and written 16 bytes per lane, all reads of a thread before its
+    // stores.
+    constexpr int SLD = BN + 4;   // padded LDS row (64 rows x 132 floats fit the 40 KB)
+    float *stage = lds;
+    const bool read_back = p.beta != 0.f;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      __syncthreads();
+      if (wm == half) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              stage[(i * 32 + 8 * (r >> 2) + 4 * h + (r & 3)) * SLD + wn * 64 + j * 32 + xl] =
+                  acc[i][j][r];
+      }
+      __syncthreads();
+      float4 cv[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int e = tid + NTHREADS * q, lrow = e >> 5, c4 = (e & 31) * 4;
+        const int row = m0 + half * 64 + lrow, col = n0 + c4;
+        cv[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (read_back && row < p.M) {
+          const float *src = C + (int64_t)row * p.ldc + col;
+          if (col + 3 < p.N) {
+            cv[q] = *reinterpret_cast<const float4 *>(src);
+          } else {
+            if (col < p.N) cv[q].x = src[0];
+            if (col + 1 < p.N) cv[q].y = src[1];
+            if (col + 2 < p.N) cv[q].z = src[2];
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int e = tid + NTHREADS * q, lrow = e >> 5, c4 = (e & 31) * 4;
+        const int row = m0 + half * 64 + lrow, col = n0 + c4;
+        if (row >= p.M) continue;
+        const float4 a = *reinterpret_cast<const float4 *>(stage + lrow * SLD + c4);
+        float4 v;
+        v.x = p.alpha * a.x + (read_back ? p.beta * cv[q].x : 0.f);
+        v.y = p.alpha * a.y + (read_back ? p.beta * cv[q].y : 0.f);
+        v.z = p.alpha * a.z + (read_back ? p.beta * cv[q].z : 0.f);
+        v.w = p.alpha * a.w + (read_back ? p.beta * cv[q].w : 0.f);
+        float *dst = C + (int64_t)row * p.ldc + col;
+        if (col + 3 < p.N) {
+          *reinterpret_cast<float4 *>(dst) = v;
+        } else {
+          if (col < p.N) dst[0] = v.x;
+          if (col + 1 < p.N) dst[1] = v.y;
+          if (col + 2 < p.N) dst[2] = v.z;
+        }
+      }
+    }
+    // a persistent launch's next tile writes the same LDS
+    if constexpr (PERSIST) __syncthreads();
+   } else {
     const bool read_back = !P && p.beta != 0.f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -356,6 +419,7 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
           }
         }
       }
+   }
   } else {
 #pragma unroll
     for (int i = 0; i < 2; ++i)
