@@ -36,6 +36,8 @@ constexpr int SHORT_K = 512;    // products with at most this much K per slice u
 // The rank-k kernel uses the same two-slab-ahead loads as the long-K one (its
 // few slabs otherwise each wait for their loads).
 constexpr bool SHORT_PREFETCH2 = true;
+// Long-K products without split-K partials also write C through LDS.
+constexpr bool STAGED_LONG_EPILOGUE = true;
 constexpr int GROUP_M = 8;
 
 
@@ -327,8 +329,10 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   // compiler cannot move a load of C above a store to C, and reading one
   // element after storing the previous one serializes 64 memory latencies).
   // Long-K products keep the register-lean element-by-element form.
-  if constexpr (SHORTK) {
+  bool staged = false;
+  if constexpr (SHORTK || (MODE == MODE_GENERAL && STAGED_LONG_EPILOGUE)) {
    if (!P && (reinterpret_cast<uintptr_t>(C) & 15u) == 0 && (p.ldc & 3) == 0) {
+    staged = true;
     // Rank-k updates are bound by their pass over C, so the tile goes
     // through LDS (free after the K loop) in two halves of 64 rows and C is
     // read and written 16 bytes per lane, all reads of a thread before its
@@ -390,7 +394,12 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
     }
     // a persistent launch's next tile writes the same LDS
     if constexpr (PERSIST) __syncthreads();
-   } else {
+   }
+  }
+  if (staged) {
+    // done
+  } else if constexpr (SHORTK) {
+   {
     const bool read_back = !P && p.beta != 0.f;
 #pragma unroll
     for (int i = 0; i < 2; ++i)
