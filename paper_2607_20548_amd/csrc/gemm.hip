@@ -330,6 +330,109 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   // element after storing the previous one serializes 64 memory latencies).
   // Long-K products keep the register-lean element-by-element form.
   bool staged = false;
+  if constexpr (MODE == MODE_SYRK && !SHORTK) {
+   if ((reinterpret_cast<uintptr_t>(C) & 15u) == 0 && (p.ldc & 3) == 0) {
+    staged = true;
+    // One triangle, mirrored, through LDS in two halves of 64 rows: the
+    // lower part (row >= col) is written as beta C + alpha acc with 16-byte
+    // reads and writes, the final values go back to LDS, and the mirror is
+    // written from the transposed half, again 16 bytes per lane (scattered
+    // 4-byte mirror stores, and a read of C after each store, otherwise).
+    constexpr int SLD = BN + 4;
+    float *stage = lds;
+    const bool read_back = p.beta != 0.f;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      __syncthreads();
+      if (wm == half) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              stage[(i * 32 + 8 * (r >> 2) + 4 * h + (r & 3)) * SLD + wn * 64 + j * 32 + xl] =
+                  acc[i][j][r];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int g4 = 0; g4 < 2; ++g4) {   // two groups of 4 (registers of the main loop)
+        float4 cv[4];
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const int q = 4 * g4 + qq;
+          const int e = tid + NTHREADS * q, lrow = e >> 5, c4 = (e & 31) * 4;
+          const int row = m0 + half * 64 + lrow, col = n0 + c4;
+          cv[qq] = make_float4(0.f, 0.f, 0.f, 0.f);
+          // only the lower triangle is read (a float4 with col <= row holds at
+          // least one element of it; the others are masked)
+          if (read_back && row < p.M && col <= row && col < p.N) {
+            const float *src = C + (int64_t)row * p.ldc + col;
+            if (col + 3 < p.N && col + 3 <= row) {
+              cv[qq] = *reinterpret_cast<const float4 *>(src);
+            } else {
+              cv[qq].x = src[0];
+              if (col + 1 < p.N && col + 1 <= row) cv[qq].y = src[1];
+              if (col + 2 < p.N && col + 2 <= row) cv[qq].z = src[2];
+              if (col + 3 < p.N && col + 3 <= row) cv[qq].w = src[3];
+            }
+          }
+        }
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+          const int q = 4 * g4 + qq;
+          const int e = tid + NTHREADS * q, lrow = e >> 5, c4 = (e & 31) * 4;
+          const int row = m0 + half * 64 + lrow, col = n0 + c4;
+          float *sp = stage + lrow * SLD + c4;
+          const float4 a = *reinterpret_cast<const float4 *>(sp);
+          float4 v;
+          v.x = p.alpha * a.x + (read_back ? p.beta * cv[qq].x : 0.f);
+          v.y = p.alpha * a.y + (read_back ? p.beta * cv[qq].y : 0.f);
+          v.z = p.alpha * a.z + (read_back ? p.beta * cv[qq].z : 0.f);
+          v.w = p.alpha * a.w + (read_back ? p.beta * cv[qq].w : 0.f);
+          *reinterpret_cast<float4 *>(sp) = v;   // final values for the mirror
+          if (row >= p.M || col > row || col >= p.N) continue;
+          float *dst = C + (int64_t)row * p.ldc + col;
+          if (col + 3 < p.N && col + 3 <= row) {
+            *reinterpret_cast<float4 *>(dst) = v;
+          } else {
+            dst[0] = v.x;
+            if (col + 1 < p.N && col + 1 <= row) dst[1] = v.y;
+            if (col + 2 < p.N && col + 2 <= row) dst[2] = v.z;
+            if (col + 3 < p.N && col + 3 <= row) dst[3] = v.w;
+          }
+        }
+        asm volatile("" ::: "memory");
+      }
+      __syncthreads();
+      // mirror: C[col][row] for row > col; thread -> (lc = output row within
+      // the tile's columns, 4 consecutive rows of this half as output columns)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int e = tid + NTHREADS * q, lc = e >> 4, r4 = (e & 15) * 4;
+        const int orow = n0 + lc, ocol = m0 + half * 64 + r4;   // C[orow][ocol] = value(ocol, orow)
+        if (orow >= p.N || ocol >= p.M) continue;
+        float4 v;
+        v.x = stage[(r4 + 0) * SLD + lc];
+        v.y = stage[(r4 + 1) * SLD + lc];
+        v.z = stage[(r4 + 2) * SLD + lc];
+        v.w = stage[(r4 + 3) * SLD + lc];
+        float *dst = C + (int64_t)orow * p.ldc + ocol;
+        // element (ocol + u, orow) of the lower triangle mirrors to here when ocol + u > orow
+        if (ocol > orow && ocol + 3 < p.M) {
+          *reinterpret_cast<float4 *>(dst) = v;
+        } else {
+          if (ocol > orow) dst[0] = v.x;
+          if (ocol + 1 > orow && ocol + 1 < p.M) dst[1] = v.y;
+          if (ocol + 2 > orow && ocol + 2 < p.M) dst[2] = v.z;
+          if (ocol + 3 > orow && ocol + 3 < p.M) dst[3] = v.w;
+        }
+      }
+    }
+    if constexpr (PERSIST) __syncthreads();
+   }
+  }
   if constexpr (SHORTK || (MODE == MODE_GENERAL && STAGED_LONG_EPILOGUE)) {
    if (!P && (reinterpret_cast<uintptr_t>(C) & 15u) == 0 && (p.ldc & 3) == 0) {
     staged = true;
