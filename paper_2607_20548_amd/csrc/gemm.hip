@@ -5,15 +5,20 @@
 // Tiling: a 256-thread workgroup (4 wave64s in a 2 x 2 arrangement) computes a
 // 128 x 128 tile of C; each wave owns a 64 x 64 sub-tile held as 2 x 2 MFMA
 // 32x32 accumulators (64 accumulation registers per lane).  K advances in slabs
-// of 16 staged through double-buffered LDS; for long K the global loads run two
-// slabs ahead in two register sets, with every load issued unconditionally at
-// a clamped address so that the waits cover exactly the slab being stored.  Both operands are kept in LDS as
+// of 16 staged through double-buffered LDS; the global loads run two slabs
+// ahead in two register sets (also for the rank-k updates, whose few slabs
+// would otherwise each wait for their loads), with every load issued
+// unconditionally at a clamped address so that the waits cover exactly the
+// slab being stored.  Both operands are kept in LDS as
 // [x][k] rows (x = output row or column, k contiguous, padded to 20 floats so
 // that 16-byte reads of 16 consecutive lanes fall in distinct banks); a lane
 // then fetches the 8 k-values it feeds to 8 consecutive MFMAs with two
 // ds_read_b128.  Within a 16-slab, lane half h of the MFMA operand carries
 // k = 8h + s at MFMA step s; A and B use the same assignment, so the sum over
 // k is complete.
+//
+// Epilogue: the tile goes through LDS (free after the K loop) so that C is read
+// and written 16 bytes per lane (see the epilogue).
 //
 // Tile order: the 8 XCDs receive workgroups round-robin, so the linear tile
 // index is remapped to give each XCD a contiguous run of tiles, and that run is
@@ -33,11 +38,6 @@ constexpr int LDSK = BK + 4;            // padded LDS row stride in floats
 constexpr int TILE_FLOATS = 128 * LDSK;  // one operand tile in LDS
 constexpr int NTHREADS = 256;
 constexpr int SHORT_K = 512;    // products with at most this much K per slice use the rank-k kernel
-// The rank-k kernel uses the same two-slab-ahead loads as the long-K one (its
-// few slabs otherwise each wait for their loads).
-constexpr bool SHORT_PREFETCH2 = true;
-// Long-K products without split-K partials also write C through LDS.
-constexpr bool STAGED_LONG_EPILOGUE = true;
 constexpr int GROUP_M = 8;
 
 
@@ -254,7 +254,7 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[i][s], fb[j][s], acc[i][j], 0, 0, 0);
   };
 
-  if constexpr (!SHORTK || SHORT_PREFETCH2) {
+  {
     // Global loads run two slabs ahead of the matrix cores (two register
     // sets), so a slab's loads have two slabs of MFMA work to land.
     SlabLoader<TA == 0, VEC> lc;
@@ -290,31 +290,6 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
     for (int kt = 0; kt < nk; kt += 2) {
       body(kt, la, lb, lc, ld);
       if (kt + 1 < nk) body(kt + 1, lc, ld, la, lb);
-    }
-  } else {
-    if (nk > 0) {
-      la.load(A, p.lda, m0, kbeg, p.M, kend, tid);
-      lb.load(B, p.ldb, n0, kbeg, p.N, kend, tid);
-      const int kvalid = min(BK, kend - kbeg);
-      la.store(buf(0, 0), tid, kvalid);
-      lb.store(buf(0, 1), tid, kvalid);
-    }
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int cur = kt & 1;
-      const bool more = kt + 1 < nk;
-      if (more) {
-        const int k0 = kbeg + (kt + 1) * BK;
-        la.load(A, p.lda, m0, k0, p.M, kend, tid);
-        lb.load(B, p.ldb, n0, k0, p.N, kend, tid);
-      }
-      compute(cur);
-      if (more) {
-        const int kvalid = min(BK, kend - (kbeg + (kt + 1) * BK));
-        la.store(buf(cur ^ 1, 0), tid, kvalid);
-        lb.store(buf(cur ^ 1, 1), tid, kvalid);
-      }
-      __syncthreads();
     }
   }
 
@@ -433,7 +408,7 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
     if constexpr (PERSIST) __syncthreads();
    }
   }
-  if constexpr (SHORTK || (MODE == MODE_GENERAL && STAGED_LONG_EPILOGUE)) {
+  if constexpr (MODE == MODE_GENERAL) {
    if (!P && (reinterpret_cast<uintptr_t>(C) & 15u) == 0 && (p.ldc & 3) == 0) {
     staged = true;
     // Rank-k updates are bound by their pass over C, so the tile goes
