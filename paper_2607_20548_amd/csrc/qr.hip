@@ -988,7 +988,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   // T by blocks of 8 columns: first every diagonal block T_JJ (rows of one
   // block are independent recurrences of at most 8 steps), then, row by row,
   //   T_IJ = -(sum_{K=I}^{J-1} T_IK S_KJ) T_JJ  for J > I.
-  // Row k belongs to the four lanes of column k; they exchange values only
+  // Row k belongs to the eight lanes of column k; they exchange values only
   // through shuffles and their own row of Ts, so no barrier is needed after
   // the diagonal blocks.
   for (int e = t; e < NB * BK_TSTR; e += BK_THREADS) Ts[e] = 0.f;
