@@ -662,16 +662,8 @@ __device__ __forceinline__ void bk_bcast4(float v, bool low, float &first, float
   second = low ? o : q;
 }
 
-// Register a[idx / 4][idx % 4] for a wave-uniform idx < 4 NQ (a compare per
+// a[idx / 4][idx % 4] += dv for a wave-uniform idx < 4 NQ (a compare per
 // candidate register instead of a select chain over the row indices).
-template <int NQ, int NI>
-__device__ __forceinline__ float bk_reg_get(const float (&a)[NI][4], int idx) {
-  float v = 0.f;
-#pragma unroll
-  for (int q = 0; q < 4 * NQ; ++q)
-    if (q == idx) v = a[q >> 2][q & 3];
-  return v;
-}
 template <int NQ, int NI>
 __device__ __forceinline__ void bk_reg_add(float (&a)[NI][4], int idx, float dv) {
 #pragma unroll
@@ -736,6 +728,19 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       }
   }
   bool alive = true;
+  // Workgroup 0 keeps a copy of its diagonal rows (local rows < NB) in Ts,
+  // unused until T is formed after the loop: Ts[k][row], rewritten after
+  // every round, so the values of the diagonal rows j, j+1 of each column are
+  // two LDS reads (not a selection among the registers).
+  auto save_diag_rows = [&]() {
+    if (w0 && col) {
+#pragma unroll
+      for (int i = 0; i < NIM; ++i)
+        *reinterpret_cast<float4 *>(Ts + k * BK_TSTR + BK_LI * i + 4 * part) =
+            make_float4(a[i][0], a[i][1], a[i][2], a[i][3]);
+    }
+  };
+  save_diag_rows();
 
   // Rounds of one or two columns.  A round broadcasts pivot column j (its
   // tail below the diagonal row j) and, if there is one, column j+1 (its tail
@@ -789,15 +794,13 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
           for (int e = 0; e < 4; ++e) acc2[e] += a[i][e] * y[BK_LI * i + 4 * part + e];
         ev = (acc2[0] + acc2[1]) + (acc2[2] + acc2[3]);
       }
-      if (w0) {   // values of the diagonal rows j and j+1 (one lane each)
-        if (part == pj0) av0 = bk_reg_get<NIM>(a, ij0);
-        if (two && part == pj1) av1 = bk_reg_get<NIM>(a, ij1);
+      if (w0) {   // values of the diagonal rows j and j+1 (every lane of the column)
+        av0 = Ts[k * BK_TSTR + j];
+        if (two) av1 = Ts[k * BK_TSTR + j + 1];
       }
     }
     d = bk_sum8(d);
     ev = bk_sum8(ev);
-    av0 = bk_sum8(av0);
-    av1 = bk_sum8(av1);
     float D = d, E = ev, A = av0, B = av1;
     if (P > 1) {
       // One hop: every workgroup posts its partials, then every workgroup
@@ -958,6 +961,9 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         }
       }
     }
+    // (not after the last round: T's formation clears Ts right after the
+    // loop, with no barrier in between)
+    if (jl + 1 < nb) save_diag_rows();
     j = jl + 1;
   }
   // Write Y (zeros above its diagonal, ones on it) and the R entries of the
