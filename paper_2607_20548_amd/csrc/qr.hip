@@ -728,6 +728,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       }
   }
   bool alive = true;
+  const bool want_r = p.Rf != nullptr;   // the triangular factor is an output
   // Workgroup 0 keeps a copy of its diagonal rows (local rows < NB) in Ts,
   // unused until T is formed after the loop: Ts[k][row], rewritten after
   // every round, so the values of the diagonal rows j, j+1 of each column are
@@ -884,8 +885,11 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
             a[i][e] = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
           }
         // workgroup 0: the broadcasts are zero in rows j (x, y) and j+1 (y),
-        // where v_j = 1 and v_{j+1} = 1 instead
-        if (w0) {
+        // where v_j = 1 and v_{j+1} = 1 instead.  These rows are R rows from
+        // now on; nothing but the triangular-factor output reads them (the
+        // later dots, broadcasts and diagonal-row values all start below
+        // row j+1), so without that output they are left as they are.
+        if (w0 && want_r) {
           if (part == pj0) bk_reg_add<NIM>(a, ij0, -f);
           if (part == pj1) bk_reg_add<NIM>(a, ij1, -(fsp * fs1 * Bj + fp));
         }
@@ -896,7 +900,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         for (int i = 0; i < NI; ++i)
 #pragma unroll
           for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[BK_LI * i + 4 * part + e], a[i][e]);
-        if (w0 && part == pj0) bk_reg_add<NIM>(a, ij0, -f);   // v_j = 1 in row j
+        if (w0 && want_r && part == pj0) bk_reg_add<NIM>(a, ij0, -f);   // v_j = 1 in row j (an R row)
       }
     } else if (k == j) {
       if (w0) {
