@@ -903,7 +903,9 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         if (w0 && want_r && part == pj0) bk_reg_add<NIM>(a, ij0, -f);   // v_j = 1 in row j (an R row)
       }
     } else if (k == j) {
-      if (w0) {
+      // (without the triangular-factor output, the rows at and above the
+      // diagonal of workgroup 0 are never read again: scaled like the rest)
+      if (w0 && want_r) {
 #pragma unroll
         for (int i = 0; i < NI; ++i)
 #pragma unroll
@@ -922,8 +924,9 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       }
     } else if (pair && k == j + 1) {
       // column j+1: H_j, then its own reflector (R entry in row j, R
-      // diagonal in row j+1, v below)
-      if (w0) {
+      // diagonal in row j+1, v below; rows up to j+1 of workgroup 0 matter
+      // only for the triangular-factor output)
+      if (w0 && want_r) {
 #pragma unroll
         for (int i = 0; i < NI; ++i)
 #pragma unroll
