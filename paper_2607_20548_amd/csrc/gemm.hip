@@ -718,6 +718,7 @@ bool vec_ok_for(const GemmDesc &d) {
 
 int choose_splitk(int64_t M, int64_t N, int64_t K, int64_t batch, int max_split) {
   const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN) * batch;
+  if (tiles <= 0) return 1;   // an empty product: nothing to split
   int64_t s = (512 + tiles - 1) / tiles;
   const int64_t kcap = K / 512;     // keep at least 512 of K per slice
   if (s > kcap) s = kcap;

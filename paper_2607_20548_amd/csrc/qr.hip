@@ -1188,6 +1188,25 @@ __global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *d
   }
 }
 
+// The first w columns of W = Y^T Q[c:, c:] for a group of w reflectors
+// starting at column c, while rows and columns c..c+w-1 of Q still hold
+// diag(d): W[i][j] = Y[j][i] d[c+j] = At[c+i][c+j] d[c+j] (i, j < w).
+// W has leading dimension ldw and batch stride sW.
+__global__ __launch_bounds__(256) void qr_q_head_kernel(float *W, int64_t ldw, int64_t sW,
+                                                        const float *At, int64_t sA,
+                                                        const float *dsign, int n, int64_t c,
+                                                        int w) {
+  const int64_t bz = blockIdx.y;
+  float *Wb = W + bz * sW;
+  const float *Ab = At + bz * sA + c * n + c;
+  const float *d = dsign + bz * n + c;
+  const int64_t ww = (int64_t)w * w;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < ww; e += (int64_t)gridDim.x * 256) {
+    const int64_t i = e / w, j = e % w;
+    Wb[i * ldw + j] = Ab[i * n + j] * d[j];
+  }
+}
+
 // dst = src^T for one n x n matrix, through 32 x 32 LDS tiles.
 __global__ __launch_bounds__(256) void transpose_kernel(float *dst, const float *src, int n) {
   __shared__ float tile[32][33];
@@ -1537,19 +1556,36 @@ hipError_t merge_t(const QrCtx &x, int lv, int64_t g, hipStream_t st) {
 
 // Q[c:, c:] -= Y (T (Y^T Q[c:, c:])) for the w reflectors stored in At rows
 // c..c+w-1 (zero above row c + their index) with T (w x w, leading dimension
-// ldt, batch stride sT).
+// ldt, batch stride sT).  The groups are applied from the last to the first,
+// so rows and columns c..c+w-1 of Q still hold diag(d) here: the first w
+// columns of W = Y^T Q[c:, c:] are Y's top w x w block scaled by d, and the
+// rest is a product over the trailing Kr - w rows and columns only.
 hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_t ldt,
                     int64_t sT, hipStream_t s) {
-  const int64_t n = x.n, Kr = n - c;
-  GemmDesc g1;  // W = Y^T Q[c:n, c:n]:  op(A)[i][k] = Y[k][i] = At[c+i][c+k]
-  g1.trans_a = 0; g1.trans_b = 0; g1.M = w; g1.N = Kr; g1.K = Kr;
-  g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
-  g1.B = x.Q + c * n + c; g1.ldb = n; g1.sB = x.sA;
-  g1.C = x.Wb; g1.ldc = Kr; g1.sC = x.L.sWbuf; g1.batch = x.batch;
-  // the partial buffer holds MAX_SPLIT slices of 2 NB x n
-  g1.splitk = choose_splitk(w, Kr, Kr, x.batch, (int)(MAX_SPLIT * 2 * NB / std::max<int64_t>(w, 2 * NB)));
-  g1.part = x.Sk;
-  SOAP_TRY(launch_gemm(g1, s));
+  const int64_t n = x.n, Kr = n - c, Kt = Kr - w;
+  {
+    const unsigned gx = (unsigned)std::min<int64_t>((w * w + 255) / 256, 1024);
+    hipLaunchKernelGGL(qr_q_head_kernel, dim3(gx, (unsigned)x.batch), dim3(256), 0, s, x.Wb, Kr,
+                       x.L.sWbuf, x.At, x.sA, x.dsign, x.ni, c, (int)w);
+    SOAP_TRY(hipGetLastError());
+  }
+  // W[:, w:] = Y[w:, :]^T Q[c+w:, c+w:]:  op(A)[i][k] = At[c+i][c+w+k]
+  // (nothing for the last group, whose Kr is w)
+  if (Kt > 0) {
+    GemmDesc g1;
+    g1.trans_a = 0; g1.trans_b = 0; g1.M = w; g1.N = Kt; g1.K = Kt;
+    g1.A = x.At + c * n + c + w; g1.lda = n; g1.sA = x.sA;
+    g1.B = x.Q + (c + w) * n + c + w; g1.ldb = n; g1.sB = x.sA;
+    g1.C = x.Wb + w; g1.ldc = Kr; g1.sC = x.L.sWbuf; g1.batch = x.batch;
+    // The partial buffer holds MAX_SPLIT slices of 2 NB x n.  A few hundred
+    // tiles of long K (the rank-1024 groups) leave a second, mostly empty
+    // round of workgroups: two K slices of half the length balance it.
+    const int g1max = (int)(MAX_SPLIT * 2 * NB / std::max<int64_t>(w, 2 * NB));
+    g1.splitk = choose_splitk(w, Kt, Kt, x.batch, g1max);
+    if (g1.splitk == 1 && g1max >= 2 && Kt >= 4096) g1.splitk = 2;
+    g1.part = x.Sk;
+    SOAP_TRY(launch_gemm(g1, s));
+  }
   GemmDesc g2;  // W2 = T W
   g2.trans_a = 0; g2.trans_b = 0; g2.M = w; g2.N = Kr; g2.K = w;
   g2.A = T; g2.lda = ldt; g2.sA = sT;
