@@ -88,6 +88,34 @@ def test_transformer_layer_shapes_sampled(shape):
     log(f"  ok {info}")
 
 
+def test_layer_shape_batched_rank1024_q_formation():
+    """Two 2048 x 8192 matrices through soap_step_batched: the R-side QR
+    (n = 8192) forms Q by rank-1024 updates, each of whose products starts
+    from the head block of W = Y^T Q taken from diag(d), for every batch
+    entry.  One step, then the sampled closed-loop checks of a second step
+    on both entries."""
+    import paper_2607_20548_amd as soap
+    from synth import gradients as sg
+    spec = next(s for s in sg.workload(4).matrices if (s.m, s.n) == (2048, 8192))
+    B, steps = 2, 2
+    log(f"batched layer shape {spec.m}x{spec.n} x{B}")
+    grads = np.stack([np.stack(list(sg.make_matrix_stream(spec, 4, steps, seed=b)))
+                      for b in range(B)], axis=1)                       # steps x B x m x n
+    W = dev(np.stack([sg.initial_weight(spec, 4, seed=b) for b in range(B)]))
+    gs = soap.SoapState(spec.m, spec.n, batch=B)
+    for t in range(1, steps):
+        gs.step(W, dev(grads[t - 1]), t, **HP)
+    pre_all = _snap(gs, W)
+    gs.step(W, dev(grads[steps - 1]), steps, **HP)
+    post_all = _snap(gs, W)
+    rng = np.random.default_rng(8192)
+    for b in range(B):
+        pre = {k: v[b] for k, v in pre_all.items()}
+        post = {k: v[b] for k, v in post_all.items()}
+        info = _sampled_step_checks(pre, post, grads[steps - 1, b].astype(np.float64), steps, rng)
+        log(f"  entry {b} ok {info}")
+
+
 def test_workload_4096_full_oracle_step():
     """One full closed-loop oracle step at 4096 x 4096 (every tensor)."""
     import oracle
