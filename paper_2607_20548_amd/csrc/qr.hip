@@ -1254,7 +1254,9 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.nq = L.np / 2;
   L.no = (n >= OCT_MIN_N) ? L.nq / 2 : 0;
   L.sWbuf = (int64_t)(L.no > 0 ? 8 : 4) * NB * n;
-  L.sSk = (int64_t)MAX_SPLIT * 2 * NB * n;
+  // Split-K partials: MAX_SPLIT slices of 2 NB x n for the trailing updates,
+  // four of 8 NB x n for the rank-1024 Q-formation products.
+  L.sSk = (int64_t)(L.no > 0 ? 32 * NB : MAX_SPLIT * 2 * NB) * n;
   L.sTP = L.np * 4 * NB * NB;
   L.sSx = L.np * 2 * NB * NB;
   L.sSkp = (int64_t)64 * NB * NB;
@@ -1577,12 +1579,13 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
     g1.A = x.At + c * n + c + w; g1.lda = n; g1.sA = x.sA;
     g1.B = x.Q + (c + w) * n + c + w; g1.ldb = n; g1.sB = x.sA;
     g1.C = x.Wb + w; g1.ldc = Kr; g1.sC = x.L.sWbuf; g1.batch = x.batch;
-    // The partial buffer holds MAX_SPLIT slices of 2 NB x n.  A few hundred
-    // tiles of long K (the rank-1024 groups) leave a second, mostly empty
-    // round of workgroups: two K slices of half the length balance it.
-    const int g1max = (int)(MAX_SPLIT * 2 * NB / std::max<int64_t>(w, 2 * NB));
+    // A few hundred tiles of long K (the rank-1024 groups) leave a last,
+    // mostly empty round of workgroups: K slices of a quarter or half the
+    // length (as many as the partial buffer holds) balance it.
+    const int g1max = (int)(x.L.sSk / n / std::max<int64_t>(w, 2 * NB));
     g1.splitk = choose_splitk(w, Kt, Kt, x.batch, g1max);
-    if (g1.splitk == 1 && g1max >= 2 && Kt >= 4096) g1.splitk = 2;
+    if (g1.splitk == 1 && g1max >= 4 && Kt >= 8192) g1.splitk = 4;
+    else if (g1.splitk == 1 && g1max >= 2 && Kt >= 4096) g1.splitk = 2;
     g1.part = x.Sk;
     SOAP_TRY(launch_gemm(g1, s));
   }
