@@ -13,7 +13,8 @@ the exact-inverse rule, the fixed point and condition number of Appendix A.3,
 and the reduction to the plain factor EMA).
 """
 from .soap_oracle import (  # noqa: F401
-    OracleState, init_state, factor_ema, householder_qr, momentum_ema, rotate_in,
+    OracleState, init_state, factor_ema, householder_qr, lapack_qr, refresh_qr, momentum_ema,
+    rotate_in,
     adam_eigenbasis, rotate_out, weight_update, bias_corrections, soap_step,
     soap_step_batched, eigenvalue_estimates, kl_factor_update, kl_factors, kl_soap_step,
     kl_soap_step_batched, refresh_due,

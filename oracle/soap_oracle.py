@@ -115,6 +115,41 @@ def householder_qr(A: np.ndarray, with_r: bool = False):
     return (Q, R) if with_r else Q
 
 
+def lapack_qr(A: np.ndarray) -> np.ndarray:
+    """Q of A = QR with non-negative diag(R) through LAPACK's blocked Householder
+    QR (dgeqrf, then dorgqr for the explicit Q: a library primitive) and the
+    same column-sign fix as householder.c (a column whose R diagonal is
+    negative is negated; a zero diagonal keeps its sign).  Same unique Q as
+    householder_qr for nonsingular A, reached by a different summation order;
+    the pins hold the two within 1e-12 of each other."""
+    from scipy.linalg import lapack
+    A = np.asfortranarray(A, dtype=np.float64)
+    n = A.shape[0]
+    if A.shape != (n, n):
+        raise ValueError("square matrices only")
+    lwork = max(1, 256 * n)
+    qr, tau, _, info = lapack.dgeqrf(A, lwork=lwork)
+    if info != 0:
+        raise RuntimeError("dgeqrf failed")
+    sgn = np.where(np.diag(qr) < 0.0, -1.0, 1.0)
+    Q, _, info = lapack.dorgqr(qr, tau, lwork=lwork, overwrite_a=True)
+    if info != 0:
+        raise RuntimeError("dorgqr failed")
+    return np.ascontiguousarray(Q * sgn[None, :])
+
+
+# Largest factor dimension whose refresh runs the textbook C Householder QR;
+# above it (its memory-bound rank-1 updates would take minutes) the refresh
+# takes LAPACK's blocked route to the same unique Q.
+TEXTBOOK_QR_MAX = 4096
+
+
+def refresh_qr(A: np.ndarray) -> np.ndarray:
+    """The eigenbasis refresh's QR(.).Q (Algorithm 2): householder_qr up to
+    TEXTBOOK_QR_MAX, lapack_qr above."""
+    return householder_qr(A) if A.shape[0] <= TEXTBOOK_QR_MAX else lapack_qr(A)
+
+
 def momentum_ema(M: np.ndarray, G: np.ndarray, beta1: float) -> np.ndarray:
     """First-moment EMA in weight space (Section 2 primer; Eq. 1 rotates m_t):
     M <- beta1 M + (1 - beta1) G."""
@@ -205,8 +240,8 @@ def _refresh_and_update(s: OracleState, G: np.ndarray, t: int, beta1: float, bet
     if FL is not None:
         AL = FL @ s.QL
         AR = FR @ s.QR
-        s.QL = householder_qr(AL)
-        s.QR = householder_qr(AR)
+        s.QL = refresh_qr(AL)
+        s.QR = refresh_qr(AR)
     s.M = momentum_ema(s.M, G, beta1)
     Gp = rotate_in(s.QL, G, s.QR)
     Mp = rotate_in(s.QL, s.M, s.QR)

@@ -5,7 +5,9 @@ wrong sign or index, a transposed operand, a misplaced EMA coefficient) fails
 at least one test:
 
 * QR: residuals, LAPACK agreement after the sign fix, closed forms (2x2,
-  diagonal, triangular, orthogonal input), rank-deficient input.
+  diagonal, triangular, orthogonal input), rank-deficient input; the
+  refresh's LAPACK route for large factors against the textbook code.
+* Products: numpy's matmul against plain triple loops.
 * Factor EMA: brute-force loops, exact symmetry, positive definiteness.
 * Rotations: the identity map and norm preservation.
 * Adam: a 1x1 closed form.
@@ -91,6 +93,71 @@ def test_qr_rank_deficient():
     assert np.linalg.norm(Q @ R - A) / np.linalg.norm(A) <= 1e-13
     assert np.linalg.norm(Q.T @ Q - np.eye(8)) <= 1e-13
     assert np.all(np.diag(R) >= 0)
+
+
+@pytest.mark.parametrize("n", [1, 2, 5, 64, 300, 1000])
+def test_lapack_route_matches_textbook_householder(n):
+    """The refresh's LAPACK route (blocked Householder, dgeqrf + dorgqr) reaches
+    the same unique Q as the unblocked textbook C code, with the same sign
+    convention, and meets the fp64 residual bars on its own."""
+    rng = np.random.default_rng(200 + n)
+    A = rng.standard_normal((n, n)) + 2 * np.eye(n)
+    Ql = oracle.lapack_qr(A)
+    assert rel(Ql, oracle.householder_qr(A)) <= 1e-12
+    assert np.linalg.norm(Ql.T @ Ql - np.eye(n)) / np.sqrt(n) <= 1e-12
+    R = Ql.T @ A
+    assert np.linalg.norm(Ql @ np.triu(R) - A) / np.linalg.norm(A) <= 1e-12
+    assert np.all(np.diag(R) >= -1e-12 * np.linalg.norm(A))
+
+
+def test_lapack_route_closed_forms():
+    for a, b, c, d in [(3.0, 1.0, 4.0, 2.0), (-1.0, 2.0, 0.5, -3.0)]:
+        A = np.array([[a, b], [c, d]])
+        r = np.hypot(a, c)
+        Q = oracle.lapack_qr(A)
+        assert np.allclose(Q[:, 0], np.array([a, c]) / r, atol=1e-15, rtol=0)
+        assert np.allclose(Q[:, 1], np.array([-c, a]) / r * np.sign(a * d - b * c),
+                           atol=1e-15, rtol=0)
+    assert np.array_equal(oracle.lapack_qr(np.diag([3.0, 1e-3, 7.0])), np.eye(3))
+    assert np.array_equal(oracle.lapack_qr(np.diag([2.0, -1.0, 3.0])), np.diag([1.0, -1.0, 1.0]))
+
+
+def test_refresh_takes_the_textbook_route_up_to_its_limit(monkeypatch):
+    rng = np.random.default_rng(11)
+    A = rng.standard_normal((50, 50)) + 3 * np.eye(50)
+    calls = []
+    monkeypatch.setattr(so, "householder_qr", lambda X: calls.append("textbook") or np.eye(50))
+    monkeypatch.setattr(so, "lapack_qr", lambda X: calls.append("lapack") or np.eye(50))
+    so.refresh_qr(A)
+    monkeypatch.setattr(so, "TEXTBOOK_QR_MAX", 49)
+    so.refresh_qr(A)
+    assert calls == ["textbook", "lapack"]
+
+
+def test_matrix_products_against_naive_loops():
+    """The oracle's products (numpy's matmul, a library primitive) against
+    plain triple loops: the power product F Q, both rotations, and the
+    factor products G G^T, G^T G."""
+    rng = np.random.default_rng(12)
+    m, n = 5, 7
+    G = rng.standard_normal((m, n))
+    QL = np.linalg.qr(rng.standard_normal((m, m)))[0]
+    QR = np.linalg.qr(rng.standard_normal((n, n)))[0]
+    S = rng.standard_normal((n, n))
+    F = S + S.T
+
+    def mm(A, B):
+        return np.array([[sum(A[i][k] * B[k][j] for k in range(len(B)))
+                          for j in range(len(B[0]))] for i in range(len(A))])
+
+    def tr(A):
+        return [list(r) for r in zip(*A)]
+
+    assert np.max(np.abs(F @ QR - mm(F, QR))) <= 1e-13
+    assert np.max(np.abs(oracle.rotate_in(QL, G, QR) - mm(mm(tr(QL), G), QR))) <= 1e-13
+    assert np.max(np.abs(oracle.rotate_out(QL, G, QR) - mm(mm(QL, G), tr(QR)))) <= 1e-13
+    assert np.max(np.abs(oracle.factor_ema(np.zeros((m, m)), G, 0.0) - mm(G, tr(G)))) <= 1e-13
+    assert np.max(np.abs(oracle.factor_ema(np.zeros((n, n)), G.T, 0.0) - mm(tr(G), G))) <= 1e-13
 
 
 # ------------------------------------------------------------------ factor EMA
