@@ -26,9 +26,16 @@
  *    Batched tensors are contiguous [batch][rows][cols].
  *  - Matrix pointers are DEVICE pointers (hipMalloc or torch device memory),
  *    16-byte aligned.  The caller owns every buffer, including the workspace;
- *    the library never allocates or frees device memory and keeps no state
- *    between calls except the thread-local error string (and, only while
- *    soap_timing_enable(1) is in force, a pool of HIP events).
+ *    the library never allocates or frees device memory.  It keeps no
+ *    optimizer state between calls.  It does keep, until the process ends:
+ *    the thread-local error string; per device, three internal streams of
+ *    default priority (created on first use: the m x m factor's chain and
+ *    the block factorizations of both QRs run on them, forked from and
+ *    joined back into the caller's stream with events); per host thread, a
+ *    pool of up to 4096 HIP events for those forks and joins; per device, the
+ *    result of one occupancy query (how many QR block workgroups the device
+ *    holds at once); and, while soap_timing_enable(1) is in force, timing
+ *    events.
  *  - Work is enqueued on `stream` (0 = the null stream) and the call returns
  *    without synchronising.  Validation happens on the host before anything is
  *    enqueued: on failure nothing is enqueued, a negative soap_status is
@@ -36,7 +43,9 @@
  *    reported as SOAP_ERR_HIP; a device fault surfaces at the caller's next
  *    synchronisation.  NaN/Inf in the inputs propagate and are not checked.
  *  - Calls on different streams are safe when their buffers and workspaces are
- *    disjoint.  No C++ exception crosses this boundary.
+ *    disjoint (several steps running at once may make a QR give up and keep
+ *    its old basis: see soap_workspace_status).  No C++ exception crosses
+ *    this boundary.
  *  - Every dimension must be in [1, SOAP_MAX_DIM].
  */
 #ifndef SOAP_MI355X_H
@@ -61,7 +70,8 @@ typedef enum {
   SOAP_ERR_ALIGN = -5,      /* a pointer is not 16-byte aligned                  */
   SOAP_ERR_ALIAS = -6,      /* grad overlaps a buffer the call writes, or two
                                written buffers overlap                           */
-  SOAP_ERR_HIP = -7         /* a HIP runtime call failed                         */
+  SOAP_ERR_HIP = -7,        /* a HIP runtime call failed                         */
+  SOAP_ERR_QR_GAVE_UP = -8  /* soap_workspace_status: a QR's bounded wait gave up  */
 } soap_status;
 
 /* Step flags (bitwise or):
@@ -82,6 +92,10 @@ enum {
 };
 
 #define SOAP_MAX_DIM 16384
+
+/* Bits of a step's status word (soap_workspace_status): the QR of the m x m
+ * factor (or soap_qr_f32's matrix) / of the n x n factor gave up. */
+enum { SOAP_STATUS_QR_L = 1u << 0, SOAP_STATUS_QR_R = 1u << 1 };
 
 /* Bytes of device workspace soap_step / soap_step_batched need for `batch`
  * matrices of shape m x n (batch = 1 for soap_step).  Returns 0 for an invalid
@@ -184,12 +198,53 @@ int soap_muon_step_batched(int64_t batch, float *param, const float *grad, float
  * Valid until the next call on the same thread. */
 const char *soap_last_error(void);
 
+/* Device-side outcome of the last step (soap_step, soap_kl_step and their
+ * batched forms) or soap_qr_f32 call enqueued with `workspace`.
+ *
+ * The QR factors each 128-column block with one launch whose workgroups must
+ * all be resident at once (they exchange partial sums through memory); the
+ * library sizes these launches from an occupancy query, but other work on the
+ * GPU (another process, communication kernels that wait for peers, concurrent
+ * steps on other streams) can hold the compute units they need.  Their waits
+ * are therefore bounded: if one gives up, that factor's factorization is
+ * marked failed, its eigenbasis (Q_L or Q_R; soap_qr_f32's Q) is LEFT AS IT
+ * WAS ON ENTRY, and the rest of the step runs with it, exactly as a step with
+ * SOAP_FLAG_SKIP_REFRESH would for that side.  The step sets the bit of that
+ * side in the status word at offset 0 of its workspace; every step clears the
+ * word when it starts.
+ *
+ * This call waits for `stream` (a host synchronisation), reads the word into
+ * *status (if not NULL) and returns SOAP_OK when it is 0, SOAP_ERR_QR_GAVE_UP
+ * when a SOAP_STATUS_QR_* bit is set (soap_last_error() names the side), or
+ * SOAP_ERR_WORKSPACE when it holds other bits (not such a workspace). */
+int soap_workspace_status(const void *workspace, uint32_t *status, hipStream_t stream);
+
+/* Byte offset, inside the workspace of soap_step / soap_step_batched /
+ * soap_kl_step(_batched), of the eigenbasis update N = (M'/c1) /
+ * (sqrt(V/c2) + eps) that the last step wrote there (fp32, [batch][m][n]);
+ * valid once that step's stream has been synchronised and until the next call
+ * with the workspace.  For diagnostics; 0 for an invalid shape. */
+size_t soap_workspace_update_offset(int64_t batch, int64_t m, int64_t n);
+
+/* TEST HOOK, not for production use.  Every later QR (of a step or of
+ * soap_qr_f32) whose SOAP_STATUS_QR_* bit is in `mask` starts with the abort
+ * flags of its resident block factorizations raised, so that each of their
+ * bounded waits gives up at once and every kernel still exits normally: the
+ * give-up path above, on demand.  mask = 0 restores normal operation.  Only
+ * QRs that take the resident block path are affected (matrices whose
+ * factorization runs in more than one workgroup per block; batches that the
+ * library factors with its panel path have no waits).  Returns
+ * SOAP_ERR_HPARAM for other bits. */
+int soap_test_force_qr_give_up(uint32_t mask);
+
 /* ---- stage entry points (used by the tests to check each kernel alone) ---- */
 
 /* Eigenbasis refresh QR (Algorithm 2, "QR(.).Q"): A = Q Rf for one n x n
  * matrix, with diag(Rf) >= 0, by blocked Householder.  A is read only; Q (n x n)
  * receives the Q factor; Rf (n x n, may be NULL) the triangular factor with its
- * strict lower part zeroed. */
+ * strict lower part zeroed.  If the factorization gives up (see
+ * soap_workspace_status, bit SOAP_STATUS_QR_L) Q is left as it was on entry
+ * and Rf is undefined. */
 size_t soap_qr_workspace_bytes(int64_t n);
 int soap_qr_f32(int64_t n, const float *A, float *Q, float *Rf, void *workspace,
                 size_t workspace_bytes, hipStream_t stream);

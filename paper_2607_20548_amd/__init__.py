@@ -25,6 +25,9 @@ SOAP_ERR_WORKSPACE = -4
 SOAP_ERR_ALIGN = -5
 SOAP_ERR_ALIAS = -6
 SOAP_ERR_HIP = -7
+SOAP_ERR_QR_GAVE_UP = -8
+SOAP_STATUS_QR_L = 1
+SOAP_STATUS_QR_R = 2
 SOAP_FLAG_NO_BIAS_CORRECTION = 1
 SOAP_FLAG_SKIP_REFRESH = 2
 SOAP_FLAG_STALE_REFRESH = 4
@@ -38,7 +41,8 @@ EXPORTED = [
     "soap_timing_stage_name", "soap_timing_collect", "soap_timing_reset", "soap_timing_get",
     "soap_kl_workspace_bytes", "soap_kl_step", "soap_kl_step_batched",
     "soap_kl_factors_workspace_bytes", "soap_kl_factors_f32", "soap_muon_workspace_bytes",
-    "soap_muon_step", "soap_muon_step_batched",
+    "soap_muon_step", "soap_muon_step_batched", "soap_workspace_status",
+    "soap_workspace_update_offset", "soap_test_force_qr_give_up",
 ]
 
 
@@ -87,6 +91,9 @@ def lib() -> ctypes.CDLL:
         "soap_muon_step_batched": (_INT, [_I64, _P, _P, _P, _I64, _I64, _F, _F, _F, _F, _P, _I64,
                                           _U32, _P, _SZ, _P]),
         "soap_last_error": (ctypes.c_char_p, []),
+        "soap_workspace_status": (_INT, [_P, ctypes.POINTER(ctypes.c_uint32), _P]),
+        "soap_workspace_update_offset": (_SZ, [_I64, _I64, _I64]),
+        "soap_test_force_qr_give_up": (_INT, [_U32]),
         "soap_qr_workspace_bytes": (_SZ, [_I64]),
         "soap_qr_f32": (_INT, [_I64, _P, _P, _P, _P, _SZ, _P]),
         "soap_gemm_f32": (_INT, [_INT, _INT, _I64, _I64, _I64, _F, _P, _I64, _P, _I64, _F, _P,
@@ -148,6 +155,25 @@ def soap_last_error() -> str:
 
 def soap_workspace_bytes(batch: int, m: int, n: int) -> int:
     return lib().soap_workspace_bytes(batch, m, n)
+
+
+def soap_workspace_status(workspace, stream=None):
+    """Waits for the stream and returns (status code, status word) of the last
+    step or QR enqueued with `workspace`: (SOAP_OK, 0) or
+    (SOAP_ERR_QR_GAVE_UP, SOAP_STATUS_QR_* bits).  Other codes raise."""
+    word = ctypes.c_uint32(0)
+    rc = lib().soap_workspace_status(_ptr(workspace), ctypes.byref(word), _stream(stream))
+    if rc not in (SOAP_OK, SOAP_ERR_QR_GAVE_UP):
+        _check(rc)
+    return rc, word.value
+
+
+def soap_workspace_update_offset(batch: int, m: int, n: int) -> int:
+    return lib().soap_workspace_update_offset(batch, m, n)
+
+
+def soap_test_force_qr_give_up(mask: int) -> None:
+    _check(lib().soap_test_force_qr_give_up(mask))
 
 
 def soap_qr_workspace_bytes(n: int) -> int:
@@ -303,6 +329,19 @@ class SoapState:
         self.ws_bytes = (soap_kl_workspace_bytes if kl else soap_workspace_bytes)(batch, m, n)
         self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         soap_init_state(batch, m, n, self.L, self.R, self.Q_L, self.Q_R, self.M, self.V)
+
+    def status(self, stream=None):
+        """(status code, SOAP_STATUS_QR_* bits) of the last step (synchronises)."""
+        return soap_workspace_status(self.workspace, stream)
+
+    def update(self):
+        """The eigenbasis update N of the last step, a view into the workspace
+        ([batch,] m x n fp32; valid until the next step)."""
+        import torch
+        off = soap_workspace_update_offset(self.batch, self.m, self.n)
+        count = self.batch * self.m * self.n
+        view = self.workspace[off:off + 4 * count].view(torch.float32)
+        return view.view((self.batch, self.m, self.n) if self.batch > 1 else (self.m, self.n))
 
     def step(self, param, grad, t: int, beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3,
              weight_decay=0.1, flags=0, stream=None, beta_kron=None, refresh_every=1,

@@ -58,6 +58,8 @@ struct KParams {
   int tiles_m, tiles_n, ntiles;
   int kslice;       // K extent of one split-K slice (multiple of BK); = K when not split
   float *part;      // split-K partials, or nullptr
+  const unsigned *skip;   // batch entry b is skipped when skip[b * sSkip] != 0 (or nullptr)
+  int64_t sSkip;
 };
 
 // Loads one operand slab of 128 x-rows by BK k-values into registers.
@@ -205,6 +207,7 @@ template <int TA, int TB, int VEC, int MODE, int TAG, int MINB, bool PERSIST = f
 __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   constexpr bool SHORTK = MINB > 1;
   __shared__ __attribute__((aligned(16))) float lds[2 * 2 * TILE_FLOATS];
+  if (p.skip && p.skip[(int64_t)blockIdx.z * p.sSkip] != 0u) return;
 
   // One tile per workgroup; PERSIST: a loop over tiles when the grid was
   // capped (the caller limited the compute units this product may hold).
@@ -565,8 +568,10 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
 // C = alpha * sum_s part[s] + beta * C, slices summed in index order.
 __global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ part, int S,
                                                      int M, int N, float *C, int64_t ldc,
-                                                     int64_t sC, float alpha, float beta) {
+                                                     int64_t sC, float alpha, float beta,
+                                                     const unsigned *skip, int64_t sSkip) {
   const int64_t bz = blockIdx.y;
+  if (skip && skip[bz * sSkip] != 0u) return;
   const int64_t mn = (int64_t)M * N;
   const float *pb = part + bz * S * mn;
   float *Cb = C + bz * sC;
@@ -671,7 +676,7 @@ hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) 
   int64_t mn = d.M * d.N;
   unsigned gx = (unsigned)std::min<int64_t>((mn + 255) / 256, 2048);
   hipLaunchKernelGGL(splitk_reduce, dim3(gx, (unsigned)d.batch), dim3(256), 0, s, kp.part, S,
-                     kp.M, kp.N, d.C, d.ldc, d.sC, d.alpha, d.beta);
+                     kp.M, kp.N, d.C, d.ldc, d.sC, d.alpha, d.beta, kp.skip, kp.sSkip);
   return hipGetLastError();
 }
 
@@ -687,6 +692,8 @@ KParams make_params(const GemmDesc &d) {
   kp.ntiles = kp.tiles_m * kp.tiles_n;
   kp.kslice = (int)d.K;
   kp.part = nullptr;
+  kp.skip = d.skip;
+  kp.sSkip = d.sSkip;
   if (d.splitk > 1 && d.part) {
     const int64_t per = (d.K + d.splitk - 1) / d.splitk;
     kp.kslice = (int)(((per + BK - 1) / BK) * BK);

@@ -42,6 +42,10 @@ struct GemmDesc {
   // are launched and each loops over tiles: the product then holds only part
   // of the compute units, leaving the rest to concurrent work.
   int max_wg = 0;
+  // If set, the product of batch entry b is not computed (C, and the split-K
+  // partials, are left untouched) when skip[b * sSkip] != 0 at launch time.
+  const unsigned *skip = nullptr;
+  int64_t sSkip = 0;
 };
 
 // A split-K factor that gives at least ~2 workgroups per CU for a product with
@@ -163,10 +167,22 @@ hipError_t launch_axpby_bf16(float *W, const uint16_t *X, int64_t count, float a
 // right after recording `mid` on s (if not null), so that the caller can
 // enqueue work that waits for that event: the factorization's later blocks
 // leave most of the GPU idle.
+//
+// Resident block factorizations wait for each other's partial sums with
+// bounded waits.  If a wait gives up (the launch's workgroups could not all
+// be resident, e.g. because other work held the compute units), the matrix's
+// factorization is marked failed: `status_bit` is or-ed into *status (if
+// status is not null), and Q (and Rf) of that matrix are left as they were
+// on entry -- the Q formation is skipped for it.  qr_force_give_up(mask)
+// makes every later call whose status_bit is in `mask` start with its
+// matrices' abort flags raised (a test hook: every bounded wait then ends at
+// once and the kernels exit normally).
 size_t qr_workspace_bytes(int64_t batch, int64_t n);
+void qr_force_give_up(unsigned mask);
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
-                                hipStream_t st, hipEvent_t q_free = nullptr,
+                                hipStream_t st, unsigned *status, unsigned status_bit,
+                                hipEvent_t q_free = nullptr,
                                 hipEvent_t mid = nullptr, float mid_frac = 0.5f,
                                 const std::function<hipError_t()> &at_mid = {});
 // dst = src^T for one n x n row-major matrix.

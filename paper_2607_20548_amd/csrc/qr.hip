@@ -44,6 +44,8 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 #include <vector>
 
 namespace soap {
@@ -519,9 +521,13 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
 // by blocks of 8 columns (the diagonal blocks by this recurrence, the others
 // by T_IJ = -(sum_{K=I}^{J-1} T_IK S_KJ) T_JJ).
 // The launch needs all of its workgroups resident at once; the host limits it
-// to BK_MAX_WG workgroups.  Waits are bounded: one that exceeds BK_SPIN_LIMIT
-// polls raises a per-matrix abort flag, after which every wait returns at
-// once and the block is written as NaN, so the kernel always ends.
+// to BK_MAX_WG workgroups and to what the device can hold at once (an
+// occupancy query).  Waits are bounded: one that exceeds BK_SPIN_LIMIT polls
+// raises a per-matrix abort flag, after which every wait returns at once and
+// the block is written as NaN, so the kernel always ends.  A workgroup that
+// saw the abort marks the matrix's factorization failed (the Q formation
+// then leaves that matrix's Q as it was) and or-s the caller's status bit
+// into its status word.
 constexpr int BK_THREADS = 1024;
 constexpr int BK_WAVES = BK_THREADS / 64;
 constexpr int BK_PARTS = 8;                     // threads per column
@@ -546,10 +552,12 @@ constexpr float BK_PAIR_TAU = 0.0625f;
 // exchange area per matrix, in 64-bit items, all by round parity: partials
 // [2][2 sums][BK_MAX_P][NB] and values of workgroup 0 in the diagonal rows j,
 // j+1 [2][2][NB], column k at position (k mod 8) * 16 + k / 8 (the columns of
-// one wave are contiguous), then the abort flag
+// one wave are contiguous), then the abort flag and the failed flag (the low
+// 32 bits of one item each)
 constexpr int64_t BK_XD = 0;
 constexpr int64_t BK_XA = 2 * 2 * (int64_t)BK_MAX_P * NB;
 constexpr int64_t BK_XABORT = BK_XA + 2 * 2 * NB;
+constexpr int64_t BK_XFAILED = BK_XABORT + 1;
 constexpr int64_t BK_XSTRIDE = BK_XABORT + 32;
 
 struct BlockParams {
@@ -562,6 +570,8 @@ struct BlockParams {
   float *dsign, *beta;       // n per matrix
   unsigned long long *xch;   // exchange area, BK_XSTRIDE items per matrix (zeroed per call)
   int P;                     // workgroups per matrix
+  unsigned *status;          // caller's status word (or nullptr) ...
+  unsigned status_bit;       // ... and the bit a give-up or-s into it
 };
 
 __device__ __forceinline__ void bk_put(unsigned long long *p, float v, unsigned gen) {
@@ -977,6 +987,12 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   // block's diagonal rows.  An aborted exchange poisons the block.
   const bool bad =
       P > 1 && __hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+  if (bad && t == 0) {   // the factorization of this matrix failed: no Q is formed from it
+    __hip_atomic_store(reinterpret_cast<unsigned *>(X + BK_XFAILED), 1u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    if (p.status)
+      __hip_atomic_fetch_or(p.status, p.status_bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   const float nan = __builtin_nanf("");
   if (col) {
     float *dst = At + (unsigned)(c + k) * un;
@@ -1177,8 +1193,10 @@ __global__ __launch_bounds__(256) void qr_reduce_tt_kernel(const float *__restri
 
 // Q <- diag(d) for each matrix of the batch.
 __global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *dsign, int n,
-                                                        int64_t sA) {
+                                                        int64_t sA, const unsigned *skip,
+                                                        int64_t sSkip) {
   const int64_t bz = blockIdx.y;
+  if (skip && skip[bz * sSkip] != 0u) return;   // failed factorization: Q is kept
   float *Qb = Q + bz * sA;
   const float *d = dsign + bz * n;
   const int64_t nn = (int64_t)n * n;
@@ -1195,8 +1213,10 @@ __global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *d
 __global__ __launch_bounds__(256) void qr_q_head_kernel(float *W, int64_t ldw, int64_t sW,
                                                         const float *At, int64_t sA,
                                                         const float *dsign, int n, int64_t c,
-                                                        int w) {
+                                                        int w, const unsigned *skip,
+                                                        int64_t sSkip) {
   const int64_t bz = blockIdx.y;
+  if (skip && skip[bz * sSkip] != 0u) return;
   float *Wb = W + bz * sW;
   const float *Ab = At + bz * sA + c * n + c;
   const float *d = dsign + bz * n + c;
@@ -1205,6 +1225,14 @@ __global__ __launch_bounds__(256) void qr_q_head_kernel(float *W, int64_t ldw, i
     const int64_t i = e / w, j = e % w;
     Wb[i * ldw + j] = Ab[i * n + j] * d[j];
   }
+}
+
+// Raises the abort flag of each of `batch` exchange areas (the forced
+// give-up of qr_force_give_up).
+__global__ __launch_bounds__(64) void qr_raise_abort_kernel(unsigned long long *xch, int64_t batch) {
+  for (int64_t b = blockIdx.x * 64 + threadIdx.x; b < batch; b += (int64_t)gridDim.x * 64)
+    __hip_atomic_store(reinterpret_cast<unsigned *>(xch + b * BK_XSTRIDE + BK_XABORT), 1u,
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // dst = src^T for one n x n matrix, through 32 x 32 LDS tiles.
@@ -1354,6 +1382,11 @@ struct QrCtx {
   int64_t batch, n, sA;
   int ni;
   QrLayout L;
+  int cap_small;             // workgroups a small-R block launch may use
+  const unsigned *skip;      // per-matrix failed flags (stride sSkip words), or nullptr
+  int64_t sSkip;
+  unsigned *status;
+  unsigned status_bit;
   float *Tb, *Wb, *W2, *Sk, *Pt, *Wi, *dsign, *betas;
   unsigned *cnt;
   unsigned long long *xch;
@@ -1378,10 +1411,10 @@ hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
   const int c = (int)(ob * NB);
   const int nb = (int)std::min<int64_t>(NB, x.n - c);
   const int Ps = (int)((x.n - c + BK_ROWS_SMALL - 1) / BK_ROWS_SMALL);
-  const bool small = Ps <= BK_SMALL_MAX_P && Ps * x.batch <= BK_MAX_WG;
+  const bool small = Ps <= BK_SMALL_MAX_P && Ps * x.batch <= x.cap_small;
   const int P = small ? Ps : (int)((x.n - c + BK_ROWS - 1) / BK_ROWS);
   BlockParams bp{x.At, x.sA, x.ni, c, nb, x.Tb + ob * NB * NB, x.L.sT, x.Rf, x.dsign, x.betas,
-                 x.xch, P};
+                 x.xch, P, x.status, x.status_bit};
   if (small)
     hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL>), dim3((unsigned)P, (unsigned)x.batch),
                        dim3(BK_THREADS), 0, s, bp);
@@ -1568,7 +1601,7 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
   {
     const unsigned gx = (unsigned)std::min<int64_t>((w * w + 255) / 256, 1024);
     hipLaunchKernelGGL(qr_q_head_kernel, dim3(gx, (unsigned)x.batch), dim3(256), 0, s, x.Wb, Kr,
-                       x.L.sWbuf, x.At, x.sA, x.dsign, x.ni, c, (int)w);
+                       x.L.sWbuf, x.At, x.sA, x.dsign, x.ni, c, (int)w, x.skip, x.sSkip);
     SOAP_TRY(hipGetLastError());
   }
   // W[:, w:] = Y[w:, :]^T Q[c+w:, c+w:]:  op(A)[i][k] = At[c+i][c+w+k]
@@ -1587,6 +1620,7 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
     if (g1.splitk == 1 && g1max >= 4 && Kt >= 8192) g1.splitk = 4;
     else if (g1.splitk == 1 && g1max >= 2 && Kt >= 4096) g1.splitk = 2;
     g1.part = x.Sk;
+    g1.skip = x.skip; g1.sSkip = x.sSkip;
     SOAP_TRY(launch_gemm(g1, s));
   }
   GemmDesc g2;  // W2 = T W
@@ -1594,6 +1628,7 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
   g2.A = T; g2.lda = ldt; g2.sA = sT;
   g2.B = x.Wb; g2.ldb = Kr; g2.sB = x.L.sWbuf;
   g2.C = x.W2; g2.ldc = Kr; g2.sC = x.L.sWbuf; g2.batch = x.batch;
+  g2.skip = x.skip; g2.sSkip = x.sSkip;
   SOAP_TRY(launch_gemm(g2, s));
   GemmDesc g3;  // Q[c:n, c:n] -= Y W2:  op(A)[k][i] = Y[k][i] = At[c+i][c+k]
   g3.trans_a = 1; g3.trans_b = 0; g3.M = Kr; g3.N = Kr; g3.K = w;
@@ -1601,18 +1636,66 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
   g3.B = x.W2; g3.ldb = Kr; g3.sB = x.L.sWbuf;
   g3.C = x.Q + c * n + c; g3.ldc = n; g3.sC = x.sA;
   g3.alpha = -1.f; g3.beta = 1.f; g3.batch = x.batch;
+  g3.skip = x.skip; g3.sSkip = x.sSkip;
   return launch_gemm(g3, s);
+}
+
+std::atomic<unsigned> g_force_give_up{0};
+
+// Workgroups of one block-kernel launch (R rows per thread) that the current
+// device holds at once, halved: the two factors' QRs of a step may run
+// together.  Asked once per device and kernel.
+int resident_cap(bool small, hipError_t *err) {
+  static std::mutex mu;
+  static int cap[64][2] = {};
+  int dev = 0;
+  if ((*err = hipGetDevice(&dev)) != hipSuccess) return 0;
+  if (dev < 0 || dev >= 64) {
+    *err = hipErrorInvalidDevice;
+    return 0;
+  }
+  std::lock_guard<std::mutex> g(mu);
+  int &c = cap[dev][small ? 1 : 0];
+  if (c == 0) {
+    int per_cu = 0, cus = 0;
+    *err = small ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                       &per_cu, qr_block_kernel<BK_R_SMALL>, BK_THREADS, 0)
+                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, qr_block_kernel<BK_R>,
+                                                                BK_THREADS, 0);
+    if (*err != hipSuccess) return 0;
+    if ((*err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) !=
+        hipSuccess)
+      return 0;
+    c = std::max(1, per_cu * cus / 2);
+  }
+  return c;
 }
 
 }  // namespace
 
+void qr_force_give_up(unsigned mask) { g_force_give_up.store(mask); }
+
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
-                                hipStream_t st, hipEvent_t q_free, hipEvent_t mid,
-                                float mid_frac, const std::function<hipError_t()> &at_mid) {
+                                hipStream_t st, unsigned *status, unsigned status_bit,
+                                hipEvent_t q_free, hipEvent_t mid, float mid_frac,
+                                const std::function<hipError_t()> &at_mid) {
   QrCtx x;
   x.L = qr_layout(batch, n);
   if (ws_bytes < x.L.total) return hipErrorInvalidValue;
+  x.cap_small = BK_MAX_WG;
+  if (x.L.block) {   // resident blocks only where the device holds them all at once
+    hipError_t err = hipSuccess;
+    const int cap_big = resident_cap(false, &err);
+    if (err != hipSuccess) return err;
+    const int cap_small = resident_cap(true, &err);
+    if (err != hipSuccess) return err;
+    const int64_t P0 = (n + BK_ROWS - 1) / BK_ROWS;
+    x.L.block = P0 * batch <= std::min(BK_MAX_WG, cap_big);
+    x.cap_small = std::min(BK_MAX_WG, cap_small);
+  }
+  x.status = status;
+  x.status_bit = status_bit;
   char *base = static_cast<char *>(ws);
   x.At = At; x.Q = Q; x.Rf = Rf; x.batch = batch; x.n = n; x.sA = n * n; x.ni = (int)n;
   x.Tb = reinterpret_cast<float *>(base + x.L.t_off);
@@ -1635,8 +1718,19 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   const int64_t nob = x.L.nob, np = x.L.np;
 
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
-  if (x.L.block)   // generations restart at 1 every call: clear the old items
+  x.skip = nullptr;
+  x.sSkip = 0;
+  if (x.L.block) {  // generations restart at 1 every call: clear the old items and flags
     SOAP_TRY(launch_zero_u32(reinterpret_cast<uint32_t *>(x.xch), 2 * batch * BK_XSTRIDE, s));
+    x.skip = reinterpret_cast<const unsigned *>(x.xch + BK_XFAILED);
+    x.sSkip = 2 * BK_XSTRIDE;
+    if (g_force_give_up.load() & status_bit) {
+      hipLaunchKernelGGL(qr_raise_abort_kernel,
+                         dim3((unsigned)std::min<int64_t>((batch + 63) / 64, 1024)), dim3(64), 0,
+                         s, x.xch, batch);
+      SOAP_TRY(hipGetLastError());
+    }
+  }
 
   // Look-ahead: block ob+1's columns are updated first (the "near" update),
   // then block ob+1 is factored on the panel stream while this stream applies
@@ -1709,7 +1803,7 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   {
     const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
     hipLaunchKernelGGL(qr_init_q_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, Q, x.dsign,
-                       x.ni, x.sA);
+                       x.ni, x.sA, x.skip, x.sSkip);
     SOAP_TRY(hipGetLastError());
   }
   // Backwards: the blocks past the last full pair one by one, then the

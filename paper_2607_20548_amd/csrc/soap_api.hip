@@ -175,14 +175,17 @@ hipError_t aux_stream(int which, hipStream_t *out) {
 // The KL step adds one m x n buffer, the eigenvalue estimates and their
 // partial sums; the QR workspaces stay last (each QR uses up to the next
 // region, the R side up to the end).
+// The status word of the step comes first (soap_workspace_status reads it at
+// offset 0).
 struct StepLayout {
-  size_t al, ar, tg, tm, nb, kz, kw, laml, lamr, partl, partr, qrl, qrr, total;
+  size_t st, al, ar, tg, tm, nb, kz, kw, laml, lamr, partl, partr, qrl, qrr, total;
 };
 
 StepLayout step_layout(int64_t batch, int64_t m, int64_t n, bool kl) {
   StepLayout L{};
   const size_t f = sizeof(float);
   size_t o = 0;
+  L.st = o; o = align256(o + sizeof(uint32_t));
   L.al = o; o = align256(o + f * batch * m * m);
   L.ar = o; o = align256(o + f * batch * n * n);
   L.tg = o; o = align256(o + f * batch * m * n);   // T_G, T_M: adjacent, so that the
@@ -558,6 +561,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   const float c2 = bc ? (float)(1.0 - std::pow((double)beta2, (double)step)) : 1.f;
 
   char *w = static_cast<char *>(ws);
+  uint32_t *status = reinterpret_cast<uint32_t *>(w + lay.st);
   float *AL = reinterpret_cast<float *>(w + lay.al);
   float *AR = reinterpret_cast<float *>(w + lay.ar);
   float *TG = reinterpret_cast<float *>(w + lay.tg);
@@ -571,6 +575,8 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   const double B = (double)batch, md = (double)m, nd = (double)n;
   hipError_t e;
 
+  // The status word starts clear; a QR that gives up sets its side's bit.
+  if ((e = soap::launch_zero_u32(status, 1, s)) != hipSuccess) return hip_fail(e, "status");
   {  // M <- b1 M + (1-b1) G (weight space)
     StageScope sc(ST_MOMENTUM, 0.0, s);
     if ((e = soap::launch_momentum(M, grad, batch * mn, beta1, s)) != hipSuccess)
@@ -672,7 +678,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     if (refresh) {  // Q_L = QR(A_L).Q
       StageScope sc(ST_QR_L, B * (8.0 / 3.0) * md * md * md, sl);
       if ((r = soap::qr_factor_and_form_q(AL, QL, nullptr, batch, m, qws_l, qws_l_bytes, sl, spl,
-                                          spl)) != hipSuccess) {
+                                          spl, status, SOAP_STATUS_QR_L)) != hipSuccess) {
         side_where = "QR L";
         return r;
       }
@@ -722,7 +728,7 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
       return rotate_in_l(true);
     };
     if ((e = soap::qr_factor_and_form_q(AR, QR, nullptr, batch, n, qws_r, qws_r_bytes, s, spr, sl,
-                                        kl ? ev_yr : nullptr, ev_mid,
+                                        status, SOAP_STATUS_QR_R, kl ? ev_yr : nullptr, ev_mid,
                                         late_l ? kLSideFrom : kRotateInFrom, at_mid)) != hipSuccess)
       return hip_fail(e, side_where ? side_where : "QR R");
   } else if ((e = rotate_in_l(false)) != hipSuccess) {
@@ -1005,6 +1011,11 @@ int soap_step_batched(int64_t batch, float *param, const float *grad, float *L, 
                    weight_decay, step, flags, workspace, workspace_bytes, stream, false, 0.f);
 }
 
+size_t soap_workspace_update_offset(int64_t batch, int64_t m, int64_t n) {
+  if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n)) return 0;
+  return step_layout(batch, m, n, false).nb;
+}
+
 size_t soap_kl_workspace_bytes(int64_t batch, int64_t m, int64_t n) {
   if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n)) return 0;
   return step_layout(batch, m, n, true).total;
@@ -1078,9 +1089,38 @@ int soap_kl_factors_f32(int64_t m, int64_t n, const float *G, float *L, float *R
 
 const char *soap_last_error(void) { return g_err; }
 
+int soap_workspace_status(const void *workspace, uint32_t *status, hipStream_t stream) {
+  if (!workspace) return fail(SOAP_ERR_NULL, "workspace is NULL");
+  uint32_t word = 0;
+  hipError_t e = hipMemcpyAsync(&word, workspace, sizeof(word), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_fail(e, "status read");
+  if (status) *status = word;
+  if (word & ~uint32_t(SOAP_STATUS_QR_L | SOAP_STATUS_QR_R))
+    return fail(SOAP_ERR_WORKSPACE, "status word 0x%x has unknown bits: not a step or QR "
+                "workspace, or it was overwritten", word);
+  if (word)
+    return fail(SOAP_ERR_QR_GAVE_UP,
+                "the eigenbasis QR of %s gave up waiting for its resident workgroups (other "
+                "work held the compute units); that basis was kept as it was",
+                word == (SOAP_STATUS_QR_L | SOAP_STATUS_QR_R)
+                    ? "both factors"
+                    : (word & SOAP_STATUS_QR_L) ? "the m x m factor" : "the n x n factor");
+  return ok();
+}
+
+int soap_test_force_qr_give_up(uint32_t mask) {
+  if (mask & ~uint32_t(SOAP_STATUS_QR_L | SOAP_STATUS_QR_R))
+    return fail(SOAP_ERR_HPARAM, "unknown QR bits 0x%x", mask);
+  soap::qr_force_give_up(mask);
+  return ok();
+}
+
+// Workspace of soap_qr_f32: the status word, A^T, the QR's own buffers.
 size_t soap_qr_workspace_bytes(int64_t n) {
   if (!dim_ok(n)) return 0;
-  return align256(sizeof(float) * n * n) + soap::qr_workspace_bytes(1, n);
+  return align256(sizeof(uint32_t)) + align256(sizeof(float) * n * n) +
+         soap::qr_workspace_bytes(1, n);
 }
 
 int soap_qr_f32(int64_t n, const float *A, float *Q, float *Rf, void *workspace,
@@ -1099,18 +1139,19 @@ int soap_qr_f32(int64_t n, const float *A, float *Q, float *Rf, void *workspace,
     for (int j = i + 1; j < 4; ++j)
       if (rs[i].bytes && rs[j].bytes && overlap(rs[i], rs[j]))
         return fail(SOAP_ERR_ALIAS, "%s overlaps %s", rs[i].name, rs[j].name);
-  float *Aw = static_cast<float *>(workspace);
-  char *rest = static_cast<char *>(workspace) + align256(sizeof(float) * n * n);
-  hipError_t e = soap::launch_transpose(Aw, A, n, stream);   // the QR factors A^T
-  if (e == hipSuccess)
-  {
+  uint32_t *status = static_cast<uint32_t *>(workspace);
+  const size_t head = align256(sizeof(uint32_t)) + align256(sizeof(float) * n * n);
+  float *Aw = reinterpret_cast<float *>(static_cast<char *>(workspace) + align256(sizeof(uint32_t)));
+  char *rest = static_cast<char *>(workspace) + head;
+  hipError_t e = soap::launch_zero_u32(status, 1, stream);
+  if (e == hipSuccess) e = soap::launch_transpose(Aw, A, n, stream);   // the QR factors A^T
+  if (e == hipSuccess) {
     hipStream_t sp = nullptr, st = nullptr;
     if (e == hipSuccess) e = aux_stream(2, &sp);
     if (e == hipSuccess) e = aux_stream(1, &st);
     if (e == hipSuccess)
-      e = soap::qr_factor_and_form_q(Aw, Q, Rf, 1, n, rest,
-                                     workspace_bytes - align256(sizeof(float) * n * n), stream, sp,
-                                     st);
+      e = soap::qr_factor_and_form_q(Aw, Q, Rf, 1, n, rest, workspace_bytes - head, stream, sp,
+                                     st, status, SOAP_STATUS_QR_L);
   }
   if (e != hipSuccess) return hip_fail(e, "QR");
   return ok();

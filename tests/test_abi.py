@@ -206,3 +206,23 @@ def test_muon_validation(L):
     assert call(co=bad.ctypes.data, it=1) == soap.SOAP_ERR_HPARAM
     assert L.soap_muon_step_batched(0, P, G, M, m, n, 0.9, 1e-3, 0.1, 1e-7, cp, 2, 0, W, ws,
                                     None) == soap.SOAP_ERR_SHAPE
+
+
+def test_status_and_diagnostic_entry_points_validate(L):
+    word = __import__("ctypes").c_uint32(7)
+    assert L.soap_workspace_status(None, None, None) == soap.SOAP_ERR_NULL
+    assert L.soap_test_force_qr_give_up(4) == soap.SOAP_ERR_HPARAM
+    assert L.soap_test_force_qr_give_up(soap.SOAP_STATUS_QR_L | soap.SOAP_STATUS_QR_R) == soap.SOAP_OK
+    assert L.soap_test_force_qr_give_up(0) == soap.SOAP_OK
+    assert word.value == 7
+    # N sits inside the step workspace, past the power products and both
+    # rotation intermediates, and is the same for the KL layout
+    for b, m, n in [(1, 8, 12), (3, 256, 512), (1, 4096, 14336)]:
+        off = soap.soap_workspace_update_offset(b, m, n)
+        assert off % 256 == 0
+        assert off >= 4 * b * (m * m + n * n + 2 * m * n)
+        assert off + 4 * b * m * n <= soap.soap_workspace_bytes(b, m, n)
+        assert off + 4 * b * m * n <= soap.soap_kl_workspace_bytes(b, m, n)
+    assert soap.soap_workspace_update_offset(1, 0, 4) == 0
+    # the QR stage's workspace holds its status word, A^T and the QR buffers
+    assert soap.soap_qr_workspace_bytes(64) > 4 * 64 * 64
