@@ -1,4 +1,6 @@
 """Helpers shared by the GPU tests: host<->device copies and error metrics."""
+import time
+
 import numpy as np
 
 
@@ -36,6 +38,21 @@ def log(msg):
 U32 = 2.0 ** -24   # unit roundoff of fp32
 
 
+def spectral_norm(G):
+    """||G||_2: exact (SVD) when the smaller side is at most 1024, otherwise
+    40 power iterations on G^T G from a fixed start, raised by 1% (the
+    iteration approaches the largest singular value from below).  Used only
+    to scale the fp32 error bounds."""
+    G = np.asarray(G, np.float64)
+    if min(G.shape) <= 1024:
+        return float(np.linalg.norm(G, 2))
+    v = np.random.default_rng(0).standard_normal(G.shape[1])
+    for _ in range(40):
+        v = G.T @ (G @ v)
+        v /= np.linalg.norm(v)
+    return 1.01 * float(np.linalg.norm(G @ v))
+
+
 def adam_fp32_bound(N_ora, Vhat_ora, g_scale, eps, factor=64.0):
     """First-order fp32 error bound of N = Mhat / (sqrt(Vhat) + eps) per entry.
 
@@ -60,74 +77,176 @@ def update_from_weights(W_prev, W_new, QL, QR, lr, wd):
 
 TOL = 1e-4
 HP = dict(beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3, weight_decay=0.1)
+# Relative Frobenius bound of N over ALL its entries (strict checks): the
+# sign-like entries at t = 1 may flip in fp32, the rest agree to ~1e-6.
+N_ALL_TOL = 1e-3
 
 
-def compare_state(st, gs, tag, tol=TOL):
-    """Every state tensor of the GPU state `gs` against the oracle state `st`."""
+def compare_state(st, gs, tag, tol=TOL, b=None):
+    """Every state tensor of the GPU state `gs` (batch entry b, if given)
+    against the oracle state `st`."""
+    sel = (lambda x: x[b]) if b is not None else (lambda x: x)
+    got = {k: sel(host(getattr(gs, k))) for k in ("L", "R", "Q_L", "Q_R", "M", "V")}
     errs = {
-        "L": rel(host(gs.L), st.L), "R": rel(host(gs.R), st.R),
-        "Q_L": rel(host(gs.Q_L), st.QL), "Q_R": rel(host(gs.Q_R), st.QR),
-        "M": rel(host(gs.M), st.M), "V": rel(host(gs.V), st.V),
+        "L": rel(got["L"], st.L), "R": rel(got["R"], st.R),
+        "Q_L": rel(got["Q_L"], st.QL), "Q_R": rel(got["Q_R"], st.QR),
+        "M": rel(got["M"], st.M), "V": rel(got["V"], st.V),
     }
     for k, v in errs.items():
         assert v <= tol, (tag, k, v)
-    assert column_signs_agree(host(gs.Q_L), st.QL) and column_signs_agree(host(gs.Q_R), st.QR)
+    assert column_signs_agree(got["Q_L"], st.QL) and column_signs_agree(got["Q_R"], st.QR), tag
     return errs
 
 
+def lambda_max(F):
+    """Largest eigenvalue of a symmetric positive semidefinite F: 50 power
+    iterations from a fixed start, raised by 1% (the iteration approaches it
+    from below).  Used only to scale error bounds."""
+    F = np.asarray(F, np.float64)
+    v = np.ones(F.shape[0]) / np.sqrt(F.shape[0])
+    for _ in range(50):
+        v = F @ v
+        v /= np.linalg.norm(v)
+    return 1.01 * float(v @ (F @ v))
+
+
+class UpdateCheck:
+    """Checks the eigenbasis update N and the weights of consecutive steps of
+    one matrix.  Expected values come from the oracle only.
+
+    Per step:
+      * every entry of N within its fp32 interval around the oracle's value,
+        1e-4 |N| + 64x the first-order fp32 error of the eigenbasis quotient
+        (adam_fp32_bound) + 1e-6;
+      * "undetermined" entries (first-order fp32 error above 1% of |N|) may
+        be sign-like decisions fp32 cannot take -- chiefly at t = 1, where N
+        is sign(G') smoothed by eps and numerator and denominator come from
+        separately rounded rotations.  Relative Frobenius error <= TOL over
+        the other entries; strict: <= N_ALL_TOL over all entries;
+      * strict: W against the oracle's W within TOL (relative Frobenius, all
+        entries, no exception: a wrong value at the undetermined entries
+        would move W by lr |dN| each);
+      * the rotation out and weight update of this step on the GPU's own
+        inputs, W = (1 - lr wd) W_prev - lr Q_L N Q_R^T evaluated in fp64 on
+        sampled rows, within CHAIN_TOL.
+
+    strict=False is for full-rank Gaussian stress gradients: their factors are
+    ill conditioned (condition numbers in the hundreds), and the fp32 QR's
+    forward error grows with the condition number of its input, which the
+    first-order model above leaves out.  There the error scale ||G||_2 becomes
+    ||G||_2 (1 + (lambda_max(L) + lambda_max(R)) / floor) (floor = beta^t:
+    identity-initialised factors stay >= beta^t I), N over all entries is not
+    bounded, and W is held to TOL plus the interval widths of
+    the undetermined entries carried through the weight updates
+    (lr ||width over undetermined||_F per step, decayed by 1 - lr wd per
+    later step, over ||W_oracle||_F)."""
+
+    CHAIN_TOL = 1e-5
+
+    def __init__(self, hp=HP, bias_correction=True, strict=True, floor_beta=None):
+        self.hp = hp
+        self.bias_correction = bias_correction
+        self.strict = strict
+        self.floor_beta = hp["beta2"] if floor_beta is None else floor_beta
+        self.g_scale = 0.0
+        self.w_budget = 0.0
+
+    def __call__(self, t, G, N_gpu, N_ora, V_ora, W_gpu, W_ora, tag="", chain=None, factors=None):
+        """chain: (W_prev, Q_L, Q_R) of the GPU for the update-chain check;
+        factors: the oracle's (L, R) after the step (needed when not strict)."""
+        import oracle
+        hp = self.hp
+        lr, wd, eps = hp["lr"], hp["weight_decay"], hp["eps"]
+        self.g_scale = max(self.g_scale, spectral_norm(G))
+        scale = self.g_scale
+        if not self.strict:
+            L, R = factors
+            scale *= 1.0 + (lambda_max(L) + lambda_max(R)) / self.floor_beta ** t
+        _, c2 = oracle.bias_corrections(hp["beta1"], hp["beta2"], t, self.bias_correction)
+        width = 1e-4 * np.abs(N_ora) + adam_fp32_bound(N_ora, V_ora / c2, scale, eps) + 1e-6
+        dN = np.abs(N_gpu - N_ora)
+        assert np.all(dN <= width), (tag, t, float(np.max(dN / width)))
+        well = adam_fp32_bound(N_ora, V_ora / c2, scale, eps, factor=1.0) <= 1e-2 * np.abs(N_ora)
+        k = int((~well).sum())
+        errs = {"N_well": rel(N_gpu[well], N_ora[well]) if well.any() else 0.0,
+                "N_all": rel(N_gpu, N_ora)}
+        assert errs["N_well"] <= TOL, (tag, t, errs["N_well"])
+        if self.strict:
+            assert errs["N_all"] <= N_ALL_TOL, (tag, t, errs["N_all"])
+        errs["W"] = rel(W_gpu, W_ora)
+        if self.strict:
+            w_bound = TOL
+        else:
+            self.w_budget = (1.0 - lr * wd) * self.w_budget + lr * float(np.linalg.norm(width[~well]))
+            w_bound = TOL + self.w_budget / np.linalg.norm(W_ora)
+            errs["W_bound"] = w_bound
+        assert errs["W"] <= w_bound, (tag, t, errs["W"], w_bound)
+        errs["undetermined"] = k
+        if chain is not None:
+            W_prev, QL, QR = chain
+            m = W_gpu.shape[0]
+            rows = np.unique(np.concatenate([np.random.default_rng(t).integers(0, m, 64),
+                                             [0, m - 1]])) if m > 66 else np.arange(m)
+            beta_w = float(np.float32(1.0) - np.float32(lr) * np.float32(wd))
+            want = beta_w * W_prev[rows] - float(np.float32(lr)) * ((QL[rows] @ N_gpu) @ QR.T)
+            errs["chain"] = rel(W_gpu[rows], want)
+            assert errs["chain"] <= self.CHAIN_TOL, (tag, t, errs["chain"])
+        return errs
+
+
 def run_open_loop(m, n, grads, W0, hp=HP, flags=0, bias_correction=True, beta_kron=None,
-                  refresh_every=1, stale_refresh=False):
+                  refresh_every=1, stale_refresh=False, tag=None, strict=True):
     """Open loop over the given gradients (SOAP, or KL-SOAP when beta_kron is
-    given).  Every step:
-      * L, R, Q_L, Q_R, M, V: relative Frobenius error <= TOL;
-      * the update N (recovered from the GPU weights): every entry within
-        1e-4 |N| plus 64x the first-order fp32 error of the eigenbasis quotient,
-        and relative Frobenius error <= TOL over the well-determined entries
-        (those whose first-order fp32 error is below 1% of |N|);
-      * W: relative Frobenius error <= TOL against the oracle's weights re-based
-        on the GPU's N at the entries that are not well determined."""
+    given): GPU and oracle start from the same initial state and each runs its
+    own trajectory.  Every step: L, R, Q_L, Q_R, M, V within TOL (relative
+    Frobenius) with no flipped eigenvector, and N (read from the workspace)
+    and W by UpdateCheck (strict: for gradients of the workloads' low-rank
+    plus noise recipe; not strict: full-rank Gaussian stress gradients)."""
     import paper_2607_20548_amd as soap
     import oracle
     kl = beta_kron is not None
+    tag = tag or f"{'KL ' if kl else ''}{m}x{n}"
     gs = soap.SoapState(m, n, kl=kl)
     W = dev(W0)
     st = oracle.init_state(W0.astype(np.float64))
-    W_adj = W0.astype(np.float64)
-    lr, wd, eps = hp["lr"], hp["weight_decay"], hp["eps"]
-    g_scale = 0.0
+    chk = UpdateCheck(hp, bias_correction, strict=strict,
+                      floor_beta=beta_kron if kl else hp["beta2"])
     extra = dict(beta_kron=beta_kron) if kl else {}
     for t, G in enumerate(grads, start=1):
-        W_prev = host(W)
         Q_prev = (host(gs.Q_L), host(gs.Q_R))
+        W_prev = host(W)
         gs.step(W, dev(G), t, flags=flags, refresh_every=refresh_every,
                 stale_refresh=stale_refresh, **extra, **hp)
         step_fn = oracle.kl_soap_step if kl else oracle.soap_step
+        t0 = time.perf_counter()
         st, d = step_fn(st, G.astype(np.float64), t, bias_correction=bias_correction,
                         diagnostics=True, refresh_every=refresh_every,
                         stale_refresh=stale_refresh, **extra, **hp)
+        if m * n >= 1 << 22:
+            log(f"{tag} t={t} oracle step {time.perf_counter() - t0:.1f} s")
         if t % refresh_every != 0:   # no refresh: the bases are kept bit for bit
             assert np.array_equal(host(gs.Q_L), Q_prev[0]) and np.array_equal(host(gs.Q_R), Q_prev[1])
-        errs = compare_state(st, gs, f"{m}x{n} t={t}")
-        g_scale = max(g_scale, np.linalg.norm(G.astype(np.float64), 2))
-        Wg = host(W)
-        N_gpu = update_from_weights(W_prev, Wg, host(gs.Q_L), host(gs.Q_R), lr, wd)
-        _, c2 = oracle.bias_corrections(hp["beta1"], hp["beta2"], t, bias_correction)
-        N_ora = d["N"]
-        bound = adam_fp32_bound(N_ora, st.V / c2, g_scale, eps)
-        dN = np.abs(N_gpu - N_ora)
-        assert np.all(dN <= 1e-4 * np.abs(N_ora) + bound + 1e-6), (t, float(np.max(dN - bound)))
-        # well determined: the expected fp32 error (factor 1) is below 1% of |N|
-        well = adam_fp32_bound(N_ora, st.V / c2, g_scale, eps, factor=1.0) <= 1e-2 * np.abs(N_ora)
-        errs["N_well"] = rel(N_gpu[well], N_ora[well]) if well.any() else 0.0
-        assert errs["N_well"] <= TOL, (t, errs["N_well"])
-        N_adj = np.where(well, N_ora, N_gpu)
-        W_adj = (1.0 - lr * wd) * W_adj - lr * (st.QL @ N_adj @ st.QR.T)
-        errs["W"] = rel(Wg, W_adj)
-        errs["W_plain"] = rel(Wg, st.W)
-        log(f"{'KL ' if kl else ''}{m}x{n} t={t} not_well_determined={int((~well).sum())} " +
-            " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
-        assert errs["W"] <= TOL, (t, errs["W"])
+        errs = compare_state(st, gs, f"{tag} t={t}")
+        assert gs.status() == (soap.SOAP_OK, 0)
+        errs.update(chk(t, G, host(gs.update()), d["N"], st.V, host(W), st.W, tag,
+                        chain=(W_prev, host(gs.Q_L), host(gs.Q_R)), factors=(st.L, st.R)))
+        log(f"{tag} t={t} " + " ".join(f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}"
+                                       for k, v in errs.items()))
     return gs, W, st
+
+
+def recipe_grads(m, n, steps, seed, rank=8, batch=None):
+    """Gradients of the workloads' recipe (rank-`rank` signal with singular
+    values 1/i plus Gaussian noise at 10% of its Frobenius norm) at any shape,
+    [batch,] m x n fp32."""
+    from synth import gradients as sg
+    if batch is None:
+        spec = sg.MatrixSpec("test", m, n, rank, "rel", 0.10, matrix_id=seed)
+        return list(sg.make_matrix_stream(spec, 0, steps, seed=1000 + seed))
+    streams = [sg.make_matrix_stream(sg.MatrixSpec("test", m, n, rank, "rel", 0.10,
+                                                   matrix_id=seed * 1000 + b),
+                                     0, steps, seed=1000 + seed) for b in range(batch)]
+    return [np.stack([next(g) for g in streams]) for _ in range(steps)]
 
 
 def check_factor_ema_sampled(pre, post, G, rng, beta2=HP["beta2"], nsamp=48):
@@ -181,11 +300,11 @@ def check_refresh_adam_sampled(pre, post, G, t, rng, hp=HP, nsamp=48, ncols=16):
     beta_w = float(np.float32(1.0) - np.float32(lr) * np.float32(wd))
     dW = (beta_w * pre["W"] - post["W"]) / float(np.float32(lr))
     N_got = np.einsum("ik,ik->k", QL[:, kk], dW @ QR[:, ll])
-    g_scale = np.linalg.norm(G, 2)
+    g_scale = spectral_norm(G)
     bound = adam_fp32_bound(N_want, post["V"][kk, ll] / c2, g_scale, eps)
     assert np.all(np.abs(N_got - N_want) <= 1e-4 * np.abs(N_want) + bound + 1e-5)
     well = adam_fp32_bound(N_want, post["V"][kk, ll] / c2, g_scale, eps, factor=1.0) <= 1e-2 * np.abs(N_want)
-    if well.sum() >= nsamp // 2:
-        assert rel(N_got[well], N_want[well]) <= TOL
+    assert well.sum() >= nsamp // 2, int(well.sum())
+    assert rel(N_got[well], N_want[well]) <= TOL
     assert np.all(np.isfinite(dW))
     return {"N_rel_well": rel(N_got[well], N_want[well]) if well.any() else 0.0}

@@ -1,32 +1,35 @@
-"""Parity at the full sizes of the benchmark workloads, in the launch
-configuration the bench uses (soap_step / soap_step_batched on the real
-shapes).
+"""Parity at the full sizes of the benchmark workloads against the fp64
+oracle, in the launch configuration the bench uses (soap_step /
+soap_step_batched on the real shapes).
 
-The fp64 oracle cannot run many full steps at 4096..14336, so these tests
-check ONE step closed-loop: the GPU takes a few steps, its state is copied to
-the host, the GPU takes one more step, and every updated quantity with a
-plain definition is recomputed in fp64 on sampled entries from the GPU's own
-pre-step state:
-  * L, R (factor EMA) and M (momentum EMA) entry by entry;
-  * the refreshed eigenbases by their defining properties -- Q^T Q = I and
-    Q^T (L Q_prev) upper triangular with a positive diagonal -- on sampled
-    columns (those properties fix the Q factor uniquely);
-  * V and the update N at sampled eigenbasis entries, from G' = Q_L^T G Q_R
-    and M' = Q_L^T M Q_R formed with matrix-vector products;
-  * W through N recovered from consecutive weights.
-The 4096 x 4096 shape also gets one full oracle step (all tensors), and the
-expert bank full oracle parity on two experts.
+Every test runs OPEN LOOP: the GPU and the oracle start from the same
+initial state (L = R = Q_L = Q_R = I, M = V = 0) and the same seeded fp32
+gradients, each follows its own trajectory, and after every step all state
+tensors are compared (relative Frobenius <= 1e-4, no flipped eigenvector),
+the update N (read from the workspace) entry by entry and in norm, and W
+against the oracle's weights (UpdateCheck in tests/gpu_helpers.py).  The
+oracle's QR of factors larger than 4096 takes LAPACK's blocked Householder
+route to the same unique Q (oracle.refresh_qr).
+
+  * 4096 x 14336 (MLP up-projection, R is 14336 x 14336): 2 steps;
+  * 4096 x 4096 (attention projection): 5 steps;
+  * the four matrix shapes of the 24-layer model: 2 steps each, and two
+    2048 x 8192 matrices through soap_step_batched (rank-1024 Q formation per
+    batch entry; one against the oracle, one against the single-matrix call);
+  * the 64-expert bank through soap_step_batched: all 20 steps, two experts
+    against the oracle every step, every ninth expert checked at the last
+    step by the properties that fix the step (sampled);
+  * the 24-layer model's 96-matrix host loop (one soap_step per matrix,
+    workspaces shared per shape, as the bench runs it): every matrix of the
+    first and last layer bit for bit equal to the same matrix stepped alone.
 """
 import numpy as np
 import pytest
 
-from tests.gpu_helpers import (dev, host, rel, log, column_signs_agree, check_factor_ema_sampled,
-                                check_refresh_adam_sampled)
+from tests.gpu_helpers import (dev, host, log, run_open_loop, compare_state, UpdateCheck,
+                                check_factor_ema_sampled, check_refresh_adam_sampled, HP)
 
 pytestmark = pytest.mark.gpu
-
-HP = dict(beta1=0.95, beta2=0.95, eps=1e-8, lr=1e-3, weight_decay=0.1)
-TOL = 1e-4
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -38,135 +41,171 @@ def _lib():
     soap.lib()
 
 
-def _snap(gs, W, b=None):
-    sel = (lambda x: x[b]) if b is not None else (lambda x: x)
-    return {k: sel(host(v)) for k, v in dict(W=W, L=gs.L, R=gs.R, QL=gs.Q_L, QR=gs.Q_R,
-                                               M=gs.M, V=gs.V).items()}
-
-
-def _sampled_step_checks(pre, post, G, t, rng, nsamp=48, ncols=16):
-    """All checks of one step from the GPU state `pre` to `post` (fp64 arrays)."""
-    check_factor_ema_sampled(pre, post, G, rng, HP["beta2"], nsamp)
-    return check_refresh_adam_sampled(pre, post, G, t, rng, HP, nsamp, ncols)
-
-
-def _run_single(spec, cfg, steps_before, seed=0):
-    import paper_2607_20548_amd as soap
+def _spec(cfg, shape=None):
     from synth import gradients as sg
-    m, n = spec.m, spec.n
-    grads = list(sg.make_matrix_stream(spec, cfg, steps_before + 1, seed=seed))
-    gs = soap.SoapState(m, n)
-    W = dev(sg.initial_weight(spec, cfg, seed=seed))
-    for t in range(1, steps_before + 1):
-        gs.step(W, dev(grads[t - 1]), t, **HP)
-    pre = _snap(gs, W)
-    t = steps_before + 1
-    gs.step(W, dev(grads[-1]), t, **HP)
-    post = _snap(gs, W)
-    return pre, post, grads[-1].astype(np.float64), t
+    specs = sg.workload(cfg).matrices
+    return specs[0] if shape is None else next(s for s in specs if (s.m, s.n) == shape)
 
 
-@pytest.mark.parametrize("cfg,steps_before", [(2, 2), (1, 3)])
-def test_single_matrix_workloads_sampled(cfg, steps_before):
+def _open_loop(cfg, steps, shape=None):
     from synth import gradients as sg
-    spec = sg.workload(cfg).matrices[0]
-    log(f"workload {spec.m}x{spec.n}: {steps_before} steps, then a sampled closed-loop step")
-    pre, post, G, t = _run_single(spec, cfg, steps_before)
-    info = _sampled_step_checks(pre, post, G, t, np.random.default_rng(cfg))
-    log(f"  ok {info}")
+    spec = _spec(cfg, shape)
+    log(f"workload {cfg}: {spec.m}x{spec.n}, {steps} open-loop steps")
+    run_open_loop(spec.m, spec.n, sg.make_matrix_stream(spec, cfg, steps),
+                  sg.initial_weight(spec, cfg), tag=f"{spec.m}x{spec.n}")
 
 
-@pytest.mark.parametrize("shape", [(2048, 6144), (2048, 2048), (2048, 8192), (8192, 2048)])
-def test_transformer_layer_shapes_sampled(shape):
+def test_mlp_up_projection_4096x14336_open_loop():
+    _open_loop(2, 2)
+
+
+def test_attention_projection_4096_open_loop():
+    _open_loop(1, 5)
+
+
+@pytest.mark.parametrize("shape", [(2048, 8192), (8192, 2048), (2048, 6144), (2048, 2048)])
+def test_transformer_layer_shapes_open_loop(shape):
     """The four matrix shapes of the 24-layer dense model (h 2048, FFN 8192),
     Student-t(3) noise at 5% of the signal."""
-    from synth import gradients as sg
-    spec = next(s for s in sg.workload(4).matrices if (s.m, s.n) == shape)
-    log(f"layer shape {shape}")
-    pre, post, G, t = _run_single(spec, 4, 2)
-    info = _sampled_step_checks(pre, post, G, t, np.random.default_rng(shape[0] + shape[1]))
-    log(f"  ok {info}")
+    _open_loop(4, 2, shape)
+
+
+def _batched_open_loop(m, n, streams, steps, W0, entries, tag):
+    """soap_step_batched for `steps` steps from W0 (B x m x n), the gradient of
+    batch entry b at each step drawn from the generator streams[b]; the
+    entries in `entries` follow their own oracle trajectories and are compared
+    after every step.  Returns the GPU state, W, and the GPU state before and
+    the gradients of the last step (for sampled checks)."""
+    import paper_2607_20548_amd as soap
+    import oracle
+    B = W0.shape[0]
+    gs = soap.SoapState(m, n, batch=B)
+    W = dev(W0)
+    sts = {e: oracle.init_state(W0[e].astype(np.float64)) for e in entries}
+    chks = {e: UpdateCheck(HP) for e in entries}
+    pre = G = None
+    for t in range(1, steps + 1):
+        G = np.stack([next(g) for g in streams])
+        W_prev = host(W)
+        if t == steps:
+            pre = dict(W=W_prev, L=host(gs.L), R=host(gs.R), QL=host(gs.Q_L), QR=host(gs.Q_R),
+                       M=host(gs.M), V=host(gs.V))
+        gs.step(W, dev(G), t, **HP)
+        assert gs.status() == (soap.SOAP_OK, 0)
+        N_all, W_all = host(gs.update()), host(W)
+        QL_all, QR_all = host(gs.Q_L), host(gs.Q_R)
+        for e in entries:
+            sts[e], d = oracle.soap_step(sts[e], G[e].astype(np.float64), t, diagnostics=True,
+                                         **HP)
+            errs = compare_state(sts[e], gs, f"{tag} entry {e} t={t}", b=e)
+            errs.update(chks[e](t, G[e], N_all[e], d["N"], sts[e].V, W_all[e], sts[e].W,
+                                f"{tag} entry {e}", chain=(W_prev[e], QL_all[e], QR_all[e])))
+            log(f"{tag} entry {e} t={t} " + " ".join(
+                f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}" for k, v in errs.items()))
+    return gs, W, pre, G
 
 
 def test_layer_shape_batched_rank1024_q_formation():
     """Two 2048 x 8192 matrices through soap_step_batched: the R-side QR
-    (n = 8192) forms Q by rank-1024 updates, each of whose products starts
-    from the head block of W = Y^T Q taken from diag(d), for every batch
-    entry.  One step, then the sampled closed-loop checks of a second step
-    on both entries."""
+    (n = 8192) forms Q by rank-1024 updates for every batch entry.  Entry 1
+    (the one at a nonzero batch offset) against the oracle for 2 steps;
+    entry 0 against the same matrix stepped alone (the single-matrix path of
+    that shape is checked against the oracle above), relative Frobenius
+    <= 1e-6 per tensor."""
+    import torch
     import paper_2607_20548_amd as soap
     from synth import gradients as sg
-    spec = next(s for s in sg.workload(4).matrices if (s.m, s.n) == (2048, 8192))
+    from tests.gpu_helpers import rel
+    spec = _spec(4, (2048, 8192))
     B, steps = 2, 2
-    log(f"batched layer shape {spec.m}x{spec.n} x{B}")
-    grads = np.stack([np.stack(list(sg.make_matrix_stream(spec, 4, steps, seed=b)))
-                      for b in range(B)], axis=1)                       # steps x B x m x n
-    W = dev(np.stack([sg.initial_weight(spec, 4, seed=b) for b in range(B)]))
-    gs = soap.SoapState(spec.m, spec.n, batch=B)
-    for t in range(1, steps):
-        gs.step(W, dev(grads[t - 1]), t, **HP)
-    pre_all = _snap(gs, W)
-    gs.step(W, dev(grads[steps - 1]), steps, **HP)
-    post_all = _snap(gs, W)
-    rng = np.random.default_rng(8192)
-    for b in range(B):
-        pre = {k: v[b] for k, v in pre_all.items()}
-        post = {k: v[b] for k, v in post_all.items()}
-        info = _sampled_step_checks(pre, post, grads[steps - 1, b].astype(np.float64), steps, rng)
-        log(f"  entry {b} ok {info}")
+    streams = [sg.make_matrix_stream(spec, 4, steps, seed=b) for b in range(B)]
+    W0 = np.stack([sg.initial_weight(spec, 4, seed=b) for b in range(B)])
+    gs, W, _, _ = _batched_open_loop(spec.m, spec.n, streams, steps, W0, [1], "batched 2048x8192")
+    alone = soap.SoapState(spec.m, spec.n)
+    Wa = dev(W0[0])
+    for t, G in enumerate(sg.make_matrix_stream(spec, 4, steps, seed=0), start=1):
+        alone.step(Wa, dev(G), t, **HP)
+    torch.cuda.synchronize()
+    for name, a, b in [("W", Wa, W[0])] + [(k, getattr(alone, k), getattr(gs, k)[0])
+                                          for k in ("L", "R", "Q_L", "Q_R", "M", "V")]:
+        err = rel(host(b), host(a))
+        assert err <= 1e-6, (name, err)
 
 
-def test_workload_4096_full_oracle_step():
-    """One full closed-loop oracle step at 4096 x 4096 (every tensor)."""
-    import oracle
-    from synth import gradients as sg
-    spec = sg.workload(1).matrices[0]
-    pre, post, G, t = _run_single(spec, 1, 2)
-    st = oracle.OracleState(pre["W"], pre["L"], pre["R"], pre["QL"], pre["QR"], pre["M"], pre["V"])
-    st, d = oracle.soap_step(st, G, t, diagnostics=True, **HP)
-    errs = {k: rel(post[k], getattr(st, a)) for k, a in
-            [("L", "L"), ("R", "R"), ("QL", "QL"), ("QR", "QR"), ("M", "M"), ("V", "V"), ("W", "W")]}
-    log("4096x4096 closed-loop step: " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
-    for k, v in errs.items():
-        assert v <= TOL, (k, v)
-    assert column_signs_agree(post["QL"], st.QL) and column_signs_agree(post["QR"], st.QR)
-
-
-def test_expert_bank_batched():
-    """64 experts of 2048 x 768 through soap_step_batched, per-expert scale
-    10^U(-4,-2).  Two experts get full oracle parity (open loop over the first
-    steps), every expert the sampled closed-loop checks of the last step."""
-    import paper_2607_20548_amd as soap
-    import oracle
+def test_expert_bank_batched_twenty_steps():
+    """64 experts of 2048 x 768 through soap_step_batched for all 20 steps,
+    per-expert scale 10^U(-4,-2).  Experts 0 and 37 against the oracle every
+    step; every ninth expert by the sampled checks of the last step (factor
+    EMA and momentum entry by entry, the refreshed bases by the properties
+    that fix them, V and N at sampled eigenbasis entries)."""
     from synth import gradients as sg
     wl = sg.workload(3)
-    B, m, n = len(wl.matrices), 2048, 768
-    steps = 3
+    B, m, n, steps = len(wl.matrices), 2048, 768, wl.steps
     scales = sg.expert_scales(0, 3, B)
-    grads = np.stack([np.stack(list(sg.make_matrix_stream(s, 3, steps, scale=scales[e])))
-                      for e, s in enumerate(wl.matrices)], axis=1)      # steps x B x m x n
+    streams = [sg.make_matrix_stream(s, 3, steps, scale=scales[e])
+               for e, s in enumerate(wl.matrices)]
     W0 = np.stack([sg.initial_weight(s, 3) for s in wl.matrices])
-    gs = soap.SoapState(m, n, batch=B)
-    W = dev(W0)
-    check = [0, 37]
-    sts = {e: oracle.init_state(W0[e].astype(np.float64)) for e in check}
-    for t in range(1, steps + 1):
-        if t == steps:
-            pre_all = {k: v for k, v in dict(W=host(W), L=host(gs.L), R=host(gs.R), QL=host(gs.Q_L),
-                                               QR=host(gs.Q_R), M=host(gs.M), V=host(gs.V)).items()}
-        gs.step(W, dev(grads[t - 1]), t, **HP)
-        for e in check:
-            sts[e] = oracle.soap_step(sts[e], grads[t - 1, e].astype(np.float64), t, **HP)
-            for k, a in [("L", "L"), ("R", "R"), ("Q_L", "QL"), ("Q_R", "QR"), ("M", "M"), ("V", "V")]:
-                err = rel(host(getattr(gs, k)[e]), getattr(sts[e], a))
-                assert err <= TOL, (e, t, k, err)
-            assert rel(host(W[e]), sts[e].W) <= TOL
+    gs, W, pre_all, G_last = _batched_open_loop(m, n, streams, steps, W0, [0, 37], "expert bank")
     post_all = dict(W=host(W), L=host(gs.L), R=host(gs.R), QL=host(gs.Q_L), QR=host(gs.Q_R),
                     M=host(gs.M), V=host(gs.V))
     rng = np.random.default_rng(3)
     for e in range(0, B, 9):
         pre = {k: v[e] for k, v in pre_all.items()}
         post = {k: v[e] for k, v in post_all.items()}
-        _sampled_step_checks(pre, post, grads[steps - 1, e].astype(np.float64), steps, rng,
-                             nsamp=32, ncols=8)
+        G = G_last[e].astype(np.float64)
+        check_factor_ema_sampled(pre, post, G, rng, HP["beta2"], 32)
+        check_refresh_adam_sampled(pre, post, G, steps, rng, HP, 32, 8)
     log("expert bank ok")
+
+
+def test_transformer_host_loop_matches_single_matrices():
+    """The 24-layer model's optimizer step as the bench runs it: one
+    soap_step per matrix from one host loop on one stream, each matrix with
+    its own state, the workspace shared by the matrices of a shape.  Two
+    steps; every matrix of layers 0 and 23 then equals, bit for bit, the same
+    matrix stepped alone with a workspace of its own (each of the four shapes
+    is checked against the oracle by test_transformer_layer_shapes_open_loop),
+    and every weight of the model is finite."""
+    import torch
+    import paper_2607_20548_amd as soap
+    from synth import gradients as sg
+    specs = sg.workload(4).matrices
+    steps = 2
+    ws = {}
+    states, weights, grads = [], [], []
+    for sp in specs:
+        key = (sp.m, sp.n)
+        if key not in ws:
+            nb = soap.soap_workspace_bytes(1, sp.m, sp.n)
+            ws[key] = (torch.empty(nb, dtype=torch.uint8, device="cuda"), nb)
+        kw = dict(dtype=torch.float32, device="cuda")
+        st = {k: torch.empty(shp, **kw) for k, shp in
+              [("L", (sp.m, sp.m)), ("R", (sp.n, sp.n)), ("Q_L", (sp.m, sp.m)),
+               ("Q_R", (sp.n, sp.n)), ("M", (sp.m, sp.n)), ("V", (sp.m, sp.n))]}
+        soap.soap_init_state(1, sp.m, sp.n, st["L"], st["R"], st["Q_L"], st["Q_R"], st["M"], st["V"])
+        states.append(st)
+        weights.append(dev(sg.initial_weight(sp, 4)))
+        grads.append([dev(G) for G in sg.make_matrix_stream(sp, 4, steps)])
+    log(f"host loop over {len(specs)} matrices, {steps} steps")
+    hp = (HP["beta1"], HP["beta2"], HP["eps"], HP["lr"], HP["weight_decay"])
+    for t in range(1, steps + 1):
+        for i, sp in enumerate(specs):
+            st = states[i]
+            w, nb = ws[(sp.m, sp.n)]
+            soap.soap_step(weights[i], grads[i][t - 1], st["L"], st["R"], st["Q_L"], st["Q_R"],
+                           st["M"], st["V"], sp.m, sp.n, *hp, t, 0, w, nb)
+    torch.cuda.synchronize()
+    for key, (w, _) in ws.items():
+        assert soap.soap_workspace_status(w) == (soap.SOAP_OK, 0), key
+    for i in range(len(specs)):
+        assert torch.isfinite(weights[i]).all(), specs[i].name
+    for i in list(range(4)) + list(range(len(specs) - 4, len(specs))):
+        sp = specs[i]
+        alone = soap.SoapState(sp.m, sp.n)
+        W = dev(sg.initial_weight(sp, 4))
+        for t in range(1, steps + 1):
+            alone.step(W, grads[i][t - 1], t, **HP)
+        for name, a, b in [("W", W, weights[i])] + [(k, getattr(alone, k), states[i][k])
+                                                    for k in ("L", "R", "Q_L", "Q_R", "M", "V")]:
+            assert torch.equal(a, b), (sp.name, name)
+        log(f"  {sp.name} equal")

@@ -7,7 +7,7 @@ sign)."""
 import numpy as np
 import pytest
 
-from tests.gpu_helpers import dev, host, rel, run_open_loop
+from tests.gpu_helpers import dev, host, rel, run_open_loop, recipe_grads
 
 pytestmark = pytest.mark.gpu
 
@@ -24,8 +24,9 @@ def _lib():
     soap.lib()
 
 
-def _run_open_loop(m, n, grads, W0, hp=HP, flags=0, bias_correction=True):
-    return run_open_loop(m, n, grads, W0, hp=hp, flags=flags, bias_correction=bias_correction)
+def _run_open_loop(m, n, grads, W0, hp=HP, flags=0, bias_correction=True, strict=True):
+    return run_open_loop(m, n, grads, W0, hp=hp, flags=flags, bias_correction=bias_correction,
+                         strict=strict)
 
 
 def test_workload0_ten_steps_open_loop():
@@ -36,18 +37,29 @@ def test_workload0_ten_steps_open_loop():
     _run_open_loop(256, 512, grads, sg.initial_weight(spec, 0))
 
 
-@pytest.mark.parametrize("m,n", [(1, 1), (3, 5), (37, 70), (130, 129), (200, 257)])
+@pytest.mark.parametrize("m,n", [(1, 1), (3, 5), (37, 70), (130, 129), (200, 257), (300, 600),
+                                 (600, 300)])
 def test_ragged_shapes(m, n):
+    """Shapes that are not multiples of the tiles, with gradients of the
+    workloads' recipe (low-rank signal + 10% noise)."""
+    rng = np.random.default_rng([m, n, 21])
+    _run_open_loop(m, n, recipe_grads(m, n, 3, 21),
+                   (0.02 * rng.standard_normal((m, n))).astype(np.float32))
+
+
+@pytest.mark.parametrize("m,n", [(37, 70), (200, 257)])
+def test_ragged_shapes_gaussian_stress(m, n):
+    """Full-rank Gaussian gradients: ill-conditioned factors, checked with the
+    conditioning-aware fp32 intervals (UpdateCheck, strict=False)."""
     rng = np.random.default_rng([m, n, 21])
     grads = [rng.standard_normal((m, n)).astype(np.float32) for _ in range(3)]
-    _run_open_loop(m, n, grads, (0.02 * rng.standard_normal((m, n))).astype(np.float32))
+    _run_open_loop(m, n, grads, (0.02 * rng.standard_normal((m, n))).astype(np.float32),
+                   strict=False)
 
 
 def test_no_bias_correction_flag():
     import paper_2607_20548_amd as soap
-    rng = np.random.default_rng(22)
-    grads = [rng.standard_normal((40, 24)).astype(np.float32) for _ in range(3)]
-    _run_open_loop(40, 24, grads, np.zeros((40, 24), np.float32),
+    _run_open_loop(40, 24, recipe_grads(40, 24, 3, 22), np.zeros((40, 24), np.float32),
                    flags=soap.SOAP_FLAG_NO_BIAS_CORRECTION, bias_correction=False)
 
 
@@ -139,6 +151,6 @@ def test_refresh_period_and_stale_refresh(F, stale):
     and the stale-refresh ablation, against the oracle."""
     rng = np.random.default_rng([F, int(stale), 26])
     m, n = 96, 160
-    grads = [rng.standard_normal((m, n)).astype(np.float32) for _ in range(6)]
-    run_open_loop(m, n, grads, (0.02 * rng.standard_normal((m, n))).astype(np.float32),
+    run_open_loop(m, n, recipe_grads(m, n, 6, 26 + F + 10 * int(stale)),
+                  (0.02 * rng.standard_normal((m, n))).astype(np.float32),
                   refresh_every=F, stale_refresh=stale)
