@@ -31,8 +31,9 @@
  *    the thread-local error string; per device, three internal streams of
  *    default priority (created on first use: the m x m factor's chain and
  *    the block factorizations of both QRs run on them, forked from and
- *    joined back into the caller's stream with events); per host thread, a
- *    pool of up to 4096 HIP events for those forks and joins; per device, the
+ *    joined back into the caller's stream with events); per host thread and
+ *    device, seven HIP events for the step's forks and joins, and per host
+ *    thread a pool of up to 4096 events for those of the QR; per device, the
  *    result of one occupancy query (how many QR block workgroups the device
  *    holds at once); and, while soap_timing_enable(1) is in force, timing
  *    events.

@@ -505,20 +505,23 @@ hipError_t kl_front(int64_t batch, int64_t m, int64_t n, const float *G, float *
   return hipSuccess;
 }
 
-// Owns the events of one step; destroys whichever were created.
+// The fork/join events of a step: seven per host thread and device, created
+// on first use and kept until the process ends.  A step records each at most
+// once and enqueues every wait on it before returning, so the next step may
+// record it again (a wait captures the record current when it is enqueued).
 struct StepEvents {
   static constexpr int kCount = 7;
-  hipEvent_t ev[kCount] = {};
+  hipEvent_t *ev = nullptr;
   hipError_t create() {
-    for (hipEvent_t &e : ev) {
-      hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
-      if (r != hipSuccess) return r;
-    }
+    thread_local hipEvent_t pool[64][kCount] = {};
+    int dev = 0;
+    hipError_t r = hipGetDevice(&dev);
+    if (r != hipSuccess) return r;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    for (hipEvent_t &e : pool[dev])
+      if (!e && (r = hipEventCreateWithFlags(&e, hipEventDisableTiming)) != hipSuccess) return r;
+    ev = pool[dev];
     return hipSuccess;
-  }
-  ~StepEvents() {
-    for (hipEvent_t e : ev)
-      if (e) (void)hipEventDestroy(e);
   }
 };
 
