@@ -131,6 +131,27 @@ int soap_step_batched(int64_t batch, float *param, const float *grad, float *L, 
                       int64_t step, uint32_t flags, void *workspace, size_t workspace_bytes,
                       hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): soap_step
+ * without a workspace argument.  The library's own scratch, a static device
+ * array of SOAP_NOALLOC_MAX_WORKSPACE_BYTES per GPU (held until the process
+ * ends), takes the workspace's place; the call allocates and frees nothing.
+ * Shapes whose soap_workspace_bytes(1, m, n) exceed it are rejected with
+ * SOAP_ERR_WORKSPACE (up to 2048 x 2048 fits).  Arguments, results and errors
+ * otherwise as for soap_step.  Every call on one GPU shares that GPU's
+ * scratch: calls that overlap on one GPU (different streams, or host threads
+ * without ordering) race and must not be issued.  The step clears what it
+ * needs cleared; the scratch keeps the last call's contents.  A QR give-up
+ * keeps the basis as in soap_step, but its status word lives in the scratch
+ * and is not readable through soap_workspace_status.  The first call on a
+ * device and host thread creates the library's streams and events (host-side
+ * objects, no device memory). */
+#define SOAP_NOALLOC_MAX_WORKSPACE_BYTES ((size_t)256 << 20)
+int soap_step_noalloc(float *param, const float *grad, float *L, float *R, float *Q_L,
+                      float *Q_R, float *M, float *V, int64_t m, int64_t n, float beta1,
+                      float beta2, float eps, float lr, float weight_decay, int64_t step,
+                      uint32_t flags, hipStream_t stream);
+
 /* ---- KL-SOAP (the variant the paper recommends: Sections 5.4.3 and 7) ----
  * One KL-SOAP step replaces step 1 of soap_step by the KL-Shampoo accumulation
  * of Algorithm 2.  With the bases and factors of the previous step:

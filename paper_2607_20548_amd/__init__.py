@@ -42,7 +42,7 @@ EXPORTED = [
     "soap_kl_workspace_bytes", "soap_kl_step", "soap_kl_step_batched",
     "soap_kl_factors_workspace_bytes", "soap_kl_factors_f32", "soap_muon_workspace_bytes",
     "soap_muon_step", "soap_muon_step_batched", "soap_workspace_status",
-    "soap_workspace_update_offset", "soap_test_force_qr_give_up",
+    "soap_workspace_update_offset", "soap_test_force_qr_give_up", "soap_step_noalloc",
 ]
 
 
@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
                              _I64, _U32, _P, _SZ, _P]),
         "soap_step_batched": (_INT, [_I64, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F,
                                      _F, _F, _F, _I64, _U32, _P, _SZ, _P]),
+        "soap_step_noalloc": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _F,
+                                     _F, _I64, _U32, _P]),
         "soap_kl_workspace_bytes": (_SZ, [_I64, _I64, _I64]),
         "soap_kl_step": (_INT, [_P, _P, _P, _P, _P, _P, _P, _P, _I64, _I64, _F, _F, _F, _F, _F,
                                 _F, _I64, _U32, _P, _SZ, _P]),
@@ -190,6 +192,16 @@ def soap_step(param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr, we
     _check(lib().soap_step(_ptr(param), _ptr(grad), _ptr(L), _ptr(R), _ptr(Q_L), _ptr(Q_R),
                            _ptr(M), _ptr(V), m, n, beta1, beta2, eps, lr, weight_decay, step,
                            flags, _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+SOAP_NOALLOC_MAX_WORKSPACE_BYTES = 256 << 20
+
+
+def soap_step_noalloc(param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
+                      weight_decay, step, flags, stream=None) -> None:
+    _check(lib().soap_step_noalloc(_ptr(param), _ptr(grad), _ptr(L), _ptr(R), _ptr(Q_L),
+                                   _ptr(Q_R), _ptr(M), _ptr(V), m, n, beta1, beta2, eps, lr,
+                                   weight_decay, step, flags, _stream(stream)))
 
 
 def soap_step_batched(batch, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,

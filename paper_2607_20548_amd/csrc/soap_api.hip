@@ -970,9 +970,62 @@ int muon_impl(int64_t batch, float *param, const float *grad, float *M, int64_t 
   return ok();
 }
 
+// ------------------------------------------------ no-allocation step
+// Scratch of soap_step_noalloc in place of a caller workspace.  Each GPU that
+// loads the library holds its own copy until the process ends.  The array's
+// name is not a device address in host code: the address comes from
+// hipGetSymbolAddress, once per device with that device current, and only
+// that pointer is handed to the kernels.
+constexpr size_t kScratchBytes = SOAP_NOALLOC_MAX_WORKSPACE_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[64] = {};
+
+hipError_t scratch_address(void **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
+
+int soap_step_noalloc(float *param, const float *grad, float *L, float *R, float *Q_L, float *Q_R,
+                      float *M, float *V, int64_t m, int64_t n, float beta1, float beta2,
+                      float eps, float lr, float weight_decay, int64_t step, uint32_t flags,
+                      hipStream_t stream) {
+  // Checks that need no device come first (the step repeats them all).
+  if (!dim_ok(m) || !dim_ok(n))
+    return fail(SOAP_ERR_SHAPE, "m=%lld n=%lld: each must be in [1, %d]", (long long)m,
+                (long long)n, SOAP_MAX_DIM);
+  const size_t need = step_layout(1, m, n, false).total;
+  if (need > kScratchBytes)
+    return fail(SOAP_ERR_WORKSPACE,
+                "a %lld x %lld step needs %zu bytes of scratch; soap_step_noalloc holds %zu "
+                "(call soap_step with a workspace instead)",
+                (long long)m, (long long)n, need, kScratchBytes);
+  const void *ptrs[] = {param, grad, L, R, Q_L, Q_R, M, V};
+  for (const void *p : ptrs)
+    if (!p) return fail(SOAP_ERR_NULL, "a state or gradient pointer is NULL");
+  int rc = check_hparams(beta1, beta2, eps, lr, weight_decay, step, flags);
+  if (rc != SOAP_OK) return rc;
+  void *ws = nullptr;
+  hipError_t e = scratch_address(&ws);
+  if (e != hipSuccess) return hip_fail(e, "scratch address");
+  return step_impl(1, param, grad, L, R, Q_L, Q_R, M, V, m, n, beta1, beta2, eps, lr,
+                   weight_decay, step, flags, ws, kScratchBytes, stream, false, 0.f);
+}
 
 size_t soap_workspace_bytes(int64_t batch, int64_t m, int64_t n) {
   if (!dim_ok(batch) || !dim_ok(m) || !dim_ok(n)) return 0;

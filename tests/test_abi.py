@@ -226,3 +226,17 @@ def test_status_and_diagnostic_entry_points_validate(L):
     assert soap.soap_workspace_update_offset(1, 0, 4) == 0
     # the QR stage's workspace holds its status word, A^T and the QR buffers
     assert soap.soap_qr_workspace_bytes(64) > 4 * 64 * 64
+
+
+def test_noalloc_step_validates_before_touching_the_device(L):
+    a = fake_args()
+    args = lambda **o: [dict(a, **o)[k] for k in ("param", "grad", "L", "R", "Q_L", "Q_R", "M", "V")]
+    hp = (0.9, 0.95, 1e-8, 1e-3, 0.1)
+    assert L.soap_step_noalloc(*args(), 0, 12, *hp, 1, 0, None) == soap.SOAP_ERR_SHAPE
+    assert L.soap_step_noalloc(*args(), 4096, 4096, *hp, 1, 0, None) == soap.SOAP_ERR_WORKSPACE
+    assert "soap_step with a workspace" in soap.soap_last_error()
+    assert L.soap_step_noalloc(*args(param=None), 8, 12, *hp, 1, 0, None) == soap.SOAP_ERR_NULL
+    assert L.soap_step_noalloc(*args(), 8, 12, 1.5, 0.95, 1e-8, 1e-3, 0.1, 1, 0, None) == soap.SOAP_ERR_HPARAM
+    assert L.soap_step_noalloc(*args(), 8, 12, *hp, 0, 0, None) == soap.SOAP_ERR_HPARAM
+    # every shape up to 2048 x 2048 fits the scratch
+    assert soap.soap_workspace_bytes(1, 2048, 2048) <= soap.SOAP_NOALLOC_MAX_WORKSPACE_BYTES
