@@ -88,14 +88,19 @@ def bench_muon(args, soap, torch, sg):
     for t in range(args.warmup):
         state.step(W, grads[t], MUON_COEFFS, bf16=bf, **MUON_HP)
     torch.cuda.synchronize()
-    soap.soap_timing_reset()
-    soap.soap_timing_enable(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(args.steps):
         state.step(W, grads[args.warmup + t], MUON_COEFFS, bf16=bf, stream=stream, **MUON_HP)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    # stage breakdown over separate steps (HIP events around every stage)
+    soap.soap_timing_reset()
+    soap.soap_timing_enable(True)
+    for t in range(args.stage_steps):
+        state.step(W, grads[(args.warmup + t) % total], MUON_COEFFS, bf16=bf, stream=stream,
+                   **MUON_HP)
+    torch.cuda.synchronize()
     soap.soap_timing_enable(False)
     soap.soap_timing_collect()
     stages = {}
@@ -126,7 +131,7 @@ def bench_muon(args, soap, torch, sg):
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": None,
                      "avg_launch_ms": ns_ms / ns_n},
-        "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
+        "stage_ms_per_step": {k: v[0] / max(1, args.stage_steps) for k, v in stages.items()},
     }
     if not args.no_cpu_baseline:
         import oracle
@@ -269,6 +274,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--stage-steps", type=int, default=3,
+                    help="steps run after the timed ones with per-stage HIP events")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibration-copy-mib", type=int, default=0)
     ap.add_argument("--kl", action="store_true", help="time the KL-SOAP step")
@@ -325,14 +332,24 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
 
-    soap.soap_timing_reset()
-    soap.soap_timing_enable(True)
+    # the timed steps run without stage events
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(1, args.steps + 1):
         state.step(W, grads[args.warmup + t - 1], t, stream=stream, **extra, **HP)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    print(f"[bench] timed {args.steps} steps: {1e3 * elapsed / args.steps:.2f} ms/step; "
+          f"stage breakdown over {args.stage_steps} more", file=sys.stderr, flush=True)
+
+    # stage breakdown (HIP events around every stage, on the stream that runs
+    # it) over separate steps, continuing the same run
+    soap.soap_timing_reset()
+    soap.soap_timing_enable(True)
+    for i in range(args.stage_steps):
+        t = args.steps + 1 + i
+        state.step(W, grads[(args.warmup + t - 1) % total], t, stream=stream, **extra, **HP)
+    torch.cuda.synchronize()
     soap.soap_timing_enable(False)
     soap.soap_timing_collect()
 
@@ -344,9 +361,17 @@ def main():
     # sequences of kernels and are reported separately)
     single = {k: v for k, v in stages.items() if k.startswith(("power", "factor", "rotate"))
               and v[1] > 0 and not k.startswith("rotate_in_QLt")}
-    dom = max(single, key=lambda k: single[k][0])
-    d_ms, d_n, d_fl = single[dom]
-    achieved = d_fl / (d_ms / d_n * 1e-3) / d_n / 1e12
+    nst = max(1, args.stage_steps)
+    roofline = None
+    if single:
+        dom = max(single, key=lambda k: single[k][0])
+        d_ms, d_n, d_fl = single[dom]
+        achieved = d_fl / (d_ms / d_n * 1e-3) / d_n / 1e12
+        roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved,
+                    "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / PEAK_FP32_MFMA_TFLOPS,
+                    "traffic": measured_traffic() if dom == "power_R" else None,
+                    "traffic_unit": "HBM bytes per launch", "avg_launch_ms": d_ms / d_n}
 
     F = (kl_step_flops if args.kl else step_flops)(m, n)
     if args.refresh_every > 1:   # the power products and QRs run on 1 step in F
@@ -376,12 +401,20 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "step_tflops": F * value / 1e12,
         "step_frac_of_fp32_mfma_peak": F * value / 1e12 / PEAK_FP32_MFMA_TFLOPS,
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved,
-                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP32_MFMA_TFLOPS, "traffic": measured_traffic(),
-                     "traffic_unit": "HBM bytes per launch", "avg_launch_ms": d_ms / d_n},
-        "stage_ms_per_step": {k: v[0] / args.steps for k, v in stages.items()},
+        "roofline": roofline,
+        "stage_ms_per_step": {k: v[0] / nst for k, v in stages.items() if v[1] > 0},
     }
+    # The eigenbasis QR of the larger factor (n x n): a chain of latency-bound
+    # block factorizations and MFMA updates, timed as one stage.
+    qr_name = "qr_R" if n >= m else "qr_L"
+    q_ms, q_n, q_fl = stages[qr_name]
+    if q_n and q_ms > 0:
+        out["qr"] = {"stage": qr_name, "n": max(m, n), "ms": q_ms / q_n,
+                     "tflops": q_fl / q_n / (q_ms / q_n * 1e-3) / 1e12,
+                     "frac_of_fp32_mfma_peak": q_fl / q_n / (q_ms / q_n * 1e-3) / 1e12
+                     / PEAK_FP32_MFMA_TFLOPS,
+                     "share_of_step": (q_ms / nst) / (1e3 * elapsed / args.steps),
+                     "flops": "(8/3) n^3: Householder factorization and explicit Q"}
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(m, n, spec.rank, kl=args.kl)
