@@ -50,6 +50,7 @@ def build(force: bool = True, verbose: bool = False, extra=(), link_extra=(), ou
     tag = os.path.splitext(os.path.basename(out))[0]
     objdir = os.path.join(BUILD_DIR, tag)
     os.makedirs(objdir, exist_ok=True)
+    os.makedirs(os.path.dirname(os.path.abspath(out)), exist_ok=True)
     objs = [os.path.join(objdir, os.path.basename(src)[:-4] + ".o") for src in SOURCES]
     newest_dep = max(os.path.getmtime(p) for p in HEADERS + [__file__])
 
