@@ -549,16 +549,16 @@ constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (sp
 // A round takes two columns when H_j leaves column j+1 at least this fraction
 // of its squared norm (rows j+1.. after H_j against rows j.. before it).
 constexpr float BK_PAIR_TAU = 0.0625f;
-// exchange area per matrix, in 64-bit items, all by round parity: partials
-// [2][2 sums][BK_MAX_P][NB] and values of workgroup 0 in the diagonal rows j,
-// j+1 [2][2][NB], column k at position (k mod 8) * 16 + k / 8 (the columns of
-// one wave are contiguous), then the abort flag and the failed flag (the low
-// 32 bits of one item each)
-constexpr int64_t BK_XD = 0;
-constexpr int64_t BK_XA = 2 * 2 * (int64_t)BK_MAX_P * NB;
-constexpr int64_t BK_XABORT = BK_XA + 2 * 2 * NB;
-constexpr int64_t BK_XFAILED = BK_XABORT + 1;
-constexpr int64_t BK_XSTRIDE = BK_XABORT + 32;
+// exchange area per matrix, in 64-bit items: the abort flag and the failed
+// flag (the low 32 bits of items 0 and 1), then, by round parity, the
+// partials of the two sums [2][2][BK_MAX_P][NB] and the values of workgroup 0
+// in the diagonal rows j, j+1 [2][2][NB], column k at position
+// (k mod 8) * 16 + k / 8 (the columns of one wave are contiguous)
+constexpr int64_t BK_XABORT = 0;
+constexpr int64_t BK_XFAILED = 1;
+constexpr int64_t BK_XD = 32;
+constexpr int64_t BK_XA = BK_XD + 2 * 2 * (int64_t)BK_MAX_P * NB;
+constexpr int64_t BK_XSTRIDE = BK_XA + 2 * 2 * NB;
 
 struct BlockParams {
   float *At;
@@ -614,18 +614,34 @@ __device__ __forceinline__ bool bk_gather(const unsigned long long *p, int strid
   bool hx = (x == nullptr);
   unsigned spins = 0;
   for (;;) {
+    // The pending items are fetched four at a time: the loads of a group are
+    // issued before any of them is examined (their conditions read the mask
+    // as it stood before the group), so a poll costs about one memory
+    // latency per group rather than one per item, while only four items are
+    // held in registers.
+    unsigned long long itx = 0;
+    if (!hx) itx = bk_get(x);
+    unsigned still = pending;
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (pending & (1u << i)) {
-        const unsigned long long it = bk_get(p + (int64_t)stride * i);
-        v[i] = __uint_as_float((unsigned)it);
-        if ((unsigned)(it >> 32) == gen) pending &= ~(1u << i);
+    for (int i0 = 0; i0 < 16; i0 += 4) {
+      if ((pending >> i0) & 0xFu) {
+        unsigned long long it[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (pending & (1u << (i0 + i))) it[i] = bk_get(p + (int64_t)stride * (i0 + i));
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (pending & (1u << (i0 + i))) {
+            v[i0 + i] = __uint_as_float((unsigned)it[i]);
+            if ((unsigned)(it[i] >> 32) == gen) still &= ~(1u << (i0 + i));
+          }
       }
-    if (!hx) {
-      const unsigned long long it = bk_get(x);
-      xv = __uint_as_float((unsigned)it);
-      hx = (unsigned)(it >> 32) == gen;
     }
+    if (!hx) {
+      xv = __uint_as_float((unsigned)itx);
+      hx = (unsigned)(itx >> 32) == gen;
+    }
+    pending = still;
     if (pending == 0u && hx) break;
     if (bk_give_up(spins, abort_flag)) return false;
   }
@@ -1415,12 +1431,11 @@ hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
   const int P = small ? Ps : (int)((x.n - c + BK_ROWS - 1) / BK_ROWS);
   BlockParams bp{x.At, x.sA, x.ni, c, nb, x.Tb + ob * NB * NB, x.L.sT, x.Rf, x.dsign, x.betas,
                  x.xch, P, x.status, x.status_bit};
+  const dim3 grid((unsigned)P, (unsigned)x.batch);
   if (small)
-    hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL>), dim3((unsigned)P, (unsigned)x.batch),
-                       dim3(BK_THREADS), 0, s, bp);
+    hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL>), grid, dim3(BK_THREADS), 0, s, bp);
   else
-    hipLaunchKernelGGL((qr_block_kernel<BK_R>), dim3((unsigned)P, (unsigned)x.batch),
-                       dim3(BK_THREADS), 0, s, bp);
+    hipLaunchKernelGGL((qr_block_kernel<BK_R>), grid, dim3(BK_THREADS), 0, s, bp);
   return hipGetLastError();
 }
 
