@@ -549,16 +549,35 @@ constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (sp
 // A round takes two columns when H_j leaves column j+1 at least this fraction
 // of its squared norm (rows j+1.. after H_j against rows j.. before it).
 constexpr float BK_PAIR_TAU = 0.0625f;
-// exchange area per matrix, in 64-bit items: the abort flag and the failed
-// flag (the low 32 bits of items 0 and 1), then, by round parity, the
-// partials of the two sums [2][2][BK_MAX_P][NB] and the values of workgroup 0
-// in the diagonal rows j, j+1 [2][2][NB], column k at position
-// (k mod 8) * 16 + k / 8 (the columns of one wave are contiguous)
+// Exchange area per matrix, in 32-bit words: a header (the abort flag, the
+// failed flag), then two slot areas that the outer blocks use in turn.  A
+// round of a block with P workgroups has a slot of its own,
+//   [2][P][NB] partials of the two sums, then [2][NB] values of workgroup 0
+//   in the diagonal rows j, j+1,
+// column k at position (k mod 8) * 16 + k / 8 (the columns of one wave are
+// contiguous).  Every word is written once per call, over the empty pattern
+// BK_EMPTY (a NaN that no post carries: posted NaNs are canonical), so a
+// reader knows a value has arrived from its bits alone and one register
+// holds one pending item.  A block kernel refills, after its rounds, the
+// area that the next block uses (the kernel before it in the same stream
+// used that area last).
 constexpr int64_t BK_XABORT = 0;
 constexpr int64_t BK_XFAILED = 1;
-constexpr int64_t BK_XD = 32;
-constexpr int64_t BK_XA = BK_XD + 2 * 2 * (int64_t)BK_MAX_P * NB;
-constexpr int64_t BK_XSTRIDE = BK_XA + 2 * 2 * NB;
+constexpr int64_t BK_XHDR = 64;
+constexpr unsigned BK_EMPTY = 0xFFFFFFFFu;
+// Workgroups of the widest block launch for order n (the big-R kernel at
+// block 0, or the small-R kernel where it is taken).
+constexpr int64_t bk_max_p(int64_t n) {
+  const int64_t big = (n + BK_ROWS - 1) / BK_ROWS;
+  const int64_t sm = (n + BK_ROWS_SMALL - 1) / BK_ROWS_SMALL;
+  const int64_t s2 = sm < BK_SMALL_MAX_P ? sm : BK_SMALL_MAX_P;
+  return big > s2 ? big : s2;
+}
+// words of one slot area: at most NB rounds per block
+constexpr int64_t bk_area_words(int64_t n) { return (int64_t)NB * (2 * bk_max_p(n) + 2) * NB; }
+constexpr int64_t bk_xstride(int64_t n) { return BK_XHDR + 2 * bk_area_words(n); }
+// words of block ob's slots (rounds <= its columns)
+constexpr int64_t bk_block_words(int64_t nbcols, int P) { return (int64_t)nbcols * (2 * P + 2) * NB; }
 
 struct BlockParams {
   float *At;
@@ -568,18 +587,21 @@ struct BlockParams {
   int64_t sT;
   float *Rf;                 // optional triangular-factor output (batch stride sA)
   float *dsign, *beta;       // n per matrix
-  unsigned long long *xch;   // exchange area, BK_XSTRIDE items per matrix (zeroed per call)
+  unsigned *xch;             // exchange area, xstride words per matrix
+  int64_t xstride, area_words;
+  int area;                  // slot area of this block (0 or 1)
+  int64_t next_words;        // words of the next block's slots (refilled here), or 0
   int P;                     // workgroups per matrix
   unsigned *status;          // caller's status word (or nullptr) ...
   unsigned status_bit;       // ... and the bit a give-up or-s into it
 };
 
-__device__ __forceinline__ void bk_put(unsigned long long *p, float v, unsigned gen) {
-  const unsigned long long item = ((unsigned long long)gen << 32) | __float_as_uint(v);
-  __hip_atomic_store(p, item, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void bk_put(unsigned *p, float v) {
+  const unsigned w = (v != v) ? 0x7FC00000u : __float_as_uint(v);   // never BK_EMPTY
+  __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ __forceinline__ unsigned long long bk_get(const unsigned long long *p) {
+__device__ __forceinline__ unsigned bk_get(const unsigned *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -602,44 +624,31 @@ __device__ __forceinline__ bool bk_give_up(unsigned &spins, unsigned *abort_flag
   return false;
 }
 
-// Waits for generation `gen` of the items p[stride i], i < cnt <= 16, and
-// (if x is not null) of the item x, re-reading only those not yet current;
-// returns the sum of the first in index order and the value of x.  false:
-// aborted.
-__device__ __forceinline__ bool bk_gather(const unsigned long long *p, int stride, int cnt,
-                                          const unsigned long long *x, unsigned gen,
-                                          unsigned *abort_flag, float &sum, float &xv) {
-  float v[16];
+// Waits for the items p[stride i], i < cnt <= 16, and (if x is not null)
+// the item x, re-reading only those still empty; returns the sum of the
+// first in index order and the value of x.  All pending items are fetched
+// at once (their loads issued before any is examined), so a poll costs about
+// one memory latency however many items there are.  false: aborted.
+__device__ __forceinline__ bool bk_gather(const unsigned *p, int stride, int cnt,
+                                          const unsigned *x, unsigned *abort_flag, float &sum,
+                                          float &xv) {
+  unsigned v[16];
   unsigned pending = (1u << cnt) - 1u;
   bool hx = (x == nullptr);
   unsigned spins = 0;
   for (;;) {
-    // The pending items are fetched four at a time: the loads of a group are
-    // issued before any of them is examined (their conditions read the mask
-    // as it stood before the group), so a poll costs about one memory
-    // latency per group rather than one per item, while only four items are
-    // held in registers.
-    unsigned long long itx = 0;
-    if (!hx) itx = bk_get(x);
+    unsigned vx = 0;
+    if (!hx) vx = bk_get(x);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (pending & (1u << i)) v[i] = bk_get(p + (int64_t)stride * i);
     unsigned still = pending;
 #pragma unroll
-    for (int i0 = 0; i0 < 16; i0 += 4) {
-      if ((pending >> i0) & 0xFu) {
-        unsigned long long it[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (pending & (1u << (i0 + i))) it[i] = bk_get(p + (int64_t)stride * (i0 + i));
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          if (pending & (1u << (i0 + i))) {
-            v[i0 + i] = __uint_as_float((unsigned)it[i]);
-            if ((unsigned)(it[i] >> 32) == gen) still &= ~(1u << (i0 + i));
-          }
-      }
-    }
-    if (!hx) {
-      xv = __uint_as_float((unsigned)itx);
-      hx = (unsigned)(itx >> 32) == gen;
+    for (int i = 0; i < 16; ++i)
+      if ((pending & (1u << i)) && v[i] != BK_EMPTY) still &= ~(1u << i);
+    if (!hx && vx != BK_EMPTY) {
+      xv = __uint_as_float(vx);
+      hx = true;
     }
     pending = still;
     if (pending == 0u && hx) break;
@@ -648,7 +657,7 @@ __device__ __forceinline__ bool bk_gather(const unsigned long long *p, int strid
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < 16; ++i)
-    if (i < cnt) s += v[i];
+    if (i < cnt) s += __uint_as_float(v[i]);
   sum = s;
   return true;
 }
@@ -739,8 +748,10 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   const int r0 = c + g * RS;
   const bool w0 = (g == 0);
   const bool col = k < nb;
-  unsigned long long *X = p.xch + bz * BK_XSTRIDE;
-  unsigned *abort_flag = reinterpret_cast<unsigned *>(X + BK_XABORT);
+  unsigned *X = p.xch + bz * p.xstride;
+  unsigned *abort_flag = X + BK_XABORT;
+  unsigned *slots = X + BK_XHDR + p.area * p.area_words;   // this block's rounds
+  const int64_t slot_words = (int64_t)(2 * P + 2) * NB;
 
   float a[NI][4];
   {
@@ -786,7 +797,6 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   int j = 0;
   for (int round = 0; j < nb; ++round) {
     const int par = round & 1;
-    const unsigned gen = (unsigned)(c + round + 1);   // rounds <= columns: unique per call
     const bool two = j + 1 < nb;
     // lane part and register index (i * 4 + e) of the diagonal rows j, j+1
     // in workgroup 0 (local row BK_LI i + 4 part + e)
@@ -837,17 +847,16 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       // 4..7 those of E; lanes 3 and 7 also fetch A and B from workgroup 0.
       const int64_t pk = (int64_t)(wave * (64 / BK_PARTS) + lane / BK_PARTS);   // position of column k
       const int q = part >> 2, u0 = part & 3;
-      if (col && (part == 0 || part == 4))
-        bk_put(X + BK_XD + (((int64_t)par * 2 + q) * BK_MAX_P + g) * NB + pk, q ? ev : d, gen);
+      unsigned *slot = slots + (int64_t)round * slot_words;
+      if (col && (part == 0 || part == 4)) bk_put(slot + ((int64_t)q * P + g) * NB + pk, q ? ev : d);
       if (w0 && col && (part == 1 || part == 5))
-        bk_put(X + BK_XA + ((int64_t)par * 2 + q) * NB + pk, q ? av1 : av0, gen);
+        bk_put(slot + ((int64_t)2 * P + q) * NB + pk, q ? av1 : av0);
       if (col && (w0 || k >= j)) {
         float ssum = 0.f, xv = 0.f;
         if (alive)
-          alive = bk_gather(X + BK_XD + (((int64_t)par * 2 + q) * BK_MAX_P + u0) * NB + pk, 4 * NB,
-                            (P - u0 + 3) / 4,
-                            (!w0 && u0 == 3) ? X + BK_XA + ((int64_t)par * 2 + q) * NB + pk : nullptr,
-                            gen, abort_flag, ssum, xv);
+          alive = bk_gather(slot + ((int64_t)q * P + u0) * NB + pk, 4 * NB, (P - u0 + 3) / 4,
+                            (!w0 && u0 == 3) ? slot + ((int64_t)2 * P + q) * NB + pk : nullptr,
+                            abort_flag, ssum, xv);
         bk_pair4(ssum, part < 4, D, E);
         float aa, bb;
         bk_bcast4(xv, part < 4, aa, bb);
@@ -1004,8 +1013,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   const bool bad =
       P > 1 && __hip_atomic_load(abort_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
   if (bad && t == 0) {   // the factorization of this matrix failed: no Q is formed from it
-    __hip_atomic_store(reinterpret_cast<unsigned *>(X + BK_XFAILED), 1u, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(X + BK_XFAILED, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (p.status)
       __hip_atomic_fetch_or(p.status, p.status_bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -1028,6 +1036,13 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
           dst[row] = bad ? nan : v;
         }
       }
+  }
+  // The next block's slots (the other area) back to the empty pattern.
+  if (p.next_words > 0) {
+    uint4 *nx = reinterpret_cast<uint4 *>(X + BK_XHDR + (1 - p.area) * p.area_words);
+    const uint4 e4 = make_uint4(BK_EMPTY, BK_EMPTY, BK_EMPTY, BK_EMPTY);
+    for (int64_t i = (int64_t)g * BK_THREADS + t; i < p.next_words / 4; i += (int64_t)P * BK_THREADS)
+      nx[i] = e4;
   }
   if (!w0) return;
   // T by blocks of 8 columns: first every diagonal block T_JJ (rows of one
@@ -1245,10 +1260,21 @@ __global__ __launch_bounds__(256) void qr_q_head_kernel(float *W, int64_t ldw, i
 
 // Raises the abort flag of each of `batch` exchange areas (the forced
 // give-up of qr_force_give_up).
-__global__ __launch_bounds__(64) void qr_raise_abort_kernel(unsigned long long *xch, int64_t batch) {
+__global__ __launch_bounds__(64) void qr_raise_abort_kernel(unsigned *xch, int64_t xstride,
+                                                            int64_t batch) {
   for (int64_t b = blockIdx.x * 64 + threadIdx.x; b < batch; b += (int64_t)gridDim.x * 64)
-    __hip_atomic_store(reinterpret_cast<unsigned *>(xch + b * BK_XSTRIDE + BK_XABORT), 1u,
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(xch + b * xstride + BK_XABORT, 1u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exchange areas at the start of a call: header words zero, the first
+// block's slots (the first `first` words of area 0) empty.
+__global__ __launch_bounds__(256) void qr_xch_init_kernel(unsigned *xch, int64_t xstride,
+                                                          int64_t first) {
+  unsigned *X = xch + (int64_t)blockIdx.y * xstride;
+  const int64_t cnt = BK_XHDR + first;
+  for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < cnt; i += (int64_t)gridDim.x * 256)
+    X[i] = (i < BK_XHDR) ? 0u : BK_EMPTY;
 }
 
 // dst = src^T for one n x n matrix, through 32 x 32 LDS tiles.
@@ -1333,7 +1359,7 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   const int64_t P0 = (n + BK_ROWS - 1) / BK_ROWS;
   L.block = P0 <= BK_MAX_P && P0 * batch <= BK_MAX_WG;
   L.x_off = o;
-  if (L.block) o = align256(o + sizeof(unsigned long long) * batch * BK_XSTRIDE);
+  if (L.block) o = align256(o + sizeof(unsigned) * batch * bk_xstride(n));
   L.total = o;
   return L;
 }
@@ -1405,7 +1431,7 @@ struct QrCtx {
   unsigned status_bit;
   float *Tb, *Wb, *W2, *Sk, *Pt, *Wi, *dsign, *betas;
   unsigned *cnt;
-  unsigned long long *xch;
+  unsigned *xch;
   float *TP, *Sx, *Skp, *TQ, *Sq, *TO, *So;
 };
 
@@ -1421,16 +1447,30 @@ int narrow_split(int64_t M, int64_t N, int64_t K, int64_t batch, int64_t cap_flo
   return (int)std::max<int64_t>(1, s);
 }
 
+// Workgroups of block ob's resident-block launch and whether it takes the
+// small-R kernel.
+int block_launch_p(const QrCtx &x, int64_t ob, bool *small) {
+  const int64_t c = ob * NB;
+  const int Ps = (int)((x.n - c + BK_ROWS_SMALL - 1) / BK_ROWS_SMALL);
+  *small = Ps <= BK_SMALL_MAX_P && Ps * x.batch <= x.cap_small;
+  return *small ? Ps : (int)((x.n - c + BK_ROWS - 1) / BK_ROWS);
+}
+
 // Factors outer block ob on stream s (resident-block kernel or panel path).
 hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
   if (!x.L.block) return panel_phase(x, ob, s);
   const int c = (int)(ob * NB);
   const int nb = (int)std::min<int64_t>(NB, x.n - c);
-  const int Ps = (int)((x.n - c + BK_ROWS_SMALL - 1) / BK_ROWS_SMALL);
-  const bool small = Ps <= BK_SMALL_MAX_P && Ps * x.batch <= x.cap_small;
-  const int P = small ? Ps : (int)((x.n - c + BK_ROWS - 1) / BK_ROWS);
+  bool small = false, small_next = false;
+  const int P = block_launch_p(x, ob, &small);
+  int64_t next_words = 0;
+  if (c + nb < x.n) {
+    const int Pn = block_launch_p(x, ob + 1, &small_next);
+    next_words = bk_block_words(std::min<int64_t>(NB, x.n - c - nb), Pn);
+  }
   BlockParams bp{x.At, x.sA, x.ni, c, nb, x.Tb + ob * NB * NB, x.L.sT, x.Rf, x.dsign, x.betas,
-                 x.xch, P, x.status, x.status_bit};
+                 x.xch, bk_xstride(x.n), bk_area_words(x.n), (int)(ob & 1), next_words, P,
+                 x.status, x.status_bit};
   const dim3 grid((unsigned)P, (unsigned)x.batch);
   if (small)
     hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL>), grid, dim3(BK_THREADS), 0, s, bp);
@@ -1722,7 +1762,7 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   x.dsign = reinterpret_cast<float *>(base + x.L.d_off);
   x.betas = reinterpret_cast<float *>(base + x.L.b_off);
   x.cnt = reinterpret_cast<unsigned *>(base + x.L.cnt_off);
-  x.xch = reinterpret_cast<unsigned long long *>(base + x.L.x_off);
+  x.xch = reinterpret_cast<unsigned *>(base + x.L.x_off);
   x.TP = reinterpret_cast<float *>(base + x.L.tp_off);
   x.Sx = reinterpret_cast<float *>(base + x.L.sx_off);
   x.Skp = reinterpret_cast<float *>(base + x.L.skp_off);
@@ -1735,14 +1775,20 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
   x.skip = nullptr;
   x.sSkip = 0;
-  if (x.L.block) {  // generations restart at 1 every call: clear the old items and flags
-    SOAP_TRY(launch_zero_u32(reinterpret_cast<uint32_t *>(x.xch), 2 * batch * BK_XSTRIDE, s));
-    x.skip = reinterpret_cast<const unsigned *>(x.xch + BK_XFAILED);
-    x.sSkip = 2 * BK_XSTRIDE;
+  if (x.L.block) {  // every slot is written once per call: header clear, block 0's slots empty
+    const int64_t xs = bk_xstride(n);
+    bool small0 = false;
+    const int64_t first = bk_block_words(std::min<int64_t>(NB, n), block_launch_p(x, 0, &small0));
+    const unsigned gx = (unsigned)std::min<int64_t>((BK_XHDR + first + 255) / 256, 1024);
+    hipLaunchKernelGGL(qr_xch_init_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, x.xch, xs,
+                       first);
+    SOAP_TRY(hipGetLastError());
+    x.skip = x.xch + BK_XFAILED;
+    x.sSkip = xs;
     if (g_force_give_up.load() & status_bit) {
       hipLaunchKernelGGL(qr_raise_abort_kernel,
                          dim3((unsigned)std::min<int64_t>((batch + 63) / 64, 1024)), dim3(64), 0,
-                         s, x.xch, batch);
+                         s, x.xch, xs, batch);
       SOAP_TRY(hipGetLastError());
     }
   }
