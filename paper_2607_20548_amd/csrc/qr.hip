@@ -1101,11 +1101,13 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
 }
 
 // Final triangular factor: entries of an earlier outer block than their column
-// come from At, entries inside an outer block were stored by the panels; every
-// row i is then scaled by d_i so that diag(R) >= 0.  Strict lower part = 0.
+// come from At, except the squares of full pairs (rows of block 2p, columns
+// of block 2p+1, p < np), which the factorization moved to Rf already scaled;
+// entries inside an outer block were stored by the panels; every row i is
+// then scaled by d_i so that diag(R) >= 0.  Strict lower part = 0.
 __global__ __launch_bounds__(256) void qr_extract_r_kernel(const float *At, float *Rf,
                                                            const float *dsign, int n,
-                                                           int64_t sA) {
+                                                           int64_t sA, int np) {
   const int64_t bz = blockIdx.y;
   const float *Ab = At + bz * sA;
   float *Rb = Rf + bz * sA;
@@ -1113,8 +1115,30 @@ __global__ __launch_bounds__(256) void qr_extract_r_kernel(const float *At, floa
   const int64_t nn = (int64_t)n * n;
   for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += (int64_t)gridDim.x * 256) {
     const int i = (int)(e / n), j = (int)(e % n);
+    const int bi = i / NB, bj = j / NB;
     if (i > j) Rb[e] = 0.f;
-    else Rb[e] = d[i] * ((i / NB < j / NB) ? Ab[(int64_t)j * n + i] : Rb[e]);
+    else if ((bi & 1) == 0 && bj == bi + 1 && bi / 2 < np) continue;   // moved already
+    else Rb[e] = d[i] * ((bi < bj) ? Ab[(int64_t)j * n + i] : Rb[e]);
+  }
+}
+
+// Full pair p = (blocks a, b = a + 1) once both are factored: the R entries
+// of block b's columns in block a's rows (At[c_b + j][c_a + i], i, j < NB)
+// are final; they move to Rf (scaled by d of their row) when it is wanted,
+// and are cleared in At, so that rows c_a..c_a+2NB of At from column c_a on
+// hold the pair's unit lower-trapezoidal Y for the rank-2NB updates.
+__global__ __launch_bounds__(256) void qr_clear_pair_square_kernel(float *At, int64_t sA,
+                                                                   float *Rf,
+                                                                   const float *dsign, int n,
+                                                                   int ca) {
+  const int64_t bz = blockIdx.y;
+  float *Ab = At + bz * sA;
+  const int cb = ca + NB;
+  for (int e = blockIdx.x * 256 + threadIdx.x; e < NB * NB; e += gridDim.x * 256) {
+    const int j = e / NB, i = e % NB;   // column cb + j, row ca + i
+    float *src = Ab + (int64_t)(cb + j) * n + ca + i;
+    if (Rf) Rf[bz * sA + (int64_t)(ca + i) * n + cb + j] = dsign[bz * n + ca + i] * *src;
+    *src = 0.f;
   }
 }
 
@@ -1298,8 +1322,9 @@ struct QrLayout {
   int64_t n, nob;
   bool block;          // outer blocks factored by qr_block_kernel (else the panel path)
   size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, x_off, total;
-  size_t tp_off, sx_off, skp_off, tq_off, sq_off, to_off, so_off;
+  size_t tp_off, sx_off, skp_off, skp2_off, tq_off, sq_off, to_off, so_off, wn_off, skn_off;
   int64_t sT, sWbuf, sSk, sPart, sWi;
+  int64_t sWn, sSkn;   // the near update's own W, W2 (NB x NB each) and split-K partials
   int64_t np;          // pairs of full outer blocks
   int64_t nq;          // quads (pairs of full pairs)
   int64_t no;          // octs (pairs of full quads), for n >= OCT_MIN_N
@@ -1330,6 +1355,8 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.sTP = L.np * 4 * NB * NB;
   L.sSx = L.np * 2 * NB * NB;
   L.sSkp = (int64_t)64 * NB * NB;
+  L.sWn = (int64_t)2 * NB * NB;
+  L.sSkn = std::max<int64_t>(1, std::min<int64_t>(64, n / 256)) * NB * NB;
   L.sTQ = L.nq * 16 * NB * NB;
   L.sSq = L.nq * 8 * NB * NB;
   L.sTO = L.no * 64 * NB * NB;
@@ -1349,10 +1376,13 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.tp_off = o;   o = align256(o + sizeof(float) * batch * L.sTP);
   L.sx_off = o;   o = align256(o + sizeof(float) * batch * L.sSx);
   L.skp_off = o;  o = align256(o + sizeof(float) * batch * L.sSkp);
+  L.skp2_off = o; o = align256(o + sizeof(float) * batch * L.sSkp);
   L.tq_off = o;   o = align256(o + sizeof(float) * batch * L.sTQ);
   L.sq_off = o;   o = align256(o + sizeof(float) * batch * L.sSq);
   L.to_off = o;   o = align256(o + sizeof(float) * batch * L.sTO);
   L.so_off = o;   o = align256(o + sizeof(float) * batch * L.sSo);
+  L.wn_off = o;   o = align256(o + sizeof(float) * batch * L.sWn);
+  L.skn_off = o;  o = align256(o + sizeof(float) * batch * L.sSkn);
   // The resident-block path needs every workgroup of a launch resident at
   // once: at most BK_MAX_WG workgroups (two such launches, one per factor,
   // may run together on the 256 compute units).
@@ -1433,6 +1463,8 @@ struct QrCtx {
   unsigned *cnt;
   unsigned *xch;
   float *TP, *Sx, *Skp, *TQ, *Sq, *TO, *So;
+  float *Wn, *Skn;
+  float *Skp2;     // split-K partials of the pair T's (the merges use Skp)
 };
 
 hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
@@ -1518,21 +1550,29 @@ hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s) {
 
 // Applies outer block ob's reflectors to the columns [j0, j1) of A (rows c..n):
 // A[c:, j0:j1] -= Y (T^T (Y^T A[c:, j0:j1])), on stream s.
-hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, hipStream_t s) {
+hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, hipStream_t s,
+                           bool near) {
   const int64_t n = x.n;
   const int64_t c = ob * NB;
   const int64_t nb = std::min<int64_t>(n, c + NB) - c, Kr = n - c, Nt = j1 - j0;
   if (Nt <= 0) return hipSuccess;
   float *Tob = x.Tb + ob * NB * NB;
+  // The near update runs beside the others on its own stream: its own
+  // buffers.  Only narrow updates (at most NB columns) go there.
+  float *Wb = near ? x.Wn : x.Wb, *W2 = near ? x.Wn + NB * NB : x.W2;
+  float *Sk = near ? x.Skn : x.Sk;
+  const int64_t sW = near ? x.L.sWn : x.L.sWbuf;
+  const int64_t skcap = x.batch * (near ? x.L.sSkn : x.L.sSk);
+  if (near && Nt > NB) return hipErrorInvalidValue;
   // W = Y^T A[c:n, j0:j1]:  W[i][j] = sum_k At[c+i][c+k] At[j0+j][c+k]
   GemmDesc g1;
   g1.trans_a = 0; g1.trans_b = 1; g1.M = nb; g1.N = Nt; g1.K = Kr;
   g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
   g1.B = x.At + j0 * n + c; g1.ldb = n; g1.sB = x.sA;
-  g1.C = x.Wb; g1.ldc = Nt; g1.sC = x.L.sWbuf; g1.batch = x.batch;
-  g1.splitk = (Nt <= NB) ? narrow_split(nb, Nt, Kr, x.batch, x.batch * x.L.sSk)
+  g1.C = Wb; g1.ldc = Nt; g1.sC = sW; g1.batch = x.batch;
+  g1.splitk = (Nt <= NB) ? narrow_split(nb, Nt, Kr, x.batch, skcap)
                           : choose_splitk(nb, Nt, Kr, x.batch, MAX_SPLIT);
-  g1.part = x.Sk;
+  g1.part = Sk;
   // split products sum their slices and form T^T W in one pass (the near
   // update is on the critical path, and so are the far updates of the first
   // half of a large factorization)
@@ -1541,20 +1581,52 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   SOAP_TRY(launch_gemm(g1, s));
   if (fused) {   // W2 = T^T (sum of the partials) in one pass
     hipLaunchKernelGGL(qr_reduce_tt_kernel, dim3((unsigned)((Nt + 7) / 8), (unsigned)x.batch),
-                       dim3(256), 0, s, x.Sk, g1.splitk, (int)nb, (int)Nt, Tob, x.L.sT, x.W2,
-                       x.L.sWbuf);
+                       dim3(256), 0, s, Sk, g1.splitk, (int)nb, (int)Nt, Tob, x.L.sT, W2, sW);
     SOAP_TRY(hipGetLastError());
   }
   // W2 = T^T W
   GemmDesc g2;
   g2.trans_a = 1; g2.trans_b = 0; g2.M = nb; g2.N = Nt; g2.K = nb;
   g2.A = Tob; g2.lda = NB; g2.sA = x.L.sT;
-  g2.B = x.Wb; g2.ldb = Nt; g2.sB = x.L.sWbuf;
-  g2.C = x.W2; g2.ldc = Nt; g2.sC = x.L.sWbuf; g2.batch = x.batch;
+  g2.B = Wb; g2.ldb = Nt; g2.sB = sW;
+  g2.C = W2; g2.ldc = Nt; g2.sC = sW; g2.batch = x.batch;
   if (!fused) SOAP_TRY(launch_gemm(g2, s));
   // At[j0+j][c+k] -= sum_i W2[i][j] Y[k][i]
   GemmDesc g3;
   g3.trans_a = 1; g3.trans_b = 0; g3.M = Nt; g3.N = Kr; g3.K = nb;
+  g3.A = W2; g3.lda = Nt; g3.sA = sW;
+  g3.B = x.At + c * n + c; g3.ldb = n; g3.sB = x.sA;
+  g3.C = x.At + j0 * n + c; g3.ldc = n; g3.sC = x.sA;
+  g3.alpha = -1.f; g3.beta = 1.f; g3.batch = x.batch;
+  return launch_gemm(g3, s);
+}
+
+// Trailing update of columns j0..n-1 by full pair p (blocks 2p, 2p+1) at
+// once, with the pair's T (2NB x 2NB): W = Y^T A[c:n, j0:n] (K = n - c),
+// W2 = T^T W, A[c:n, j0:n] -= Y W2 (K = 2NB), c = 2p NB.  Needs the pair's
+// square cleared (Y unit lower trapezoidal over rows c.. of the 2NB rows of
+// At) and T_p formed.  Rank 2NB: half the passes over the trailing matrix
+// of two rank-NB updates, at a higher matrix-core rate.
+hipError_t far_update_pair(const QrCtx &x, int64_t p, int64_t j0, hipStream_t s) {
+  const int64_t n = x.n, c = 2 * p * NB, w = 2 * NB, Kr = n - c, Nt = n - j0;
+  if (Nt <= 0) return hipSuccess;
+  const float *Tp = x.TP + p * 4 * NB * NB;
+  GemmDesc g1;  // W[i][j] = sum_k At[c+i][c+k] At[j0+j][c+k]
+  g1.trans_a = 0; g1.trans_b = 1; g1.M = w; g1.N = Nt; g1.K = Kr;
+  g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
+  g1.B = x.At + j0 * n + c; g1.ldb = n; g1.sB = x.sA;
+  g1.C = x.Wb; g1.ldc = Nt; g1.sC = x.L.sWbuf; g1.batch = x.batch;
+  g1.splitk = choose_splitk(w, Nt, Kr, x.batch, MAX_SPLIT);
+  g1.part = x.Sk;
+  SOAP_TRY(launch_gemm(g1, s));
+  GemmDesc g2;  // W2 = T^T W
+  g2.trans_a = 1; g2.trans_b = 0; g2.M = w; g2.N = Nt; g2.K = w;
+  g2.A = Tp; g2.lda = w; g2.sA = x.L.sTP;
+  g2.B = x.Wb; g2.ldb = Nt; g2.sB = x.L.sWbuf;
+  g2.C = x.W2; g2.ldc = Nt; g2.sC = x.L.sWbuf; g2.batch = x.batch;
+  SOAP_TRY(launch_gemm(g2, s));
+  GemmDesc g3;  // At[j0+j][c+k] -= sum_i W2[i][j] Y[k][i]
+  g3.trans_a = 1; g3.trans_b = 0; g3.M = Nt; g3.N = Kr; g3.K = w;
   g3.A = x.W2; g3.lda = Nt; g3.sA = x.L.sWbuf;
   g3.B = x.At + c * n + c; g3.ldb = n; g3.sB = x.sA;
   g3.C = x.At + j0 * n + c; g3.ldc = n; g3.sC = x.sA;
@@ -1562,11 +1634,13 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   return launch_gemm(g3, s);
 }
 
-// T of pair p (full blocks a = 2p, b = 2p+1), on stream st:
+// T of pair p (full blocks a = 2p, b = 2p+1), on stream st (the stream
+// that then applies the pair's far update):
 //   S = Y_a^T Y_b over rows >= c_b (where Y_b is nonzero), X = T_a S,
 //   T_ab = -X T_b into the top-right block of the pair's T, then the
 //   diagonal blocks.  Reads only At rows of the two blocks at columns >= c_b
-//   and their T, which the concurrent trailing update does not touch.
+//   and their T, which the concurrent updates and factorizations do not
+//   touch.  Its split-K partials are its own (the merges run beside it).
 hipError_t pair_t(const QrCtx &x, int64_t p, hipStream_t st) {
   const int64_t n = x.n, ca = 2 * p * NB, cb = ca + NB;
   float *S = x.Sx + p * 2 * NB * NB, *X = S + NB * NB;
@@ -1578,7 +1652,7 @@ hipError_t pair_t(const QrCtx &x, int64_t p, hipStream_t st) {
   gs.B = x.At + cb * n + cb; gs.ldb = n; gs.sB = x.sA;
   gs.C = S; gs.ldc = NB; gs.sC = x.L.sSx; gs.batch = x.batch;
   gs.splitk = narrow_split(NB, NB, n - cb, x.batch, x.batch * x.L.sSkp);
-  gs.part = x.Skp;
+  gs.part = x.Skp2;
   SOAP_TRY(launch_gemm(gs, st));
   GemmDesc gx;  // X = T_a S
   gx.M = NB; gx.N = NB; gx.K = NB;
@@ -1766,10 +1840,13 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   x.TP = reinterpret_cast<float *>(base + x.L.tp_off);
   x.Sx = reinterpret_cast<float *>(base + x.L.sx_off);
   x.Skp = reinterpret_cast<float *>(base + x.L.skp_off);
+  x.Skp2 = reinterpret_cast<float *>(base + x.L.skp2_off);
   x.TQ = reinterpret_cast<float *>(base + x.L.tq_off);
   x.Sq = reinterpret_cast<float *>(base + x.L.sq_off);
   x.TO = reinterpret_cast<float *>(base + x.L.to_off);
   x.So = reinterpret_cast<float *>(base + x.L.so_off);
+  x.Wn = reinterpret_cast<float *>(base + x.L.wn_off);
+  x.Skn = reinterpret_cast<float *>(base + x.L.skn_off);
   const int64_t nob = x.L.nob, np = x.L.np;
 
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
@@ -1793,48 +1870,70 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     }
   }
 
-  // Look-ahead: block ob+1's columns are updated first (the "near" update),
-  // then block ob+1 is factored on the panel stream while this stream applies
-  // the rest of block ob's trailing update.
+  // Look-ahead of depth two.  The block stream sp carries the critical
+  // chain: block ob+1's columns updated by block ob (the "near" update),
+  // then block ob+1 factored.  Stream s applies the rest of block ob's
+  // trailing update once block ob is factored: block by block to the
+  // columns of blocks ob+2 and (ob even) ob+3, which the next near updates
+  // wait for; the columns past those by pairs of blocks: once block 2p+1 is
+  // factored, the pair's T is formed and the pair updates every column from
+  // block 2p+4 on at once (rank 2NB), while blocks 2p+2 and 2p+3 are
+  // factored.  The quad and oct T's of the Q formation follow on st.
   hipEvent_t ev;
   SOAP_TRY(t_events.get(&ev));
   SOAP_TRY(hipEventRecord(ev, s));
   SOAP_TRY(hipStreamWaitEvent(sp, ev, 0));
   SOAP_TRY(factor_block(x, 0, sp));
-  SOAP_TRY(t_events.get(&ev));
-  SOAP_TRY(hipEventRecord(ev, sp));
-  SOAP_TRY(hipStreamWaitEvent(s, ev, 0));        // block 0 factored
+  hipEvent_t ev_f;                                // block ob factored (on sp)
+  SOAP_TRY(t_events.get(&ev_f));
+  SOAP_TRY(hipEventRecord(ev_f, sp));
+  hipEvent_t ev_a = nullptr;                      // block ob+1's columns current (on s)
   const int64_t mid_ob = (int64_t)(mid_frac * (float)nob);
   bool mid_done = (mid == nullptr && !at_mid);
+  auto col0 = [&](int64_t b) { return std::min<int64_t>(n, b * NB); };
   for (int64_t ob = 0; ob < nob; ++ob) {
-    const int64_t cend = std::min<int64_t>(n, (ob + 1) * NB);
     if (!mid_done && ob >= mid_ob) {
       if (mid) SOAP_TRY(hipEventRecord(mid, s));
       if (at_mid) SOAP_TRY(at_mid());
       mid_done = true;
     }
-    if (cend >= n) break;
-    const int64_t cend2 = std::min<int64_t>(n, cend + NB);
-    SOAP_TRY(trailing_update(x, ob, cend, cend2, s));          // near: block ob+1
-    SOAP_TRY(t_events.get(&ev));
-    SOAP_TRY(hipEventRecord(ev, s));
-    SOAP_TRY(hipStreamWaitEvent(sp, ev, 0));
-    SOAP_TRY(factor_block(x, ob + 1, sp));                      // factor block ob+1
-    hipEvent_t ev_panel;
-    SOAP_TRY(t_events.get(&ev_panel));
-    SOAP_TRY(hipEventRecord(ev_panel, sp));
-    if ((ob + 1) % 2 == 1 && (ob + 1) / 2 < np) {               // pair (ob, ob+1) complete
-      SOAP_TRY(hipStreamWaitEvent(st, ev_panel, 0));
-      const int64_t p = (ob + 1) / 2;
-      SOAP_TRY(pair_t(x, p, st));
+    hipEvent_t ev_next = nullptr;
+    if (ob + 1 < nob) {
+      if (ev_a) SOAP_TRY(hipStreamWaitEvent(sp, ev_a, 0));
+      SOAP_TRY(trailing_update(x, ob, col0(ob + 1), col0(ob + 2), sp, true));  // near
+      SOAP_TRY(factor_block(x, ob + 1, sp));
+      SOAP_TRY(t_events.get(&ev_next));
+      SOAP_TRY(hipEventRecord(ev_next, sp));
+    }
+    SOAP_TRY(hipStreamWaitEvent(s, ev_f, 0));                   // block ob factored
+    ev_a = nullptr;
+    if (ob + 2 < nob) {                                         // block ob+2's columns
+      SOAP_TRY(trailing_update(x, ob, col0(ob + 2), col0(ob + 3), s, false));
+      SOAP_TRY(t_events.get(&ev_a));
+      SOAP_TRY(hipEventRecord(ev_a, s));
+    }
+    if (ob % 2 == 0) {
+      if (ob + 3 < nob)                                         // block ob+3's columns
+        SOAP_TRY(trailing_update(x, ob, col0(ob + 3), col0(ob + 4), s, false));
+    } else if (ob / 2 < np) {                                   // pair (ob-1, ob) complete
+      const int64_t p = ob / 2;
+      hipLaunchKernelGGL(qr_clear_pair_square_kernel, dim3(64, (unsigned)batch), dim3(256), 0, s,
+                         x.At, x.sA, x.Rf, x.dsign, x.ni, (int)((ob - 1) * NB));
+      SOAP_TRY(hipGetLastError());
+      SOAP_TRY(pair_t(x, p, s));
       if (p % 2 == 1 && p / 2 < x.L.nq) {                  // quad (p-1, p) complete
+        SOAP_TRY(t_events.get(&ev));
+        SOAP_TRY(hipEventRecord(ev, s));
+        SOAP_TRY(hipStreamWaitEvent(st, ev, 0));
         const int64_t q = p / 2;
         SOAP_TRY(merge_t(x, 2, q, st));
         if (q % 2 == 1 && q / 2 < x.L.no) SOAP_TRY(merge_t(x, 3, q / 2, st));   // oct (q-1, q)
       }
+      if (ob + 3 < nob) SOAP_TRY(far_update_pair(x, p, col0(ob + 3), s));   // blocks ob+3..
+    } else if (ob + 3 < nob) {
+      return hipErrorInvalidValue;   // unreachable: unpaired blocks have no columns past ob+2
     }
-    SOAP_TRY(trailing_update(x, ob, cend2, n, s));              // far: the rest
-    SOAP_TRY(hipStreamWaitEvent(s, ev_panel, 0));               // block ob+1 factored
+    if (ev_next) ev_f = ev_next;
   }
   if (!mid_done) {
     if (mid) SOAP_TRY(hipEventRecord(mid, s));
@@ -1849,7 +1948,7 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     const int64_t nn = n * n;
     const unsigned gx = (unsigned)std::min<int64_t>((nn + 255) / 256, 2048);
     hipLaunchKernelGGL(qr_extract_r_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, At, Rf,
-                       x.dsign, x.ni, x.sA);
+                       x.dsign, x.ni, x.sA, (int)np);
     SOAP_TRY(hipGetLastError());
   }
   if (np > 0) {   // R is no longer needed: clear it above the block rows of every column
