@@ -131,6 +131,41 @@ def test_forced_give_up_of_one_qr_keeps_only_that_basis(side):
             f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}" for k, v in errs.items()))
 
 
+@pytest.mark.parametrize("m,n", [(256, 1024), (200, 1100)])
+def test_forced_give_up_of_r_at_wider_orders(m, n):
+    """n >= 2m with several reflector groups in the R-side QR: when that QR
+    gives up, the step rotates by the kept Q_R and equals the oracle's step
+    with the refresh of Q_R skipped."""
+    import paper_2607_20548_amd as soap
+    import oracle
+    grads = _grads(m, n, 3, 12)
+    W0 = (0.02 * np.random.default_rng(13).standard_normal((m, n))).astype(np.float32)
+    gs = soap.SoapState(m, n)
+    W = dev(W0)
+    st = oracle.init_state(W0.astype(np.float64))
+    chk = UpdateCheck(HP)
+    bit = soap.SOAP_STATUS_QR_R
+    for t, G in enumerate(grads, start=1):
+        forced = t == 3
+        QR_prev = host(gs.Q_R)
+        W_prev = host(W)
+        soap.soap_test_force_qr_give_up(bit if forced else 0)
+        gs.step(W, dev(G), t, **HP)
+        soap.soap_test_force_qr_give_up(0)
+        assert gs.status() == ((soap.SOAP_ERR_QR_GAVE_UP, bit) if forced else (soap.SOAP_OK, 0))
+        if forced:
+            assert np.array_equal(host(gs.Q_R), QR_prev)
+            st, N = _oracle_one_side_kept(st, G.astype(np.float64), t, keep_left=False)
+        else:
+            st, d = oracle.soap_step(st, G.astype(np.float64), t, diagnostics=True, **HP)
+            N = d["N"]
+        errs = compare_state(st, gs, f"{m}x{n} t={t}")
+        errs.update(chk(t, G, host(gs.update()), N, st.V, host(W), st.W, f"{m}x{n} t={t}",
+                        chain=(W_prev, host(gs.Q_L), host(gs.Q_R))))
+        log(f"give-up R {m}x{n} t={t} forced={forced} " + " ".join(
+            f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}" for k, v in errs.items()))
+
+
 def test_forced_give_up_batched_keeps_every_entry():
     """Three matrices through soap_step_batched: a forced give-up of the n x n
     QR keeps Q_R of every entry; the next step refreshes normally."""

@@ -47,6 +47,16 @@ def test_ragged_shapes(m, n):
                    (0.02 * rng.standard_normal((m, n))).astype(np.float32))
 
 
+@pytest.mark.parametrize("m,n", [(256, 1024), (200, 1100), (128, 2100), (300, 2300)])
+def test_wide_shapes_several_reflector_groups(m, n):
+    """n >= 2m at orders where the R-side QR forms several quads of blocks
+    (rank-512 Q formation, pair updates of the far columns, a ragged last
+    block), with the L side's QR started from inside the R side's loop."""
+    rng = np.random.default_rng([m, n, 23])
+    _run_open_loop(m, n, recipe_grads(m, n, 3, 23),
+                   (0.02 * rng.standard_normal((m, n))).astype(np.float32))
+
+
 @pytest.mark.parametrize("m,n", [(37, 70), (200, 257)])
 def test_ragged_shapes_gaussian_stress(m, n):
     """Full-rank Gaussian gradients: ill-conditioned factors, checked with the
