@@ -34,8 +34,13 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 constexpr int BM = 128;
 constexpr int BN = 128;
 constexpr int BK = 16;
-constexpr int LDSK = BK + 4;            // padded LDS row stride in floats
+constexpr int LDSK = BK + 4;            // padded LDS row stride in floats ([x][k] rows)
 constexpr int TILE_FLOATS = 128 * LDSK;  // one operand tile in LDS
+// [k][x] rows of an x-contiguous operand (vector path): 128 x-values padded to
+// 132 floats, so that the two lane halves of a fragment read (k and k + 8)
+// fall in disjoint banks.
+constexpr int LDSX = BN + 4;
+static_assert(BK * LDSX <= TILE_FLOATS, "an x-contiguous slab must fit one tile buffer");
 constexpr int NTHREADS = 256;
 constexpr int SHORT_K = 512;    // products with at most this much K per slice use the rank-k kernel
 constexpr int GROUP_M = 8;
@@ -66,9 +71,16 @@ struct KParams {
 //   KCONTIG = true : global element (x, k) at base[x*ld + k]
 //   KCONTIG = false: global element (x, k) at base[k*ld + x]
 // Work split: 512 (x, k-quad) items over 256 threads, two per thread; with
-// VEC == 4 an x-contiguous slab is instead read as 4 x 2 blocks (k-quad, x
-// pair), one per thread.
-template <bool KCONTIG, int VEC>
+// VEC == 4 an x-contiguous slab is instead read either as 4 x 2 blocks
+// (k-quad, x pair; 8-byte loads), one per thread, transposed in registers to
+// [x][k] rows, or (KX) as 512 (k, x-quad) items with 16-byte loads, each wave
+// covering two k rows per load instruction, kept in LDS as [k][x] rows
+// exactly as loaded.  The rank-k kernel takes the second form (5-7% faster
+// at K = 128-512: the register copies of the transposition had made its
+// loads wait right after their issue); for the long-K kernel it measured 1%
+// slower (its fragments then need eight 4-byte LDS reads instead of two
+// 16-byte ones).
+template <bool KCONTIG, int VEC, bool KX = false>
 struct SlabLoader {
   float r[8];
 
@@ -81,7 +93,8 @@ struct SlabLoader {
   // so that nothing consumes a loaded register early.  The scalar path
   // (VEC == 1) masks both at load time.  Requires X >= 1, K >= 1 (and the
   // VEC == 4 preconditions: K % 4 == 0 for k-contiguous, X even for
-  // x-contiguous operands).
+  // x-contiguous operands, and with KX X % 4 == 0 and a leading dimension
+  // and base aligned to 16 bytes).
   __device__ __forceinline__ void load(const float *__restrict__ base, int64_t ld, int x0,
                                        int k0, int X, int K, int tid) {
 #pragma unroll
@@ -101,6 +114,19 @@ struct SlabLoader {
             r[4 * s + e] = (x < X && k + e < K) ? v : 0.f;
           }
         }
+      } else if (VEC == 4 && KX) {
+        // x-contiguous with 16-byte loads: wave w reads k rows 8s + 2w (lanes
+        // 0-31) and 8s + 2w + 1 (lanes 32-63), four consecutive x per lane.
+        // The row address is formed on the scalar unit (k is uniform within
+        // each half wave; the second half adds one row, or none at the end
+        // of K), each lane adds its column offset.
+        const int lane = tid & 63;
+        const int kb = k0 + 8 * s + 2 * __builtin_amdgcn_readfirstlane(tid >> 6);
+        const float *rowp = base + (int64_t)min(kb, K - 1) * ld;
+        const int64_t dr = (kb < K - 1) ? ld : 0;
+        const unsigned xc = (unsigned)min(x0 + 4 * (lane & 31), X - 4);
+        const float4 v = *reinterpret_cast<const float4 *>(rowp + ((lane >> 5) ? dr : 0) + xc);
+        r[4 * s + 0] = v.x; r[4 * s + 1] = v.y; r[4 * s + 2] = v.z; r[4 * s + 3] = v.w;
       } else if (VEC == 4) {
         // x-contiguous with 8-byte loads: thread -> (k-quad, x pair); the
         // 4 x 2 block is transposed in registers (r[0..3] = column x,
@@ -132,9 +158,21 @@ struct SlabLoader {
     }
   }
 
-  // Writes the slab to LDS as [x][k] rows; kvalid = number of k-values of
-  // this slab inside K (BK except in the last, ragged slab).
+  // Writes the slab to LDS, as [x][k] rows ([k][x] rows for an x-contiguous
+  // operand on the vector path); kvalid = number of k-values of this slab
+  // inside K (BK except in the last, ragged slab).
   __device__ __forceinline__ void store(float *lds, int tid, int kvalid) {
+    if (!KCONTIG && VEC == 4 && KX) {
+      const int lane = tid & 63, w = tid >> 6;
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int k = 8 * s + 2 * w + (lane >> 5);
+        float4 v = make_float4(r[4 * s + 0], r[4 * s + 1], r[4 * s + 2], r[4 * s + 3]);
+        if (k >= kvalid) v = make_float4(0.f, 0.f, 0.f, 0.f);
+        *reinterpret_cast<float4 *>(lds + k * LDSX + 4 * (lane & 31)) = v;
+      }
+      return;
+    }
     if (VEC == 4 && kvalid < BK) {
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
@@ -169,11 +207,19 @@ struct SlabLoader {
   }
 };
 
+// The 8 k-values k = 8h + s (s = 0..7) of operand row x from LDS: two 16-byte
+// reads from [x][k] rows, or (KX) eight 4-byte reads from [k][x] rows.
+template <bool KX>
 __device__ __forceinline__ void read_frag(const float *lds, int x, int h, float (&f)[8]) {
-  const float4 lo = *reinterpret_cast<const float4 *>(lds + x * LDSK + 8 * h);
-  const float4 hi = *reinterpret_cast<const float4 *>(lds + x * LDSK + 8 * h + 4);
-  f[0] = lo.x; f[1] = lo.y; f[2] = lo.z; f[3] = lo.w;
-  f[4] = hi.x; f[5] = hi.y; f[6] = hi.z; f[7] = hi.w;
+  if constexpr (KX) {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) f[s] = lds[(8 * h + s) * LDSX + x];
+  } else {
+    const float4 lo = *reinterpret_cast<const float4 *>(lds + x * LDSK + 8 * h);
+    const float4 hi = *reinterpret_cast<const float4 *>(lds + x * LDSK + 8 * h + 4);
+    f[0] = lo.x; f[1] = lo.y; f[2] = lo.z; f[3] = lo.w;
+    f[4] = hi.x; f[5] = hi.y; f[6] = hi.z; f[7] = hi.w;
+  }
 }
 
 // Maps the linear workgroup id to a (tile-row, tile-column) pair.
@@ -225,8 +271,10 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
 
   // op(A) rows are x = i: k-contiguous when TA == 0.  op(B) columns are x = j:
   // k-contiguous when TB == 1.
-  SlabLoader<TA == 0, VEC> la;
-  SlabLoader<TB == 1, VEC> lb;
+  // the rank-k kernel keeps x-contiguous operands as [k][x] rows in LDS
+  constexpr bool KXL = SHORTK && VEC == 4;
+  SlabLoader<TA == 0, VEC, KXL> la;
+  SlabLoader<TB == 1, VEC, KXL> lb;
 
   v16f acc[2][2];
 #pragma unroll
@@ -242,12 +290,13 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   const int kend = min(p.K, kbeg + p.kslice);
   const int nk = (kend - kbeg + BK - 1) / BK;
   // One K slab from LDS buffer `cur` into the accumulators.
+  constexpr bool AKX = KXL && TA == 1, BKX = KXL && TB == 0;
   auto compute = [&](int cur) {
     float fa[2][8], fb[2][8];
-    read_frag(buf(cur, 1), wn * 64 + xl, h, fb[0]);
-    read_frag(buf(cur, 1), wn * 64 + 32 + xl, h, fb[1]);
-    read_frag(buf(cur, 0), wm * 64 + xl, h, fa[0]);
-    read_frag(buf(cur, 0), wm * 64 + 32 + xl, h, fa[1]);
+    read_frag<BKX>(buf(cur, 1), wn * 64 + xl, h, fb[0]);
+    read_frag<BKX>(buf(cur, 1), wn * 64 + 32 + xl, h, fb[1]);
+    read_frag<AKX>(buf(cur, 0), wm * 64 + xl, h, fa[0]);
+    read_frag<AKX>(buf(cur, 0), wm * 64 + 32 + xl, h, fa[1]);
 #pragma unroll
     for (int s = 0; s < 8; ++s)
 #pragma unroll
@@ -260,14 +309,14 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
   {
     // Global loads run two slabs ahead of the matrix cores (two register
     // sets), so a slab's loads have two slabs of MFMA work to land.
-    SlabLoader<TA == 0, VEC> lc;
-    SlabLoader<TB == 1, VEC> ld;
-    auto load_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TB == 1, VEC> &xb, int kt) {
+    SlabLoader<TA == 0, VEC, KXL> lc;
+    SlabLoader<TB == 1, VEC, KXL> ld;
+    auto load_set = [&](SlabLoader<TA == 0, VEC, KXL> &xa, SlabLoader<TB == 1, VEC, KXL> &xb, int kt) {
       const int k0 = kbeg + kt * BK;
       xa.load(A, p.lda, m0, k0, p.M, kend, tid);
       xb.load(B, p.ldb, n0, k0, p.N, kend, tid);
     };
-    auto store_set = [&](SlabLoader<TA == 0, VEC> &xa, SlabLoader<TB == 1, VEC> &xb, int stage,
+    auto store_set = [&](SlabLoader<TA == 0, VEC, KXL> &xa, SlabLoader<TB == 1, VEC, KXL> &xb, int stage,
                          int kt) {
       const int kvalid = min(BK, kend - (kbeg + kt * BK));
       xa.store(buf(stage, 0), tid, kvalid);
@@ -276,8 +325,8 @@ __global__ __launch_bounds__(NTHREADS, MINB) void gemm_f32_mfma(KParams p) {
     // slab kt is computed from LDS while the register set `held` carries
     // slab kt+1 (stored to the other buffer after the MFMAs) and `next`
     // receives slab kt+2.
-    auto body = [&](int kt, SlabLoader<TA == 0, VEC> &ha, SlabLoader<TB == 1, VEC> &hb,
-                    SlabLoader<TA == 0, VEC> &na, SlabLoader<TB == 1, VEC> &nb) {
+    auto body = [&](int kt, SlabLoader<TA == 0, VEC, KXL> &ha, SlabLoader<TB == 1, VEC, KXL> &hb,
+                    SlabLoader<TA == 0, VEC, KXL> &na, SlabLoader<TB == 1, VEC, KXL> &nb) {
       const int cur = kt & 1;
       load_set(na, nb, kt + 2);   // past the end: clamped loads, all zero
       compute(cur);
@@ -587,8 +636,10 @@ __global__ __launch_bounds__(256) void splitk_reduce(const float *__restrict__ p
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// vec_ok, vec_ok_kx: the vector path's preconditions for the long-K kernel
+// and for the rank-k kernel (vec_ok_for).
 template <int MODE>
-hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) {
+hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok, bool vec_ok_kx) {
   dim3 block(NTHREADS);
   const int S = (MODE == MODE_GENERAL && d.splitk > 1 && d.part) ? d.splitk : 1;
   // A cap counts every workgroup (split slices and batch included); the
@@ -613,7 +664,7 @@ hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) 
 #define SOAP_LAUNCH_P(TA, TB, VEC, MINB) \
   hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE_GENERAL, 0, MINB, true>), grid, block, 0, s, kp)
     const bool shortk = kp.kslice <= SHORT_K;
-    switch (code * 4 + (vec_ok ? 2 : 0) + (shortk ? 1 : 0)) {
+    switch (code * 4 + ((shortk ? vec_ok_kx : vec_ok) ? 2 : 0) + (shortk ? 1 : 0)) {
       case 0: SOAP_LAUNCH_P(0, 0, 1, 1); break;
       case 1: SOAP_LAUNCH_P(0, 0, 1, 3); break;
       case 2: SOAP_LAUNCH_P(0, 0, 4, 1); break;
@@ -639,7 +690,7 @@ hipError_t dispatch(const GemmDesc &d, KParams &kp, hipStream_t s, bool vec_ok) 
   } else if (MODE == MODE_GENERAL && kp.kslice <= SHORT_K) {
 #define SOAP_LAUNCH_RANK(TA, TB, VEC) \
   hipLaunchKernelGGL((gemm_f32_mfma<TA, TB, VEC, MODE_GENERAL, 0, 3>), grid, block, 0, s, kp)
-    if (vec_ok) {
+    if (vec_ok_kx) {
       switch (code) {
         case 0: SOAP_LAUNCH_RANK(0, 0, 4); break;
         case 1: SOAP_LAUNCH_RANK(0, 1, 4); break;
@@ -706,16 +757,23 @@ KParams make_params(const GemmDesc &d) {
 // leading dimension, batch stride multiples of 4 floats, 16-byte aligned
 // base); an x-contiguous operand uses 8-byte loads along x (even x extent,
 // leading dimension and batch stride, 8-byte aligned base).
+
 bool aligned8(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
-bool vec_ok_for(const GemmDesc &d) {
+// The vector path's preconditions; kx: the rank-k kernel, whose x-contiguous
+// operands are read 16 bytes at a time along x.
+bool vec_ok_for(const GemmDesc &d, bool kx) {
   bool ok = true;
   if (d.trans_a == 0)
     ok = ok && d.K % 4 == 0 && d.lda % 4 == 0 && d.sA % 4 == 0 && aligned16(d.A);
+  else if (kx)
+    ok = ok && d.M % 4 == 0 && d.lda % 4 == 0 && d.sA % 4 == 0 && aligned16(d.A);
   else
     ok = ok && d.M % 2 == 0 && d.lda % 2 == 0 && d.sA % 2 == 0 && aligned8(d.A);
   if (d.trans_b == 1)
     ok = ok && d.K % 4 == 0 && d.ldb % 4 == 0 && d.sB % 4 == 0 && aligned16(d.B);
+  else if (kx)
+    ok = ok && d.N % 4 == 0 && d.ldb % 4 == 0 && d.sB % 4 == 0 && aligned16(d.B);
   else
     ok = ok && d.N % 2 == 0 && d.ldb % 2 == 0 && d.sB % 2 == 0 && aligned8(d.B);
   return ok;
@@ -737,14 +795,14 @@ int choose_splitk(int64_t M, int64_t N, int64_t K, int64_t batch, int max_split)
 hipError_t launch_gemm(const GemmDesc &d, hipStream_t s) {
   if (d.M <= 0 || d.N <= 0 || d.batch <= 0) return hipSuccess;
   KParams kp = make_params(d);
-  return dispatch<MODE_GENERAL>(d, kp, s, vec_ok_for(d));
+  return dispatch<MODE_GENERAL>(d, kp, s, vec_ok_for(d, false), vec_ok_for(d, true));
 }
 
 hipError_t launch_syrk_ema(const GemmDesc &d, hipStream_t s) {
   if (d.M <= 0 || d.batch <= 0) return hipSuccess;
   KParams kp = make_params(d);
   kp.ntiles = kp.tiles_m * (kp.tiles_m + 1) / 2;
-  return dispatch<MODE_SYRK>(d, kp, s, vec_ok_for(d));
+  return dispatch<MODE_SYRK>(d, kp, s, vec_ok_for(d, false), vec_ok_for(d, true));
 }
 
 hipError_t launch_gemm_adam(const GemmDesc &d, const AdamEpi &e, hipStream_t s) {
@@ -754,7 +812,7 @@ hipError_t launch_gemm_adam(const GemmDesc &d, const AdamEpi &e, hipStream_t s) 
   kp.V = e.V;
   kp.Nout = e.Nout;
   kp.b2 = e.b2; kp.c1 = e.c1; kp.c2 = e.c2; kp.eps = e.eps;
-  return dispatch<MODE_ADAM>(d, kp, s, vec_ok_for(d));
+  return dispatch<MODE_ADAM>(d, kp, s, vec_ok_for(d, false), vec_ok_for(d, true));
 }
 
 }  // namespace soap
