@@ -497,26 +497,22 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
 // same number of active columns as the factorization advances) and lane part
 // holds the local rows 32 i + 4 part + e (i < BK_R/4, e < 4): 32 values per
 // lane and four waves per SIMD to hide the latency of each round.  The columns
-// are taken in rounds of two (see the loop for the one-column rounds).  Per
-// round:
-//   * the two pivot columns are broadcast through LDS and every thread forms
-//     the partial dots of its column with both, below their diagonal rows;
-//   * the partials are summed grid-wide in one hop through global memory.
-//     Every value travels as a 64-bit item (value bits | generation << 32)
-//     written and read with agent-scope atomics, so a reader recognises a
-//     fresh value by its generation (round index + 1 past the block's first
-//     column) and needs no barrier or flag: each workgroup posts its partials
-//     of all columns (contiguous rows of items) and workgroup 0 the
-//     diagonal-row values; every workgroup then reads the P partials of each
-//     column it needs and sums them in one fixed order, so all of them apply
-//     bit-identical reflectors.  Items are double-buffered by round parity:
-//     no workgroup can get two rounds ahead of a reader;
-//   * every thread applies both reflectors to its own column.
-// Workgroup 0 holds the block's diagonal rows: its pivot broadcast is zero at
-// and above the diagonal row (so its dot products need no masks), it posts
-// the diagonal-row values, and it keeps S = strict upper part of Y^T Y,
-//   S[l][j] = y_l^T v_j = A_l + D_l / v0_j  (from the same dot products),
-// from which it forms T after the column loop,
+// are taken in rounds of up to BK_KMAX.  Per round (pivot columns j..j+K-1):
+//   * the pivot columns are broadcast through LDS, pivot j+i with its rows up
+//     to j+i cleared (its tail y_i), and every thread forms the partial dots
+//     of its column with every tail;
+//   * the partials are summed grid-wide in one hop through global memory:
+//     each workgroup posts its partials, workgroup 0 also the column's values
+//     in the diagonal rows j..j+K-1, and every workgroup reads back the P
+//     partials of each dot of the columns it needs and sums them in one
+//     fixed order, so that all of them hold bit-identical totals;
+//   * from the totals of the pivot columns, one wave forms the round's
+//     reflectors (Gram recurrence below), and every thread applies them to its
+//     own column as one combination of the tails.
+// Workgroup 0 holds the block's diagonal rows: its broadcasts are zero at and
+// above each pivot's diagonal row (so its dot products need no masks), and it
+// keeps S = strict upper part of Y^T Y (from the same dot products), from
+// which it forms T after the column loop,
 //   T[k][k] = beta_k,  T[k][j] = -beta_j sum_{l=k}^{j-1} T[k][l] S[l][j]  (j > k),
 // by blocks of 8 columns (the diagonal blocks by this recurrence, the others
 // by T_IJ = -(sum_{K=I}^{J-1} T_IK S_KJ) T_JJ).
@@ -541,28 +537,32 @@ constexpr int BK_R_SMALL = 16;
 constexpr int BK_ROWS_SMALL = BK_PARTS * BK_R_SMALL;
 constexpr int BK_SMALL_MAX_P = 32;
 constexpr int BK_LI = 4 * BK_PARTS;             // local-row stride of a thread's register groups
-constexpr int BK_MAX_P = 64;                    // workgroups per matrix (n <= 16384);
-                                                // a reader lane sums at most 16 partials
+constexpr int BK_MAX_P = 64;                    // workgroups per matrix (n <= 16384)
 constexpr int BK_MAX_WG = 96;                   // workgroups per launch
 constexpr unsigned BK_SPIN_LIMIT = 1u << 22;
 constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (spreads banks)
-// A round takes two columns when H_j leaves column j+1 at least this fraction
-// of its squared norm (rows j+1.. after H_j against rows j.. before it).
-constexpr float BK_PAIR_TAU = 0.0625f;
+constexpr int BK_KMAX = 4;                      // columns per round at most
+// A round stops before pivot j+i (i > 0) when the reflectors j..j+i-1 leave
+// less than this fraction of its squared norm (rows j+i.. after them against
+// rows j.. before them): the sums that give its reflector would lose digits
+// to cancellation.
+constexpr float BK_TAU = 0.0625f;
 // Exchange area per matrix, in 32-bit words: a header (the abort flag, the
-// failed flag), then two slot areas that the outer blocks use in turn.  A
-// round of a block with P workgroups has a slot of its own,
-//   [2][P][NB] partials of the two sums, then [2][NB] values of workgroup 0
-//   in the diagonal rows j, j+1,
-// column k at position (k mod 8) * 16 + k / 8 (the columns of one wave are
-// contiguous).  Every word is written once per call, over the empty pattern
-// BK_EMPTY (a NaN that no post carries: posted NaNs are canonical), so a
-// reader knows a value has arrived from its bits alone and one register
-// holds one pending item.  A block kernel refills, after its rounds, the
-// area that the next block uses (the kernel before it in the same stream
-// used that area last).
+// failed flag, and per slot area the words written there since it was last
+// emptied), then two slot areas that the outer blocks use in turn.  A round
+// of a block with P workgroups has a slot of its own, bk_col_words(P) items
+// of NB columns each: [BK_KMAX][P] partials of the dots (pivot i, workgroup g
+// is item i * P + g), then the BK_KMAX values of workgroup 0 in the diagonal
+// rows; item e of column k at word e * NB + (k mod 8) * 16 + k / 8 (the
+// columns of one wave are adjacent, so that one load by a wave touches few
+// cache lines).  Every word is written at most once between two
+// emptyings, over the empty pattern BK_EMPTY (a NaN that no post carries:
+// posted NaNs are canonical), so a reader knows a value has arrived from its
+// bits alone.  A block kernel empties, after its rounds, what the previous
+// block wrote into the area that the next block uses.
 constexpr int64_t BK_XABORT = 0;
 constexpr int64_t BK_XFAILED = 1;
+constexpr int64_t BK_XUSED = 2;                 // words 2, 3: written words of area 0, 1
 constexpr int64_t BK_XHDR = 64;
 constexpr unsigned BK_EMPTY = 0xFFFFFFFFu;
 // Workgroups of the widest block launch for order n (the big-R kernel at
@@ -573,11 +573,10 @@ constexpr int64_t bk_max_p(int64_t n) {
   const int64_t s2 = sm < BK_SMALL_MAX_P ? sm : BK_SMALL_MAX_P;
   return big > s2 ? big : s2;
 }
+__host__ __device__ constexpr int64_t bk_col_words(int64_t P) { return BK_KMAX * P + BK_KMAX; }
 // words of one slot area: at most NB rounds per block
-constexpr int64_t bk_area_words(int64_t n) { return (int64_t)NB * (2 * bk_max_p(n) + 2) * NB; }
+constexpr int64_t bk_area_words(int64_t n) { return (int64_t)NB * NB * bk_col_words(bk_max_p(n)); }
 constexpr int64_t bk_xstride(int64_t n) { return BK_XHDR + 2 * bk_area_words(n); }
-// words of block ob's slots (rounds <= its columns)
-constexpr int64_t bk_block_words(int64_t nbcols, int P) { return (int64_t)nbcols * (2 * P + 2) * NB; }
 
 struct BlockParams {
   float *At;
@@ -590,7 +589,6 @@ struct BlockParams {
   unsigned *xch;             // exchange area, xstride words per matrix
   int64_t xstride, area_words;
   int area;                  // slot area of this block (0 or 1)
-  int64_t next_words;        // words of the next block's slots (refilled here), or 0
   int P;                     // workgroups per matrix
   unsigned *status;          // caller's status word (or nullptr) ...
   unsigned status_bit;       // ... and the bit a give-up or-s into it
@@ -624,27 +622,39 @@ __device__ __forceinline__ bool bk_give_up(unsigned &spins, unsigned *abort_flag
   return false;
 }
 
-// Waits for the items p[stride i], i < cnt <= 16, and (if x is not null)
-// the item x, re-reading only those still empty; returns the sum of the
-// first in index order and the value of x.  All pending items are fetched
-// at once (their loads issued before any is examined), so a poll costs about
-// one memory latency however many items there are.  false: aborted.
-__device__ __forceinline__ bool bk_gather(const unsigned *p, int stride, int cnt,
-                                          const unsigned *x, unsigned *abort_flag, float &sum,
-                                          float &xv) {
-  unsigned v[16];
-  unsigned pending = (1u << cnt) - 1u;
-  bool hx = (x == nullptr);
+// Waits for the cnt <= H items at byte offsets off + 4 NB i (i < cnt) of the
+// buffer r and, if xoff >= 0, the item at byte offset xoff, re-reading only
+// those still empty; returns the sum of the first in index order and the
+// value of x.  The loads take the cache policy of an agent-scope load (sc1,
+// as the atomic loads above) through a buffer resource, so that one offset
+// register and the instruction's offset field address every item.  All
+// pending items are fetched at once (their loads issued before any is
+// examined), so a poll costs about one memory latency however many items
+// there are.  false: aborted.
+constexpr int BK_LOAD_AGENT = 16;   // cache policy operand: sc1
+constexpr int BK_RSRC_WORD3 = 0x00020000;   // buffer resource: raw 32-bit data
+template <int H>
+__device__ __forceinline__ bool bk_gather(__amdgpu_buffer_rsrc_t r, unsigned off, int cnt,
+                                          int xoff, unsigned *abort_flag, float &sum, float &xv) {
+  static_assert(H <= 32, "one pending bit per item");
+  unsigned v[H];
+  unsigned pending = cnt >= 32 ? 0xFFFFFFFFu : ((1u << cnt) - 1u);
+  bool hx = xoff < 0;
   unsigned spins = 0;
   for (;;) {
+    // a new offset value each poll as far as the compiler knows: the loads
+    // are issued again, not kept from the previous poll
+    asm volatile("" : "+v"(off));
     unsigned vx = 0;
-    if (!hx) vx = bk_get(x);
+    if (!hx) vx = __builtin_amdgcn_raw_buffer_load_b32(r, xoff + (int)(off & 0u), 0, BK_LOAD_AGENT);
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (pending & (1u << i)) v[i] = bk_get(p + (int64_t)stride * i);
+    for (int i = 0; i < H; ++i)
+      if (pending & (1u << i))
+        v[i] = __builtin_amdgcn_raw_buffer_load_b32(r, (int)(off + (unsigned)(i * NB * 4)), 0,
+                                                    BK_LOAD_AGENT);
     unsigned still = pending;
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
+    for (int i = 0; i < H; ++i)
       if ((pending & (1u << i)) && v[i] != BK_EMPTY) still &= ~(1u << i);
     if (!hx && vx != BK_EMPTY) {
       xv = __uint_as_float(vx);
@@ -656,54 +666,41 @@ __device__ __forceinline__ bool bk_gather(const unsigned *p, int stride, int cnt
   }
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < 16; ++i)
+  for (int i = 0; i < H; ++i)
     if (i < cnt) s += __uint_as_float(v[i]);
   sum = s;
   return true;
 }
 
 // Lane exchanges inside the 8 lanes of a column (lanes 8q..8q+7, one half of
-// a DPP row) by DPP moves, which take no LDS round trip: bk_sum8 leaves the
-// sum of the 8 values in every lane, bk_pair4 the sums of lanes 0-3 (first)
-// and 4-7 (second), bk_bcast4 the values of lanes 3 and 7.  Additions are
-// commutative, so every lane holds bit-identical results.
+// a DPP row) by DPP moves, which take no LDS round trip: bk_sum2, bk_sum4 and
+// bk_sum8 leave in every lane the sum over its aligned group of 2, 4 and 8
+// lanes.  Additions are commutative, so every lane of a group holds a
+// bit-identical result.
 template <int CTRL>
 __device__ __forceinline__ float bk_mov(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
 }
 constexpr int DPP_XOR1 = 0xB1;         // quad_perm [1, 0, 3, 2]
 constexpr int DPP_XOR2 = 0x4E;         // quad_perm [2, 3, 0, 1]
-constexpr int DPP_LANE3 = 0xFF;        // quad_perm [3, 3, 3, 3]
 constexpr int DPP_HALF_MIRROR = 0x141; // lane i <- lane 7 - i within 8 lanes
+__device__ __forceinline__ float bk_sum2(float v) { return v + bk_mov<DPP_XOR1>(v); }
 __device__ __forceinline__ float bk_sum4(float v) {
-  v += bk_mov<DPP_XOR1>(v);
+  v = bk_sum2(v);
   return v + bk_mov<DPP_XOR2>(v);
 }
 __device__ __forceinline__ float bk_sum8(float v) {
   v = bk_sum4(v);
   return v + bk_mov<DPP_HALF_MIRROR>(v);
 }
-// first = sum of lanes 0-3, second = sum of lanes 4-7 (in every lane of the 8)
-__device__ __forceinline__ void bk_pair4(float v, bool low, float &first, float &second) {
-  const float q = bk_sum4(v);
-  const float o = bk_mov<DPP_HALF_MIRROR>(q);
-  first = low ? q : o;
-  second = low ? o : q;
-}
-__device__ __forceinline__ void bk_bcast4(float v, bool low, float &first, float &second) {
-  const float q = bk_mov<DPP_LANE3>(v);
-  const float o = bk_mov<DPP_HALF_MIRROR>(q);
-  first = low ? q : o;
-  second = low ? o : q;
-}
 
-// a[idx / 4][idx % 4] += dv for a wave-uniform idx < 4 NQ (a compare per
-// candidate register instead of a select chain over the row indices).
+// a[idx / 4][idx % 4] = v for a wave-uniform or lane-varying idx < 4 NQ (a
+// compare per candidate register instead of a select chain over the rows).
 template <int NQ, int NI>
-__device__ __forceinline__ void bk_reg_add(float (&a)[NI][4], int idx, float dv) {
+__device__ __forceinline__ void bk_reg_set(float (&a)[NI][4], int idx, float v) {
 #pragma unroll
   for (int q = 0; q < 4 * NQ; ++q)
-    if (q == idx) a[q >> 2][q & 3] += dv;
+    if (q == idx) a[q >> 2][q & 3] = v;
 }
 
 // Householder reflector of a column with diagonal value x0 and tail sum of
@@ -725,15 +722,27 @@ __device__ __forceinline__ void bk_reflector(float x0, float st, float &bet, flo
   }
 }
 
-template <int R>
+// Columns per round of the two block kernels (rows per thread BK_R and
+// BK_R_SMALL).
+constexpr int BK_K_BIG = 4;
+constexpr int BK_K_SMALL = 4;
+
+template <int R, int KM>
 __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
+  static_assert(KM >= 1 && KM <= BK_KMAX, "columns per round");
   constexpr int NI = R / 4;
   constexpr int RS = BK_PARTS * R;
+  // Items per lane of a gather: the P partials of one dot over 8 / K' lanes
+  // (K' = columns of the round rounded up to a power of two), at most H
+  // (registers).  Launches of the big kernel with more than 56 workgroups
+  // (orders past 14336) take two columns per round.
+  constexpr int KP2 = KM > 2 ? 4 : KM;
+  constexpr int H = (R == BK_R && KP2 == 4) ? 28 : ((R == BK_R ? BK_MAX_P : BK_SMALL_MAX_P) * KP2 + 7) / 8;
   // register groups i that can hold one of the diagonal rows 0..NB-1 of
   // workgroup 0 (local row BK_LI i + 4 part + e < NB); only these need masks
   constexpr int NIM = (NB / BK_LI < NI) ? NB / BK_LI : NI;
-  __shared__ float px[2][2][RS];         // pivot columns j, j+1, by round parity
-  __shared__ float pv[2][8];             // their totals, by round parity
+  __shared__ float px[2][KM][RS];   // pivot tails, by round parity
+  __shared__ float pv[2][KM][8];    // pivot totals: dots, diagonal-row values
   __shared__ float bs[NB];               // beta_j (workgroup 0)
   __shared__ float Ss[NB * BK_TSTR];     // S (workgroup 0), row-major
   __shared__ float Ts[NB * BK_TSTR];     // T (workgroup 0), row-major
@@ -751,7 +760,9 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   unsigned *X = p.xch + bz * p.xstride;
   unsigned *abort_flag = X + BK_XABORT;
   unsigned *slots = X + BK_XHDR + p.area * p.area_words;   // this block's rounds
-  const int64_t slot_words = (int64_t)(2 * P + 2) * NB;
+  const int64_t cw = (int64_t)KM * P + KM;          // items per column and round
+  const int64_t pk = (int64_t)(wave * (64 / BK_PARTS) + lane / BK_PARTS);   // position of column k
+  const int lbase = lane & ~(BK_PARTS - 1);
 
   float a[NI][4];
   {
@@ -768,8 +779,8 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   const bool want_r = p.Rf != nullptr;   // the triangular factor is an output
   // Workgroup 0 keeps a copy of its diagonal rows (local rows < NB) in Ts,
   // unused until T is formed after the loop: Ts[k][row], rewritten after
-  // every round, so the values of the diagonal rows j, j+1 of each column are
-  // two LDS reads (not a selection among the registers).
+  // every round, so the values of the diagonal rows of each column are LDS
+  // reads (not a selection among the registers).
   auto save_diag_rows = [&]() {
     if (w0 && col) {
 #pragma unroll
@@ -780,30 +791,36 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   };
   save_diag_rows();
 
-  // Rounds of one or two columns.  A round broadcasts pivot column j (its
-  // tail below the diagonal row j) and, if there is one, column j+1 (its tail
-  // below row j+1); every thread forms the dots of its column with both, and
-  // one grid-wide exchange gives every column
-  //   D = sum_{r>j} a_r x_r,  E = sum_{r>j+1} a_r y_r,  A = a_j,  B = a_{j+1}.
-  // Reflector j comes from (D_j, A_j) as in a one-column step.  The effect of
-  // H_j on column j+1 and on the dots with it follows from these sums (the
-  // 2 x 2 Gram correction below), so reflector j+1 and the update of every
-  // later column by H_j H_{j+1} need no second exchange.  When H_j removes
-  // most of column j+1 (its norm from row j+1 down falls below a quarter of
-  // its norm from row j down) the corrected sums would lose digits to
-  // cancellation: the round then applies H_j alone and the next round starts
-  // at column j+1.  Every workgroup takes this decision from the same totals
-  // with the same arithmetic, so all of them follow the same rounds.
+  // Round at column j with K pivots p_0..p_{K-1} (columns j..j+K-1); rows are
+  // counted from j (row s is row j+s).  A column a enters the round with its
+  // diagonal-row values A[s] (s < K) and its dots with the tails,
+  //   D[i] = sum_{s > i} a[s] p_i[s].
+  // After reflectors 0..i-1 a column is a - sum_{l<i} g_l y_l on every row
+  // past i-1 (each tail y_l covers them), so the reflectors act on the
+  // coefficients g alone: with Phi_i(u, w) = sum_{s > i} u[s] w[s],
+  //   Phi_i(p_l, a) = D[l] - sum_{s=l+1}^{i} p_l[s] A[s]          (l < i),
+  //   a_i = A[i] - sum_{l<i} g_l p_l[i]        (its value in row i),
+  //   v_i^T a = a_i + (1/v0_i) (D[i] - sum_l gamma_i[l] Phi_i(p_l, a)
+  //                                   - sum_l g_l c_i[l]),
+  // where gamma_i are the coefficients of pivot i when its reflector is
+  // formed and c_i[l] = Phi_i(current pivot i, p_l).  Reflector i is applied
+  // as f = beta_i v_i^T a, g_i = f / v0_i, g_l -= g_i gamma_i[l].  The pivot
+  // columns' own totals give the reflectors (the same recurrence run on them,
+  // with the pivot's squared tail Phi_i(pivot i, pivot i)); a round stops
+  // before a pivot whose norm the earlier reflectors have mostly removed
+  // (BK_TAU).  Every workgroup forms the same rounds from the same totals
+  // with the same arithmetic.  Rows 0..taken-1 are R rows afterwards; the
+  // combination leaves them inexact, and nothing but the triangular-factor
+  // output reads them (later dots, broadcasts and diagonal-row values start
+  // below them), which sets them from the recurrence.
   int j = 0;
-  for (int round = 0; j < nb; ++round) {
+  int round = 0;
+  for (; j < nb; ++round) {
     const int par = round & 1;
-    const bool two = j + 1 < nb;
-    // lane part and register index (i * 4 + e) of the diagonal rows j, j+1
-    // in workgroup 0 (local row BK_LI i + 4 part + e)
-    const int pj0 = (j >> 2) & (BK_PARTS - 1), ij0 = (j / BK_LI) * 4 + (j & 3);
-    const int pj1 = ((j + 1) >> 2) & (BK_PARTS - 1), ij1 = ((j + 1) / BK_LI) * 4 + ((j + 1) & 3);
-    if (k == j || (two && k == j + 1)) {
-      float *dst = px[par][k - j];
+    const int kr = min((KM > 2 && (P * KP2 + 7) / 8 > H) ? 2 : KM, nb - j);
+    const int rho = k - j;                          // this column's index in the round
+    if (rho >= 0 && rho < kr) {
+      float *dst = px[par][rho];
 #pragma unroll
       for (int i = 0; i < NI; ++i)
 #pragma unroll
@@ -813,200 +830,250 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         }
     }
     __syncthreads();
-    const float *x = px[par][0];
-    const float *y = px[par][1];
-    float d = 0.f, ev = 0.f, av0 = 0.f, av1 = 0.f;
+    float D[KM], A[KM];
+#pragma unroll
+    for (int q = 0; q < KM; ++q) D[q] = A[q] = 0.f;
     if (col) {
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < NI; ++i)
+      for (int q = 0; q < KM; ++q) {
+        if (q < kr) {
+          const float *y = px[par][q];
+          float acc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] += a[i][e] * x[BK_LI * i + 4 * part + e];
-      d = (acc[0] + acc[1]) + (acc[2] + acc[3]);
-      if (two) {
-        float acc2[4] = {0.f, 0.f, 0.f, 0.f};
+          for (int i = 0; i < NI; ++i)
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) acc2[e] += a[i][e] * y[BK_LI * i + 4 * part + e];
-        ev = (acc2[0] + acc2[1]) + (acc2[2] + acc2[3]);
+            for (int e = 0; e < 4; ++e) acc[e] += a[i][e] * y[BK_LI * i + 4 * part + e];
+          D[q] = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+        }
       }
-      if (w0) {   // values of the diagonal rows j and j+1 (every lane of the column)
-        av0 = Ts[k * BK_TSTR + j];
-        if (two) av1 = Ts[k * BK_TSTR + j + 1];
+      if (w0) {
+#pragma unroll
+        for (int s = 0; s < KM; ++s)
+          if (s < kr) A[s] = Ts[k * BK_TSTR + j + s];
       }
     }
-    d = bk_sum8(d);
-    ev = bk_sum8(ev);
-    float D = d, E = ev, A = av0, B = av1;
+#pragma unroll
+    for (int q = 0; q < KM; ++q)
+      if (q < kr) D[q] = bk_sum8(D[q]);
     if (P > 1) {
-      // One hop: every workgroup posts its partials, then every workgroup
-      // reads the P partials of each column it needs and sums them in the
-      // same order, so all of them hold bit-identical totals.  Lanes 0..3 of
-      // a column sum the D partials of the workgroups u = part mod 4, lanes
-      // 4..7 those of E; lanes 3 and 7 also fetch A and B from workgroup 0.
-      const int64_t pk = (int64_t)(wave * (64 / BK_PARTS) + lane / BK_PARTS);   // position of column k
-      const int q = part >> 2, u0 = part & 3;
-      unsigned *slot = slots + (int64_t)round * slot_words;
-      if (col && (part == 0 || part == 4)) bk_put(slot + ((int64_t)q * P + g) * NB + pk, q ? ev : d);
-      if (w0 && col && (part == 1 || part == 5))
-        bk_put(slot + ((int64_t)2 * P + q) * NB + pk, q ? av1 : av0);
+      // Lane part < K posts its column's partial of dot `part`; lanes 4..7 of
+      // workgroup 0 the diagonal-row values.  Then each dot's P partials are
+      // read by 8/K' lanes (K' = K rounded up to a power of two), ceil(P K'/8)
+      // contiguous items each, summed in index order and then over the lanes
+      // of the dot in a fixed tree; lanes part < K also fetch the diagonal-row
+      // value `part` from workgroup 0.
+      unsigned *sl = slots + (int64_t)round * NB * cw;        // this round's slot
+      unsigned *cb = sl + pk;                                  // item e at cb[e * NB]
+      if (col) {
+        float mine = D[0];
+#pragma unroll
+        for (int q = 1; q < KM; ++q)
+          if (part == q) mine = D[q];
+        if (part < kr) bk_put(cb + ((int64_t)part * P + g) * NB, mine);
+        if (w0 && part >= 4 && part - 4 < kr) {
+          float tv = A[0];
+#pragma unroll
+          for (int s = 1; s < KM; ++s)
+            if (part - 4 == s) tv = A[s];
+          bk_put(cb + ((int64_t)KM * P + (part - 4)) * NB, tv);
+        }
+      }
       if (col && (w0 || k >= j)) {
-        float ssum = 0.f, xv = 0.f;
+        const int lg = (kr == 1) ? 3 : ((kr == 2) ? 2 : 1);    // log2 lanes per dot
+        const int q = part >> lg, h = part & ((1 << lg) - 1);
+        const int hn = (P + (1 << lg) - 1) >> lg;
+        const int g0 = h * hn;
+        const int cnt = (q < kr) ? max(0, min(P - g0, hn)) : 0;
+        const int xoff = (!w0 && part < kr) ? (int)(((KM * P + part) * NB + pk) * 4) : -1;
+        const __amdgpu_buffer_rsrc_t rs =
+            __builtin_amdgcn_make_buffer_rsrc(sl, (short)0, (int)(NB * cw * 4), BK_RSRC_WORD3);
+        float ssum = 0.f, xval = 0.f;
         if (alive)
-          alive = bk_gather(slot + ((int64_t)q * P + u0) * NB + pk, 4 * NB, (P - u0 + 3) / 4,
-                            (!w0 && u0 == 3) ? slot + ((int64_t)2 * P + q) * NB + pk : nullptr,
-                            abort_flag, ssum, xv);
-        bk_pair4(ssum, part < 4, D, E);
-        float aa, bb;
-        bk_bcast4(xv, part < 4, aa, bb);
+          alive = bk_gather<H>(rs, (unsigned)(((q * P + g0) * NB + pk) * 4), cnt, xoff, abort_flag,
+                               ssum, xval);
+        float s = ssum;
+        if (lg == 1) s = bk_sum2(s);
+        else if (lg == 2) s = bk_sum4(s);
+        else s = bk_sum8(s);
+#pragma unroll
+        for (int qq = 0; qq < KM; ++qq)
+          if (qq < kr) D[qq] = __shfl(s, lbase + (qq << lg));
         if (!w0) {
-          A = aa;
-          B = bb;
+#pragma unroll
+          for (int ss = 0; ss < KM; ++ss)
+            if (ss < kr) A[ss] = __shfl(xval, lbase + ss);
         }
       }
     }
-    if (part == 0) {
-      if (k == j) {
-        pv[par][0] = D;
-        pv[par][1] = A;
-        pv[par][2] = B;
-      } else if (two && k == j + 1) {
-        pv[par][3] = D;
-        pv[par][4] = A;
-        pv[par][5] = B;
-        pv[par][6] = E;
+    if (rho >= 0 && rho < kr && part == 0) {
+#pragma unroll
+      for (int q = 0; q < KM; ++q) {
+        pv[par][rho][q] = D[q];
+        pv[par][rho][KM + q] = A[q];
       }
     }
     __syncthreads();
-    const float st = pv[par][0], x0 = pv[par][1], Bj = pv[par][2];
-    float bet, inv_v0, rjj;
-    bk_reflector(x0, st, bet, inv_v0, rjj);
-    // Column j+1 after H_j: f1 = beta_j v_j^T a_{j+1}, its diagonal value
-    // x0b and tail sum of squares stb from the sums; sxy and sxx are the dots
-    // of x with y and with itself below row j+1.
-    bool pair = false;
-    float fs1 = 0.f, sxy = 0.f, sxx = 0.f, f1 = 0.f;
-    float bet2 = 0.f, inv_v02 = 0.f, rjj2 = 0.f;
-    if (two) {
-      const float D1 = pv[par][3], A1 = pv[par][4], B1 = pv[par][5], E1 = pv[par][6];
-      f1 = bet * (A1 + D1 * inv_v0);
-      fs1 = f1 * inv_v0;
-      sxy = D1 - B1 * Bj;
-      sxx = st - Bj * Bj;
-      const float x0b = B1 - fs1 * Bj;
-      const float stb = E1 - 2.f * fs1 * sxy + fs1 * fs1 * sxx;
-      const float ref = A1 * A1 + B1 * B1 + E1;
-      pair = stb >= 0.f && x0b * x0b + stb >= BK_PAIR_TAU * ref;
-      if (pair) bk_reflector(x0b, stb, bet2, inv_v02, rjj2);
-    }
-    const int jl = pair ? j + 1 : j;           // last column of this round
-    if (col && k > jl) {
-      const float f = bet * (A + D * inv_v0);
-      const float fs = f * inv_v0;
-      if (pair) {
-        // H_j H_{j+1} at once: a -= fs x + fsp (y - fs1 x) below row j+1,
-        // with fsp from the dot of the updated column and updated pivot.
-        const float ak1 = B - fs * Bj;
-        const float dp = E - fs1 * (D - B * Bj) - fs * sxy + fs * fs1 * sxx;
-        const float fp = bet2 * (ak1 + dp * inv_v02);
-        const float fsp = fp * inv_v02;
-        const float c1 = fs - fsp * fs1;
+    // The round's reflectors from the pivots' totals, formed alike in every
+    // thread (registers only): pt[m][s] = p_m[s], ph[m][l] = Phi_i(p_l, p_m),
+    // gm[m][l] = coefficients of pivot m (l < m); per step i: beta rb[i],
+    // 1/v0 rv[i], R diagonal rr[i], gamma_i = gm[i][l] and c_i = rc[i][l].
+    float pt[KM][KM], rb[KM], rv[KM], rr[KM], gm[KM][KM], rc[KM][KM];
+    int taken = kr;
+    {
+      float ph[KM][KM];
 #pragma unroll
-        for (int i = 0; i < NI; ++i)
+      for (int m = 0; m < KM; ++m) {
+        rb[m] = rv[m] = rr[m] = 0.f;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int lr = BK_LI * i + 4 * part + e;
-            a[i][e] = fmaf(-c1, x[lr], fmaf(-fsp, y[lr], a[i][e]));
+        for (int l = 0; l < KM; ++l) {
+          const bool in = m < kr && l < kr;
+          ph[m][l] = in ? pv[par][m][l] : 0.f;
+          pt[m][l] = in ? pv[par][m][KM + l] : 0.f;
+          gm[m][l] = rc[m][l] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < KM; ++i) {
+        if (i < taken) {
+          // row i leaves the tails Phi(p_l, .), l < i
+#pragma unroll
+          for (int m = 0; m < KM; ++m)
+#pragma unroll
+            for (int l = 0; l < i; ++l) ph[m][l] -= pt[l][i] * pt[m][i];
+          float x0 = pt[i][i];
+#pragma unroll
+          for (int l = 0; l < i; ++l) {
+            x0 -= gm[i][l] * pt[l][i];
+            float v = ph[l][i];
+#pragma unroll
+            for (int l2 = 0; l2 < i; ++l2) v -= gm[i][l2] * ph[l][l2];
+            rc[i][l] = v;
           }
-        // workgroup 0: the broadcasts are zero in rows j (x, y) and j+1 (y),
-        // where v_j = 1 and v_{j+1} = 1 instead.  These rows are R rows from
-        // now on; nothing but the triangular-factor output reads them (the
-        // later dots, broadcasts and diagonal-row values all start below
-        // row j+1), so without that output they are left as they are.
+          float st = ph[i][i];
+#pragma unroll
+          for (int l = 0; l < i; ++l) st -= gm[i][l] * (ph[i][l] + rc[i][l]);
+          float ref = ph[i][i];
+#pragma unroll
+          for (int s = 0; s <= i; ++s) ref += pt[i][s] * pt[i][s];
+          const bool ok = (i == 0) || (st >= 0.f && x0 * x0 + st >= BK_TAU * ref);
+          if (!ok) {
+            taken = i;
+          } else {
+            bk_reflector(x0, st, rb[i], rv[i], rr[i]);
+            const float bet = rb[i], iv0 = rv[i];
+#pragma unroll
+            for (int m = i + 1; m < KM; ++m) {
+              float cur = pt[m][i];
+              float phv = ph[m][i];
+#pragma unroll
+              for (int l = 0; l < i; ++l) {
+                cur -= gm[m][l] * pt[l][i];
+                phv -= gm[i][l] * ph[m][l] + gm[m][l] * rc[i][l];
+              }
+              const float qf = bet * (cur + iv0 * phv) * iv0;
+#pragma unroll
+              for (int l = 0; l < i; ++l) gm[m][l] -= qf * gm[i][l];
+              gm[m][i] = qf;
+            }
+          }
+        }
+      }
+    }
+    // this column's 1/v0 and R diagonal if it is a pivot the round takes
+    float iv0_own = 1.f, rj_own = 0.f;
+#pragma unroll
+    for (int m = 0; m < KM; ++m)
+      if (rho == m && m < taken) {
+        iv0_own = rv[m];
+        rj_own = rr[m];
+      }
+    if (col && (rho >= 0 || w0)) {
+      // This column's coefficients, its R entries in rows j.. (Rr) and, for
+      // the reflectors past it, S = y_k^T v (stored and consumed columns).
+      float gc[KM], Rr[KM];
+#pragma unroll
+      for (int q = 0; q < KM; ++q) gc[q] = Rr[q] = 0.f;
+      float phi[KM];
+#pragma unroll
+      for (int q = 0; q < KM; ++q) phi[q] = D[q];
+#pragma unroll
+      for (int i = 0; i < KM; ++i) {
+        if (i < taken) {
+          const float Ai = A[i];
+          float cur = Ai;
+#pragma unroll
+          for (int l = 0; l < i; ++l) {
+            phi[l] -= pt[l][i] * Ai;
+            cur -= gc[l] * pt[l][i];
+          }
+          float phv = phi[i];
+#pragma unroll
+          for (int l = 0; l < i; ++l) phv -= gm[i][l] * phi[l] + gc[l] * rc[i][l];
+          const float hv = cur + rv[i] * phv;
+          if (rho > i) {
+            const float f = rb[i] * hv;
+            Rr[i] = cur - f;
+            const float qf = f * rv[i];
+#pragma unroll
+            for (int l = 0; l < i; ++l) gc[l] -= qf * gm[i][l];
+            gc[i] = qf;
+          } else if (rho < i && w0 && part == 0) {
+            Ss[k * BK_TSTR + j + i] = hv * iv0_own;
+          }
+        }
+      }
+      if (rho >= 0) {
+        // a -= sum_l g_l y_l (a consumed pivot: its own coefficients, then
+        // scaled by 1/v0 into its reflector's vector)
+#pragma unroll
+        for (int l = 0; l < KM; ++l)
+          if (l < taken) {
+            const float *y = px[par][l];
+            const float gl = gc[l];
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                a[i][e] = fmaf(-gl, y[BK_LI * i + 4 * part + e], a[i][e]);
+          }
+        if (rho < taken) {
+          // (with the triangular-factor output, workgroup 0's R rows above
+          // the pivot's diagonal row keep their values)
+          const bool keep_r = w0 && want_r;
+#pragma unroll
+          for (int i = 0; i < NI; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (!keep_r || i >= NIM || BK_LI * i + 4 * part + e > k) a[i][e] *= iv0_own;
+        }
         if (w0 && want_r) {
-          if (part == pj0) bk_reg_add<NIM>(a, ij0, -f);
-          if (part == pj1) bk_reg_add<NIM>(a, ij1, -(fsp * fs1 * Bj + fp));
+          // R rows j..: R[j+s][k] = Rr[s] for the reflectors applied to this
+          // column, and the R diagonal for a consumed pivot
+          const int nl = rho < taken ? rho : taken;
+#pragma unroll
+          for (int s = 0; s < KM; ++s) {
+            const int row = j + s;
+            if (s < nl && part == ((row >> 2) & (BK_PARTS - 1)))
+              bk_reg_set<NIM>(a, (row / BK_LI) * 4 + (row & 3), Rr[s]);
+          }
+          if (rho < taken && part == ((k >> 2) & (BK_PARTS - 1)))
+            bk_reg_set<NIM>(a, (k / BK_LI) * 4 + (k & 3), rj_own);
         }
-      } else {
-        // a -= f v with v = [1 at the diagonal row; x / v0 below it]; in
-        // workgroup 0 the broadcast x is zero at and above the diagonal row
-#pragma unroll
-        for (int i = 0; i < NI; ++i)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) a[i][e] = fmaf(-fs, x[BK_LI * i + 4 * part + e], a[i][e]);
-        if (w0 && want_r && part == pj0) bk_reg_add<NIM>(a, ij0, -f);   // v_j = 1 in row j (an R row)
-      }
-    } else if (k == j) {
-      // (without the triangular-factor output, the rows at and above the
-      // diagonal of workgroup 0 are never read again: scaled like the rest)
-      if (w0 && want_r) {
-#pragma unroll
-        for (int i = 0; i < NI; ++i)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int lr = BK_LI * i + 4 * part + e;
-            if (i < NIM)
-              a[i][e] = (lr > j) ? a[i][e] * inv_v0 : ((lr == j) ? rjj : a[i][e]);
-            else
-              a[i][e] *= inv_v0;
-          }
-      } else {
-#pragma unroll
-        for (int i = 0; i < NI; ++i)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) a[i][e] *= inv_v0;
-      }
-    } else if (pair && k == j + 1) {
-      // column j+1: H_j, then its own reflector (R entry in row j, R
-      // diagonal in row j+1, v below; rows up to j+1 of workgroup 0 matter
-      // only for the triangular-factor output)
-      if (w0 && want_r) {
-#pragma unroll
-        for (int i = 0; i < NI; ++i)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int lr = BK_LI * i + 4 * part + e;
-            const float v = fmaf(-fs1, x[lr], a[i][e]) * inv_v02;
-            if (i < NIM)
-              a[i][e] = (lr > j + 1) ? v : ((lr == j + 1) ? rjj2 : ((lr == j) ? a[i][e] - f1 : a[i][e]));
-            else
-              a[i][e] = v;
-          }
-      } else {
-#pragma unroll
-        for (int i = 0; i < NI; ++i)
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            a[i][e] = fmaf(-fs1, x[BK_LI * i + 4 * part + e], a[i][e]) * inv_v02;
       }
     }
-    if (w0) {
-      // S[l][j] = y_l^T v_j for the stored reflectors l < j, and for pairs
-      // S[l][j+1] = y_l^T v_{j+1} (l <= j), from the same sums
-      if (col && part == 0) {
-        if (k < j) {
-          Ss[k * BK_TSTR + j] = A + D * inv_v0;
-          if (pair) Ss[k * BK_TSTR + j + 1] = B + inv_v02 * (E - fs1 * (D - B * Bj));
-        } else if (pair && k == j) {
-          Ss[j * BK_TSTR + j + 1] = Bj * inv_v0 + inv_v0 * inv_v02 * (sxy - fs1 * sxx);
+    if (w0 && t == 0) {
+#pragma unroll
+      for (int i = 0; i < KM; ++i)
+        if (i < taken) {
+          bs[j + i] = rb[i];
+          p.beta[bz * n + c + j + i] = rb[i];
+          p.dsign[bz * n + c + j + i] = (rr[i] < 0.f) ? -1.f : 1.f;
         }
-      }
-      if (t == 0) {
-        bs[j] = bet;
-        p.beta[bz * n + c + j] = bet;
-        p.dsign[bz * n + c + j] = (rjj < 0.f) ? -1.f : 1.f;
-        if (pair) {
-          bs[j + 1] = bet2;
-          p.beta[bz * n + c + j + 1] = bet2;
-          p.dsign[bz * n + c + j + 1] = (rjj2 < 0.f) ? -1.f : 1.f;
-        }
-      }
     }
     // (not after the last round: T's formation clears Ts right after the
     // loop, with no barrier in between)
-    if (jl + 1 < nb) save_diag_rows();
-    j = jl + 1;
+    if (j + taken < nb) save_diag_rows();
+    j += taken;
   }
   // Write Y (zeros above its diagonal, ones on it) and the R entries of the
   // block's diagonal rows.  An aborted exchange poisons the block.
@@ -1037,11 +1104,18 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         }
       }
   }
-  // The next block's slots (the other area) back to the empty pattern.
-  if (p.next_words > 0) {
+  {
+    // The words this block wrote, for the emptying after the next block;
+    // then what the previous block wrote into the other area (which the next
+    // block uses) back to the empty pattern.
+    if (w0 && t == 0)
+      __hip_atomic_store(X + BK_XUSED + p.area, P > 1 ? (unsigned)(round * NB * cw) : 0u,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int64_t used = (int64_t)__hip_atomic_load(X + BK_XUSED + (1 - p.area), __ATOMIC_RELAXED,
+                                                    __HIP_MEMORY_SCOPE_AGENT);
     uint4 *nx = reinterpret_cast<uint4 *>(X + BK_XHDR + (1 - p.area) * p.area_words);
     const uint4 e4 = make_uint4(BK_EMPTY, BK_EMPTY, BK_EMPTY, BK_EMPTY);
-    for (int64_t i = (int64_t)g * BK_THREADS + t; i < p.next_words / 4; i += (int64_t)P * BK_THREADS)
+    for (int64_t i = (int64_t)g * BK_THREADS + t; i < used / 4; i += (int64_t)P * BK_THREADS)
       nx[i] = e4;
   }
   if (!w0) return;
@@ -1291,14 +1365,15 @@ __global__ __launch_bounds__(64) void qr_raise_abort_kernel(unsigned *xch, int64
                        __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Exchange areas at the start of a call: header words zero, the first
-// block's slots (the first `first` words of area 0) empty.
+// Exchange areas at the start of a call: header words zero, area 0 (the
+// first block's) empty, and area 1 marked as written throughout, so that the
+// first block empties all of it for the second.
 __global__ __launch_bounds__(256) void qr_xch_init_kernel(unsigned *xch, int64_t xstride,
-                                                          int64_t first) {
+                                                          int64_t area_words) {
   unsigned *X = xch + (int64_t)blockIdx.y * xstride;
-  const int64_t cnt = BK_XHDR + first;
+  const int64_t cnt = BK_XHDR + area_words;
   for (int64_t i = blockIdx.x * 256 + threadIdx.x; i < cnt; i += (int64_t)gridDim.x * 256)
-    X[i] = (i < BK_XHDR) ? 0u : BK_EMPTY;
+    X[i] = (i < BK_XHDR) ? (i == BK_XUSED + 1 ? (unsigned)area_words : 0u) : BK_EMPTY;
 }
 
 // dst = src^T for one n x n matrix, through 32 x 32 LDS tiles.
@@ -1493,21 +1568,16 @@ hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
   if (!x.L.block) return panel_phase(x, ob, s);
   const int c = (int)(ob * NB);
   const int nb = (int)std::min<int64_t>(NB, x.n - c);
-  bool small = false, small_next = false;
+  bool small = false;
   const int P = block_launch_p(x, ob, &small);
-  int64_t next_words = 0;
-  if (c + nb < x.n) {
-    const int Pn = block_launch_p(x, ob + 1, &small_next);
-    next_words = bk_block_words(std::min<int64_t>(NB, x.n - c - nb), Pn);
-  }
   BlockParams bp{x.At, x.sA, x.ni, c, nb, x.Tb + ob * NB * NB, x.L.sT, x.Rf, x.dsign, x.betas,
-                 x.xch, bk_xstride(x.n), bk_area_words(x.n), (int)(ob & 1), next_words, P,
+                 x.xch, bk_xstride(x.n), bk_area_words(x.n), (int)(ob & 1), P,
                  x.status, x.status_bit};
   const dim3 grid((unsigned)P, (unsigned)x.batch);
   if (small)
-    hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL>), grid, dim3(BK_THREADS), 0, s, bp);
+    hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL, BK_K_SMALL>), grid, dim3(BK_THREADS), 0, s, bp);
   else
-    hipLaunchKernelGGL((qr_block_kernel<BK_R>), grid, dim3(BK_THREADS), 0, s, bp);
+    hipLaunchKernelGGL((qr_block_kernel<BK_R, BK_K_BIG>), grid, dim3(BK_THREADS), 0, s, bp);
   return hipGetLastError();
 }
 
@@ -1788,8 +1858,8 @@ int resident_cap(bool small, hipError_t *err) {
   if (c == 0) {
     int per_cu = 0, cus = 0;
     *err = small ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                       &per_cu, qr_block_kernel<BK_R_SMALL>, BK_THREADS, 0)
-                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, qr_block_kernel<BK_R>,
+                       &per_cu, qr_block_kernel<BK_R_SMALL, BK_K_SMALL>, BK_THREADS, 0)
+                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, qr_block_kernel<BK_R, BK_K_BIG>,
                                                                 BK_THREADS, 0);
     if (*err != hipSuccess) return 0;
     if ((*err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) !=
@@ -1852,13 +1922,11 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
   x.skip = nullptr;
   x.sSkip = 0;
-  if (x.L.block) {  // every slot is written once per call: header clear, block 0's slots empty
-    const int64_t xs = bk_xstride(n);
-    bool small0 = false;
-    const int64_t first = bk_block_words(std::min<int64_t>(NB, n), block_launch_p(x, 0, &small0));
-    const unsigned gx = (unsigned)std::min<int64_t>((BK_XHDR + first + 255) / 256, 1024);
+  if (x.L.block) {  // header clear, area 0 empty, area 1 emptied by the first block
+    const int64_t xs = bk_xstride(n), aw = bk_area_words(n);
+    const unsigned gx = (unsigned)std::min<int64_t>((BK_XHDR + aw + 255) / 256, 1024);
     hipLaunchKernelGGL(qr_xch_init_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, x.xch, xs,
-                       first);
+                       aw);
     SOAP_TRY(hipGetLastError());
     x.skip = x.xch + BK_XFAILED;
     x.sSkip = xs;
