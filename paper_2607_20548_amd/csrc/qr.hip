@@ -955,7 +955,12 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
           float ref = ph[i][i];
 #pragma unroll
           for (int s = 0; s <= i; ++s) ref += pt[i][s] * pt[i][s];
-          const bool ok = (i == 0) || (st >= 0.f && x0 * x0 + st >= BK_TAU * ref);
+          // (every lane holds the same totals: the decision is read from lane 0
+          // so that the round's bounds stay wave-uniform scalars)
+          const bool ok =
+              __builtin_amdgcn_readfirstlane((i == 0 || (st >= 0.f && x0 * x0 + st >= BK_TAU * ref))
+                                                 ? 1
+                                                 : 0) != 0;
           if (!ok) {
             taken = i;
           } else {
