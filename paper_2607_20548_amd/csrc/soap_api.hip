@@ -699,9 +699,9 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     return hipSuccess;
   };
   // T_G = Q_L^T G,  T_M = Q_L^T M on the L side's block stream (free once the
-  // L-side QR is done), capped to part of the GPU (the R-side block kernels
-  // need whole compute units free); when the L side runs early they are
-  // still held back to the R-side factorization's tail.
+  // L-side QR is done), held back to the R-side factorization's second half;
+  // beside a much larger R side they are capped to part of the GPU (its
+  // block kernels need whole compute units free).
   auto rotate_in_l = [&](bool after_mid) -> hipError_t {
     hipError_t r;
     if ((r = hipStreamWaitEvent(spl, ev_lside, 0)) != hipSuccess) { side_where = "L side wait"; return r; }
@@ -715,7 +715,11 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
     d.A = QL; d.lda = m; d.sA = mm; d.B = grad; d.ldb = n; d.sB = mn;
     // T_G and T_M interleaved by rows over the T_G and T_M buffers (adjacent,
     // 2 m n floats per matrix): row 2i = T_G row i, row 2i+1 = T_M row i.
-    d.C = TG; d.ldc = 2 * n; d.sC = 2 * mn; d.batch = batch; d.max_wg = kSideWorkgroups;
+    // Capped only beside a much larger R-side factorization; otherwise the
+    // two QRs are of similar size (or the L side is the larger) and this
+    // product runs when the R side has no resident blocks left to starve.
+    d.C = TG; d.ldc = 2 * n; d.sC = 2 * mn; d.batch = batch;
+    d.max_wg = late_l ? kSideWorkgroups : 0;
     if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { side_where = "rotate in G"; return r; }
     d.B = M; d.C = TG + n;
     if ((r = soap::launch_gemm(d, spl)) != hipSuccess) { side_where = "rotate in M"; return r; }
