@@ -531,11 +531,12 @@ constexpr int BK_R = 32;                        // rows per thread
 constexpr int BK_ROWS = BK_PARTS * BK_R;        // rows per workgroup
 // Blocks with few rows take half as many rows per thread (twice the
 // workgroups): the work of each round halves while the exchange grows by P
-// items per column (measured on 14336 x 14336: faster up to about 32
-// workgroups, slower from about 40 on).
+// items per column (with four-column rounds, measured on the 4096 x 4096 and
+// 24-layer steps: best up to 24 workgroups, 16 and 32 slightly slower, 40
+// slower still).
 constexpr int BK_R_SMALL = 16;
 constexpr int BK_ROWS_SMALL = BK_PARTS * BK_R_SMALL;
-constexpr int BK_SMALL_MAX_P = 32;
+constexpr int BK_SMALL_MAX_P = 24;
 constexpr int BK_LI = 4 * BK_PARTS;             // local-row stride of a thread's register groups
 constexpr int BK_MAX_P = 64;                    // workgroups per matrix (n <= 16384)
 constexpr int BK_MAX_WG = 96;                   // workgroups per launch
