@@ -1258,16 +1258,20 @@ __global__ __launch_bounds__(256) void qr_assemble_pair_t_kernel(float *TP, int6
 // the partials into LDS, stages T, and forms its 8 columns of T^T W (k in
 // increasing order).  Replaces a reduction pass and a latency-bound GEMM with
 // K = nb on the factorization's critical path.
+template <int CW>
 __global__ __launch_bounds__(256) void qr_reduce_tt_kernel(const float *__restrict__ part,
                                                                 int S, int nb, int Nt,
                                                                 const float *__restrict__ T,
                                                                 int64_t sT, float *__restrict__ W2,
                                                                 int64_t sW) {
+  // CW columns per workgroup; EPT entries per thread, loaded SB slices at a
+  // time (32 loads in flight per thread)
+  constexpr int EPT = NB * CW / 256, SB = 32 / EPT;
   __shared__ float Ts[NB][NB + 1];
-  __shared__ float Ws[NB][8];
+  __shared__ float Ws[NB][CW];
   const int64_t bz = blockIdx.y;
   const int t = threadIdx.x;
-  const int j0 = blockIdx.x * 8;
+  const int j0 = blockIdx.x * CW;
   const float *Tb = T + bz * sT;
   if (nb == NB && (reinterpret_cast<uintptr_t>(Tb) & 15u) == 0) {   // 16 float4 per thread
     const float4 *T4 = reinterpret_cast<const float4 *>(Tb);
@@ -1287,42 +1291,43 @@ __global__ __launch_bounds__(256) void qr_reduce_tt_kernel(const float *__restri
   }
   const int64_t slice = (int64_t)nb * Nt;
   const float *pb = part + bz * S * slice;
-  // Four entries per thread, slices in order; loads issued eight slices at a
-  // time so that their latencies overlap.
-  float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  int64_t off[4];
-  bool ok[4];
+  // EPT entries per thread, slices summed in order, SB at a time so that
+  // their load latencies overlap.
+  float acc[EPT];
+  int64_t off[EPT];
+  bool ok[EPT];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int e = t + 256 * q, k = e >> 3, j = j0 + (e & 7);
+  for (int q = 0; q < EPT; ++q) {
+    const int e = t + 256 * q, k = e / CW, j = j0 + (e % CW);
+    acc[q] = 0.f;
     ok[q] = k < nb && j < Nt;
     off[q] = ok[q] ? (int64_t)k * Nt + j : 0;
   }
-  for (int s0 = 0; s0 < S; s0 += 8) {
-    float v[8][4];
+  for (int s0 = 0; s0 < S; s0 += SB) {
+    float v[SB][EPT];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < SB; ++u)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
+      for (int q = 0; q < EPT; ++q)
         v[u][q] = (s0 + u < S && ok[q]) ? pb[(int64_t)(s0 + u) * slice + off[q]] : 0.f;
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
+    for (int u = 0; u < SB; ++u)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[q] += v[u][q];
+      for (int q = 0; q < EPT; ++q) acc[q] += v[u][q];
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
+  for (int q = 0; q < EPT; ++q) {
     const int e = t + 256 * q;
-    Ws[e >> 3][e & 7] = acc[q];
+    Ws[e / CW][e % CW] = acc[q];
   }
   __syncthreads();
   float *Wb = W2 + bz * sW;
-  for (int e = t; e < NB * 8; e += 256) {
-    const int i = e >> 3, c = e & 7, j = j0 + c;
+  for (int e = t; e < NB * CW; e += 256) {
+    const int i = e / CW, c = e % CW, j = j0 + c;
     if (i >= nb || j >= Nt) continue;
-    float acc = 0.f;
-    for (int k = 0; k < nb; ++k) acc += Ts[k][i] * Ws[k][c];
-    Wb[(int64_t)i * Nt + j] = acc;
+    float a = 0.f;
+    for (int k = 0; k < nb; ++k) a += Ts[k][i] * Ws[k][c];
+    Wb[(int64_t)i * Nt + j] = a;
   }
 }
 
@@ -1656,8 +1661,14 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   g1.partials_only = fused;
   SOAP_TRY(launch_gemm(g1, s));
   if (fused) {   // W2 = T^T (sum of the partials) in one pass
-    hipLaunchKernelGGL(qr_reduce_tt_kernel, dim3((unsigned)((Nt + 7) / 8), (unsigned)x.batch),
-                       dim3(256), 0, s, Sk, g1.splitk, (int)nb, (int)Nt, Tob, x.L.sT, W2, sW);
+    // many slices (the near update's): two columns per workgroup, so that
+    // each thread's loads are in flight together
+    if (g1.splitk > 8)
+      hipLaunchKernelGGL(qr_reduce_tt_kernel<2>, dim3((unsigned)((Nt + 1) / 2), (unsigned)x.batch),
+                         dim3(256), 0, s, Sk, g1.splitk, (int)nb, (int)Nt, Tob, x.L.sT, W2, sW);
+    else
+      hipLaunchKernelGGL(qr_reduce_tt_kernel<8>, dim3((unsigned)((Nt + 7) / 8), (unsigned)x.batch),
+                         dim3(256), 0, s, Sk, g1.splitk, (int)nb, (int)Nt, Tob, x.L.sT, W2, sW);
     SOAP_TRY(hipGetLastError());
   }
   // W2 = T^T W
