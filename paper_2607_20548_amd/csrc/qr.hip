@@ -1424,6 +1424,9 @@ constexpr int MAX_SPLIT = 8;
 // longer K brings the update near the long-K products' rate, which outweighs
 // the coarser trapezoid (1.5 w / n more flops than the block-level count).
 constexpr int64_t OCT_MIN_N = 8192;
+// Shortest K slice of the near update's first product (its split-K slices
+// run side by side: shorter slices, more workgroups, less latency).
+constexpr int64_t NEAR_MIN_K = 64;
 
 QrLayout qr_layout(int64_t batch, int64_t n) {
   QrLayout L{};
@@ -1442,7 +1445,7 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.sSx = L.np * 2 * NB * NB;
   L.sSkp = (int64_t)64 * NB * NB;
   L.sWn = (int64_t)2 * NB * NB;
-  L.sSkn = std::max<int64_t>(1, std::min<int64_t>(64, n / 256)) * NB * NB;
+  L.sSkn = std::max<int64_t>(1, std::min<int64_t>(64, n / NEAR_MIN_K)) * NB * NB;
   L.sTQ = L.nq * 16 * NB * NB;
   L.sSq = L.nq * 8 * NB * NB;
   L.sTO = L.no * 64 * NB * NB;
@@ -1556,11 +1559,11 @@ struct QrCtx {
 hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
 
 // Split-K for a latency-critical product with a single tile row/column
-// (M, N <= NB, e.g. the near update's W = Y^T A_next): enough slices to fill
-// the GPU with at least 256 of K each, within the partial buffer of
-// cap_floats floats.
-int narrow_split(int64_t M, int64_t N, int64_t K, int64_t batch, int64_t cap_floats) {
-  int64_t s = std::min<int64_t>(64, K / 256);
+// (M, N <= NB, e.g. the near update's W = Y^T A_next): up to 64 slices of at
+// least min_k of K each, within the partial buffer of cap_floats floats.
+int narrow_split(int64_t M, int64_t N, int64_t K, int64_t batch, int64_t cap_floats,
+                 int64_t min_k = 256) {
+  int64_t s = std::min<int64_t>(64, K / min_k);
   s = std::min<int64_t>(s, cap_floats / std::max<int64_t>(1, M * N * batch));
   return (int)std::max<int64_t>(1, s);
 }
@@ -1651,7 +1654,7 @@ hipError_t trailing_update(const QrCtx &x, int64_t ob, int64_t j0, int64_t j1, h
   g1.A = x.At + c * n + c; g1.lda = n; g1.sA = x.sA;
   g1.B = x.At + j0 * n + c; g1.ldb = n; g1.sB = x.sA;
   g1.C = Wb; g1.ldc = Nt; g1.sC = sW; g1.batch = x.batch;
-  g1.splitk = (Nt <= NB) ? narrow_split(nb, Nt, Kr, x.batch, skcap)
+  g1.splitk = (Nt <= NB) ? narrow_split(nb, Nt, Kr, x.batch, skcap, near ? NEAR_MIN_K : 256)
                           : choose_splitk(nb, Nt, Kr, x.batch, MAX_SPLIT);
   g1.part = Sk;
   // split products sum their slices and form T^T W in one pass (the near
