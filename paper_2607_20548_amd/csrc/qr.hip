@@ -714,9 +714,10 @@ __device__ __forceinline__ void bk_reflector(float x0, float st, float &bet, flo
     inv_v0 = 0.f;
     rjj = x0;
   } else {
-    const float sigma = sqrtf(x0 * x0 + st);
+    // hardware square root and reciprocals (1 ulp each): beta is formed from
+    // v0 as computed, so the reflector stays orthogonal to rounding
+    const float sigma = __builtin_amdgcn_sqrtf(x0 * x0 + st);
     const float v0 = (x0 >= 0.f) ? (x0 + sigma) : (x0 - sigma);
-    // hardware reciprocals (1 ulp): these feed every column's update
     bet = 2.f * v0 * v0 * __builtin_amdgcn_rcpf(st + v0 * v0);
     inv_v0 = __builtin_amdgcn_rcpf(v0);
     rjj = (x0 >= 0.f) ? -sigma : sigma;
@@ -743,7 +744,7 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   // workgroup 0 (local row BK_LI i + 4 part + e < NB); only these need masks
   constexpr int NIM = (NB / BK_LI < NI) ? NB / BK_LI : NI;
   __shared__ float px[2][KM][RS];   // pivot tails, by round parity
-  __shared__ float pv[2][KM][8];    // pivot totals: dots, diagonal-row values
+  __shared__ __align__(16) float pv[2][KM][8];  // pivot totals: dots, diagonal-row values
   __shared__ float bs[NB];               // beta_j (workgroup 0)
   __shared__ float Ss[NB * BK_TSTR];     // S (workgroup 0), row-major
   __shared__ float Ts[NB * BK_TSTR];     // T (workgroup 0), row-major
@@ -921,15 +922,20 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
     float pt[KM][KM], rb[KM], rv[KM], rr[KM], gm[KM][KM], rc[KM][KM];
     int taken = kr;
     {
+      // (rows and columns past kr hold stale values: no step below reads them
+      // into a value it keeps, since every step i < taken <= kr reads only
+      // indices below i or its own row)
       float ph[KM][KM];
 #pragma unroll
       for (int m = 0; m < KM; ++m) {
         rb[m] = rv[m] = rr[m] = 0.f;
+        float row[8];
+        *reinterpret_cast<float4 *>(&row[0]) = *reinterpret_cast<const float4 *>(&pv[par][m][0]);
+        *reinterpret_cast<float4 *>(&row[4]) = *reinterpret_cast<const float4 *>(&pv[par][m][4]);
 #pragma unroll
         for (int l = 0; l < KM; ++l) {
-          const bool in = m < kr && l < kr;
-          ph[m][l] = in ? pv[par][m][l] : 0.f;
-          pt[m][l] = in ? pv[par][m][KM + l] : 0.f;
+          ph[m][l] = row[l];
+          pt[m][l] = row[KM + l];
           gm[m][l] = rc[m][l] = 0.f;
         }
       }
