@@ -542,7 +542,7 @@ constexpr int BK_MAX_P = 64;                    // workgroups per matrix (n <= 1
 constexpr int BK_MAX_WG = 96;                   // workgroups per launch
 constexpr unsigned BK_SPIN_LIMIT = 1u << 22;
 constexpr int BK_TSTR = NB + 4;                 // LDS row stride of T and S (spreads banks)
-constexpr int BK_KMAX = 4;                      // columns per round at most
+constexpr int BK_KMAX = 8;                      // columns per round at most
 // A round stops before pivot j+i (i > 0) when the reflectors j..j+i-1 leave
 // less than this fraction of its squared norm (rows j+i.. after them against
 // rows j.. before them): the sums that give its reflector would lose digits
@@ -724,10 +724,18 @@ __device__ __forceinline__ void bk_reflector(float x0, float st, float &bet, flo
   }
 }
 
-// Columns per round of the two block kernels (rows per thread BK_R and
-// BK_R_SMALL).
+// Columns per round of the block kernels: up to eight with 16 rows per
+// thread (BK_R_SMALL) and with 32 rows per thread for launches of at most
+// BK_MID_MAX_P workgroups (the gather then holds one dot's P partials per
+// lane), four for the wider 32-row launches (two lanes per dot).
 constexpr int BK_K_BIG = 4;
-constexpr int BK_K_SMALL = 4;
+constexpr int BK_K_MID = 8;
+constexpr int BK_MID_MAX_P = 16;
+constexpr int BK_K_SMALL = 8;
+// Parameters of one reflector of a round of more than four columns, as the
+// column loop reads them (an LDS row of bk_prm_words(K) floats): beta, 1/v0,
+// R diagonal, (unused), gamma_i[l], c_i[l], p_l[i] (l < K).
+constexpr int bk_prm_words(int K) { return 4 + 3 * K; }
 
 template <int R, int KM>
 __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
@@ -738,16 +746,36 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   // (K' = columns of the round rounded up to a power of two), at most H
   // (registers).  Launches of the big kernel with more than 56 workgroups
   // (orders past 14336) take two columns per round.
-  constexpr int KP2 = KM > 2 ? 4 : KM;
-  constexpr int H = (R == BK_R && KP2 == 4) ? 28 : ((R == BK_R ? BK_MAX_P : BK_SMALL_MAX_P) * KP2 + 7) / 8;
+  constexpr int KP2 = KM > 4 ? 8 : (KM > 2 ? 4 : KM);
+  constexpr int H = R == BK_R ? (KM > 4 ? BK_MID_MAX_P : 28) : (BK_SMALL_MAX_P * KP2 + 7) / 8;
+  // rounds of more than four columns form their reflectors in wave 0, one
+  // lane per pivot, and leave them in LDS for every column
+  constexpr bool LANE_PIVOTS = KM > 4;
+  constexpr int PRM = bk_prm_words(KM);
   // register groups i that can hold one of the diagonal rows 0..NB-1 of
   // workgroup 0 (local row BK_LI i + 4 part + e < NB); only these need masks
   constexpr int NIM = (NB / BK_LI < NI) ? NB / BK_LI : NI;
-  __shared__ float px[2][KM][RS];   // pivot tails, by round parity
-  __shared__ __align__(16) float pv[2][KM][8];  // pivot totals: dots, diagonal-row values
-  __shared__ float bs[NB];               // beta_j (workgroup 0)
-  __shared__ float Ss[NB * BK_TSTR];     // S (workgroup 0), row-major
-  __shared__ float Ts[NB * BK_TSTR];     // T (workgroup 0), row-major
+  // One LDS block, the small arrays that every round reads first (their
+  // addresses then fit the 16-bit offset of an LDS instruction).
+  struct Lds {
+    float pv[2][KM][2 * KM];            // pivot totals: dots, diagonal-row values
+    float prm[LANE_PIVOTS ? KM : 1][PRM];   // the round's reflectors
+    float bs[NB];                       // beta_j (workgroup 0)
+    float px[2][KM][RS];                // pivot tails, by round parity
+    float Ss[NB * BK_TSTR];             // S (workgroup 0), row-major
+    float Ts[NB * BK_TSTR];             // T (workgroup 0), row-major
+    int prm_taken;                      // reflectors the round takes
+  };
+  static_assert(sizeof(float) * (2 * 2 * KM * KM + (LANE_PIVOTS ? KM : 1) * PRM + NB) % 16 == 0,
+                "16-byte aligned LDS arrays");
+  __shared__ __align__(16) Lds lds;
+  auto &pv = lds.pv;
+  auto &prm = lds.prm;
+  auto &bs = lds.bs;
+  auto &px = lds.px;
+  float *const Ss = lds.Ss;
+  float *const Ts = lds.Ts;
+  int &prm_taken = lds.prm_taken;
 
   const int g = blockIdx.x;
   const int64_t bz = blockIdx.y;
@@ -819,7 +847,13 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   int round = 0;
   for (; j < nb; ++round) {
     const int par = round & 1;
-    const int kr = min((KM > 2 && (P * KP2 + 7) / 8 > H) ? 2 : KM, nb - j);
+    // columns this round: the most (a power of two up to KM) whose partials
+    // fit H items per lane of a gather
+    int kcap = KM;
+#pragma unroll
+    for (int q = 0; q < 3; ++q)
+      if (kcap > 1 && (P * kcap + 7) / 8 > H) kcap >>= 1;
+    const int kr = min(kcap, nb - j);
     const int rho = k - j;                          // this column's index in the round
     if (rho >= 0 && rho < kr) {
       float *dst = px[par][rho];
@@ -872,7 +906,14 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         for (int q = 1; q < KM; ++q)
           if (part == q) mine = D[q];
         if (part < kr) bk_put(cb + ((int64_t)part * P + g) * NB, mine);
-        if (w0 && part >= 4 && part - 4 < kr) {
+        if (KM > 4 && w0 && part < kr) {
+          float tv = A[0];
+#pragma unroll
+          for (int s = 1; s < KM; ++s)
+            if (part == s) tv = A[s];
+          bk_put(cb + ((int64_t)KM * P + part) * NB, tv);
+        }
+        if (KM <= 4 && w0 && part >= 4 && part - 4 < kr) {
           float tv = A[0];
 #pragma unroll
           for (int s = 1; s < KM; ++s)
@@ -881,22 +922,27 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
         }
       }
       if (col && (w0 || k >= j)) {
-        const int lg = (kr == 1) ? 3 : ((kr == 2) ? 2 : 1);    // log2 lanes per dot
+        const int lg = (kr == 1) ? 3 : ((kr == 2) ? 2 : (kr <= 4 ? 1 : 0));   // log2 lanes per dot
         const int q = part >> lg, h = part & ((1 << lg) - 1);
         const int hn = (P + (1 << lg) - 1) >> lg;
         const int g0 = h * hn;
         const int cnt = (q < kr) ? max(0, min(P - g0, hn)) : 0;
-        const int xoff = (!w0 && part < kr) ? (int)(((KM * P + part) * NB + pk) * 4) : -1;
+        // (the column position is formed again from the thread index each
+        // round: kept across the loop, its offsets would go to scratch)
+        int tq = t;
+        asm volatile("" : "+v"(tq));
+        const int pkq = (tq >> 6) * (64 / BK_PARTS) + (tq & 63) / BK_PARTS;
+        const int xoff = (!w0 && part < kr) ? ((KM * P + part) * NB + pkq) * 4 : -1;
         const __amdgpu_buffer_rsrc_t rs =
             __builtin_amdgcn_make_buffer_rsrc(sl, (short)0, (int)(NB * cw * 4), BK_RSRC_WORD3);
         float ssum = 0.f, xval = 0.f;
         if (alive)
-          alive = bk_gather<H>(rs, (unsigned)(((q * P + g0) * NB + pk) * 4), cnt, xoff, abort_flag,
+          alive = bk_gather<H>(rs, (unsigned)(((q * P + g0) * NB + pkq) * 4), cnt, xoff, abort_flag,
                                ssum, xval);
         float s = ssum;
         if (lg == 1) s = bk_sum2(s);
         else if (lg == 2) s = bk_sum4(s);
-        else s = bk_sum8(s);
+        else if (lg == 3) s = bk_sum8(s);
 #pragma unroll
         for (int qq = 0; qq < KM; ++qq)
           if (qq < kr) D[qq] = __shfl(s, lbase + (qq << lg));
@@ -915,177 +961,355 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
       }
     }
     __syncthreads();
-    // The round's reflectors from the pivots' totals, formed alike in every
-    // thread (registers only): pt[m][s] = p_m[s], ph[m][l] = Phi_i(p_l, p_m),
-    // gm[m][l] = coefficients of pivot m (l < m); per step i: beta rb[i],
-    // 1/v0 rv[i], R diagonal rr[i], gamma_i = gm[i][l] and c_i = rc[i][l].
-    float pt[KM][KM], rb[KM], rv[KM], rr[KM], gm[KM][KM], rc[KM][KM];
-    int taken = kr;
-    {
-      // (rows and columns past kr hold stale values: no step below reads them
-      // into a value it keeps, since every step i < taken <= kr reads only
-      // indices below i or its own row)
-      float ph[KM][KM];
+    if constexpr (LANE_PIVOTS) {
+      // Wave 0 forms the round's reflectors from the pivots' totals, lane m
+      // holding pivot m's row of ph, pt and gm (the quantities of the
+      // per-thread form below); each step reads the values it needs from
+      // other lanes as wave-uniform scalars and leaves, in prm[i], what the
+      // column loop needs of reflector i.  Every workgroup runs the same
+      // instructions on the same totals.
+      if (wave == 0) {
+        float phr[KM], ptr[KM], gmr[KM];
+        {
+          const int mm = lane < KM ? lane : 0;
+          float row[2 * KM];
 #pragma unroll
-      for (int m = 0; m < KM; ++m) {
-        rb[m] = rv[m] = rr[m] = 0.f;
-        float row[8];
-        *reinterpret_cast<float4 *>(&row[0]) = *reinterpret_cast<const float4 *>(&pv[par][m][0]);
-        *reinterpret_cast<float4 *>(&row[4]) = *reinterpret_cast<const float4 *>(&pv[par][m][4]);
+          for (int q = 0; q < 2 * KM; q += 4)
+            *reinterpret_cast<float4 *>(&row[q]) = *reinterpret_cast<const float4 *>(&pv[par][mm][q]);
 #pragma unroll
-        for (int l = 0; l < KM; ++l) {
-          ph[m][l] = row[l];
-          pt[m][l] = row[KM + l];
-          gm[m][l] = rc[m][l] = 0.f;
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < KM; ++i) {
-        if (i < taken) {
-          // row i leaves the tails Phi(p_l, .), l < i
-#pragma unroll
-          for (int m = 0; m < KM; ++m)
-#pragma unroll
-            for (int l = 0; l < i; ++l) ph[m][l] -= pt[l][i] * pt[m][i];
-          float x0 = pt[i][i];
-#pragma unroll
-          for (int l = 0; l < i; ++l) {
-            x0 -= gm[i][l] * pt[l][i];
-            float v = ph[l][i];
-#pragma unroll
-            for (int l2 = 0; l2 < i; ++l2) v -= gm[i][l2] * ph[l][l2];
-            rc[i][l] = v;
+          for (int l = 0; l < KM; ++l) {
+            phr[l] = row[l];
+            ptr[l] = row[KM + l];
+            gmr[l] = 0.f;
           }
-          float st = ph[i][i];
+        }
+        auto rdl = [](float v, int l) {
+          return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+        };
+        int tk = kr;
 #pragma unroll
-          for (int l = 0; l < i; ++l) st -= gm[i][l] * (ph[i][l] + rc[i][l]);
-          float ref = ph[i][i];
+        for (int i = 0; i < KM; ++i) {
+          if (i < tk) {
+            float spt[KM], sgi[KM], src[KM];
 #pragma unroll
-          for (int s = 0; s <= i; ++s) ref += pt[i][s] * pt[i][s];
-          // (every lane holds the same totals: the decision is read from lane 0
-          // so that the round's bounds stay wave-uniform scalars)
-          const bool ok =
-              __builtin_amdgcn_readfirstlane((i == 0 || (st >= 0.f && x0 * x0 + st >= BK_TAU * ref))
-                                                 ? 1
-                                                 : 0) != 0;
-          if (!ok) {
-            taken = i;
-          } else {
-            bk_reflector(x0, st, rb[i], rv[i], rr[i]);
-            const float bet = rb[i], iv0 = rv[i];
+            for (int l = 0; l < i; ++l) spt[l] = rdl(ptr[i], l);   // p_l[i]
+            // row i leaves the tails Phi(p_l, .), l < i
 #pragma unroll
-            for (int m = i + 1; m < KM; ++m) {
-              float cur = pt[m][i];
-              float phv = ph[m][i];
+            for (int l = 0; l < i; ++l) phr[l] -= spt[l] * ptr[i];
+            // the lane's pivot in row i after reflectors 0..i-1 (x0 in lane i)
+            float cur = ptr[i];
 #pragma unroll
-              for (int l = 0; l < i; ++l) {
-                cur -= gm[m][l] * pt[l][i];
-                phv -= gm[i][l] * ph[m][l] + gm[m][l] * rc[i][l];
+            for (int l = 0; l < i; ++l) cur -= gmr[l] * spt[l];
+#pragma unroll
+            for (int l = 0; l < i; ++l) sgi[l] = rdl(gmr[l], i);   // gamma_i[l]
+            float tt = phr[i];
+#pragma unroll
+            for (int l = 0; l < i; ++l) tt -= sgi[l] * phr[l];
+#pragma unroll
+            for (int l = 0; l < i; ++l) src[l] = rdl(tt, l);       // c_i[l]
+            // Phi_i(current pivot i, lane's pivot) (the squared tail in lane i)
+            float phv = tt;
+#pragma unroll
+            for (int l = 0; l < i; ++l) phv -= gmr[l] * src[l];
+            float ref = phr[i];
+#pragma unroll
+            for (int q = 0; q <= i; ++q) ref += ptr[q] * ptr[q];
+            const float x0 = rdl(cur, i), st = rdl(phv, i), rf = rdl(ref, i);
+            if (i > 0 && !(st >= 0.f && x0 * x0 + st >= BK_TAU * rf)) {
+              tk = i;
+            } else {
+              float bet, iv0, rjj;
+              bk_reflector(x0, st, bet, iv0, rjj);
+              float *pr = prm[i];
+              if (lane == i) {
+                pr[0] = bet;
+                pr[1] = iv0;
+                pr[2] = rjj;
+#pragma unroll
+                for (int l = 0; l < i; ++l) pr[4 + l] = gmr[l];
               }
-              const float qf = bet * (cur + iv0 * phv) * iv0;
+              if (lane < i) {
+                pr[4 + KM + lane] = tt;
+                pr[4 + 2 * KM + lane] = ptr[i];
+              }
+              if (lane > i && lane < KM) {
+                const float qf = bet * (cur + iv0 * phv) * iv0;
 #pragma unroll
-              for (int l = 0; l < i; ++l) gm[m][l] -= qf * gm[i][l];
-              gm[m][i] = qf;
+                for (int l = 0; l < i; ++l) gmr[l] -= qf * sgi[l];
+                gmr[i] = qf;
+              }
             }
           }
         }
+        if (lane == 0) prm_taken = tk;
       }
-    }
-    // this column's 1/v0 and R diagonal if it is a pivot the round takes
-    float iv0_own = 1.f, rj_own = 0.f;
-#pragma unroll
-    for (int m = 0; m < KM; ++m)
-      if (rho == m && m < taken) {
-        iv0_own = rv[m];
-        rj_own = rr[m];
+      __syncthreads();
+      const int taken = __builtin_amdgcn_readfirstlane(prm_taken);
+      float iv0_own = 1.f, rj_own = 0.f;
+      if (rho >= 0 && rho < taken) {
+        iv0_own = prm[rho][1];
+        rj_own = prm[rho][2];
       }
-    if (col && (rho >= 0 || w0)) {
-      // This column's coefficients, its R entries in rows j.. (Rr) and, for
-      // the reflectors past it, S = y_k^T v (stored and consumed columns).
-      float gc[KM], Rr[KM];
+      if (col && (rho >= 0 || w0)) {
+        // as below, with reflector i's quantities read from prm[i]
+        float gc[KM], Rr[KM], phi[KM];
 #pragma unroll
-      for (int q = 0; q < KM; ++q) gc[q] = Rr[q] = 0.f;
-      float phi[KM];
+        for (int q = 0; q < KM; ++q) {
+          gc[q] = Rr[q] = 0.f;
+          phi[q] = D[q];
+        }
 #pragma unroll
-      for (int q = 0; q < KM; ++q) phi[q] = D[q];
+        for (int i = 0; i < KM; ++i) {
+          if (i < taken) {
+            const float *pr = prm[i];
+            const float bet = pr[0], iv0 = pr[1];
+            const float Ai = A[i];
+            float cur = Ai;
 #pragma unroll
-      for (int i = 0; i < KM; ++i) {
-        if (i < taken) {
-          const float Ai = A[i];
-          float cur = Ai;
+            for (int l = 0; l < i; ++l) {
+              const float pli = pr[4 + 2 * KM + l];
+              phi[l] -= pli * Ai;
+              cur -= gc[l] * pli;
+            }
+            float phv = phi[i];
 #pragma unroll
-          for (int l = 0; l < i; ++l) {
-            phi[l] -= pt[l][i] * Ai;
-            cur -= gc[l] * pt[l][i];
-          }
-          float phv = phi[i];
+            for (int l = 0; l < i; ++l) phv -= pr[4 + l] * phi[l] + gc[l] * pr[4 + KM + l];
+            const float hv = cur + iv0 * phv;
+            if (rho > i) {
+              const float f = bet * hv;
+              Rr[i] = cur - f;
+              const float qf = f * iv0;
 #pragma unroll
-          for (int l = 0; l < i; ++l) phv -= gm[i][l] * phi[l] + gc[l] * rc[i][l];
-          const float hv = cur + rv[i] * phv;
-          if (rho > i) {
-            const float f = rb[i] * hv;
-            Rr[i] = cur - f;
-            const float qf = f * rv[i];
-#pragma unroll
-            for (int l = 0; l < i; ++l) gc[l] -= qf * gm[i][l];
-            gc[i] = qf;
-          } else if (rho < i && w0 && part == 0) {
-            Ss[k * BK_TSTR + j + i] = hv * iv0_own;
+              for (int l = 0; l < i; ++l) gc[l] -= qf * pr[4 + l];
+              gc[i] = qf;
+            } else if (rho < i && w0 && part == 0) {
+              Ss[k * BK_TSTR + j + i] = hv * iv0_own;
+            }
           }
         }
-      }
-      if (rho >= 0) {
-        // a -= sum_l g_l y_l (a consumed pivot: its own coefficients, then
-        // scaled by 1/v0 into its reflector's vector)
+        if (rho >= 0) {
+          // a -= sum_l g_l y_l (a consumed pivot: its own coefficients, then
+          // scaled by 1/v0 into its reflector's vector)
 #pragma unroll
-        for (int l = 0; l < KM; ++l)
-          if (l < taken) {
-            const float *y = px[par][l];
-            const float gl = gc[l];
+          for (int l = 0; l < KM; ++l)
+            if (l < taken) {
+              const float *y = px[par][l];
+              const float gl = gc[l];
+#pragma unroll
+              for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  a[i][e] = fmaf(-gl, y[BK_LI * i + 4 * part + e], a[i][e]);
+            }
+          if (rho < taken) {
+            // (with the triangular-factor output, workgroup 0's R rows above
+            // the pivot's diagonal row keep their values)
+            const bool keep_r = w0 && want_r;
 #pragma unroll
             for (int i = 0; i < NI; ++i)
 #pragma unroll
               for (int e = 0; e < 4; ++e)
-                a[i][e] = fmaf(-gl, y[BK_LI * i + 4 * part + e], a[i][e]);
+                if (!keep_r || i >= NIM || BK_LI * i + 4 * part + e > k) a[i][e] *= iv0_own;
           }
-        if (rho < taken) {
-          // (with the triangular-factor output, workgroup 0's R rows above
-          // the pivot's diagonal row keep their values)
-          const bool keep_r = w0 && want_r;
+          if (w0 && want_r) {
+            // R rows j..: R[j+s][k] = Rr[s] for the reflectors applied to this
+            // column, and the R diagonal for a consumed pivot
+            const int nl = rho < taken ? rho : taken;
 #pragma unroll
-          for (int i = 0; i < NI; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (!keep_r || i >= NIM || BK_LI * i + 4 * part + e > k) a[i][e] *= iv0_own;
-        }
-        if (w0 && want_r) {
-          // R rows j..: R[j+s][k] = Rr[s] for the reflectors applied to this
-          // column, and the R diagonal for a consumed pivot
-          const int nl = rho < taken ? rho : taken;
-#pragma unroll
-          for (int s = 0; s < KM; ++s) {
-            const int row = j + s;
-            if (s < nl && part == ((row >> 2) & (BK_PARTS - 1)))
-              bk_reg_set<NIM>(a, (row / BK_LI) * 4 + (row & 3), Rr[s]);
+            for (int s = 0; s < KM; ++s) {
+              const int row = j + s;
+              if (s < nl && part == ((row >> 2) & (BK_PARTS - 1)))
+                bk_reg_set<NIM>(a, (row / BK_LI) * 4 + (row & 3), Rr[s]);
+            }
+            if (rho < taken && part == ((k >> 2) & (BK_PARTS - 1)))
+              bk_reg_set<NIM>(a, (k / BK_LI) * 4 + (k & 3), rj_own);
           }
-          if (rho < taken && part == ((k >> 2) & (BK_PARTS - 1)))
-            bk_reg_set<NIM>(a, (k / BK_LI) * 4 + (k & 3), rj_own);
         }
       }
-    }
-    if (w0 && t == 0) {
+      if (w0 && t == 0) {
 #pragma unroll
-      for (int i = 0; i < KM; ++i)
-        if (i < taken) {
-          bs[j + i] = rb[i];
-          p.beta[bz * n + c + j + i] = rb[i];
-          p.dsign[bz * n + c + j + i] = (rr[i] < 0.f) ? -1.f : 1.f;
+        for (int i = 0; i < KM; ++i)
+          if (i < taken) {
+            bs[j + i] = prm[i][0];
+            p.beta[bz * n + c + j + i] = prm[i][0];
+            p.dsign[bz * n + c + j + i] = (prm[i][2] < 0.f) ? -1.f : 1.f;
+          }
+      }
+      if (j + taken < nb) save_diag_rows();
+      j += taken;
+    } else {
+      // The round's reflectors from the pivots' totals, formed alike in every
+      // thread (registers only): pt[m][s] = p_m[s], ph[m][l] = Phi_i(p_l, p_m),
+      // gm[m][l] = coefficients of pivot m (l < m); per step i: beta rb[i],
+      // 1/v0 rv[i], R diagonal rr[i], gamma_i = gm[i][l] and c_i = rc[i][l].
+      float pt[KM][KM], rb[KM], rv[KM], rr[KM], gm[KM][KM], rc[KM][KM];
+      int taken = kr;
+      {
+        // (rows and columns past kr hold stale values: no step below reads them
+        // into a value it keeps, since every step i < taken <= kr reads only
+        // indices below i or its own row)
+        float ph[KM][KM];
+#pragma unroll
+        for (int m = 0; m < KM; ++m) {
+          rb[m] = rv[m] = rr[m] = 0.f;
+          float row[8];
+          *reinterpret_cast<float4 *>(&row[0]) = *reinterpret_cast<const float4 *>(&pv[par][m][0]);
+          *reinterpret_cast<float4 *>(&row[4]) = *reinterpret_cast<const float4 *>(&pv[par][m][4]);
+#pragma unroll
+          for (int l = 0; l < KM; ++l) {
+            ph[m][l] = row[l];
+            pt[m][l] = row[KM + l];
+            gm[m][l] = rc[m][l] = 0.f;
+          }
         }
+#pragma unroll
+        for (int i = 0; i < KM; ++i) {
+          if (i < taken) {
+            // row i leaves the tails Phi(p_l, .), l < i
+#pragma unroll
+            for (int m = 0; m < KM; ++m)
+#pragma unroll
+              for (int l = 0; l < i; ++l) ph[m][l] -= pt[l][i] * pt[m][i];
+            float x0 = pt[i][i];
+#pragma unroll
+            for (int l = 0; l < i; ++l) {
+              x0 -= gm[i][l] * pt[l][i];
+              float v = ph[l][i];
+#pragma unroll
+              for (int l2 = 0; l2 < i; ++l2) v -= gm[i][l2] * ph[l][l2];
+              rc[i][l] = v;
+            }
+            float st = ph[i][i];
+#pragma unroll
+            for (int l = 0; l < i; ++l) st -= gm[i][l] * (ph[i][l] + rc[i][l]);
+            float ref = ph[i][i];
+#pragma unroll
+            for (int s = 0; s <= i; ++s) ref += pt[i][s] * pt[i][s];
+            // (every lane holds the same totals: the decision is read from lane 0
+            // so that the round's bounds stay wave-uniform scalars)
+            const bool ok =
+                __builtin_amdgcn_readfirstlane((i == 0 || (st >= 0.f && x0 * x0 + st >= BK_TAU * ref))
+                                                   ? 1
+                                                   : 0) != 0;
+            if (!ok) {
+              taken = i;
+            } else {
+              bk_reflector(x0, st, rb[i], rv[i], rr[i]);
+              const float bet = rb[i], iv0 = rv[i];
+#pragma unroll
+              for (int m = i + 1; m < KM; ++m) {
+                float cur = pt[m][i];
+                float phv = ph[m][i];
+#pragma unroll
+                for (int l = 0; l < i; ++l) {
+                  cur -= gm[m][l] * pt[l][i];
+                  phv -= gm[i][l] * ph[m][l] + gm[m][l] * rc[i][l];
+                }
+                const float qf = bet * (cur + iv0 * phv) * iv0;
+#pragma unroll
+                for (int l = 0; l < i; ++l) gm[m][l] -= qf * gm[i][l];
+                gm[m][i] = qf;
+              }
+            }
+          }
+        }
+      }
+      // this column's 1/v0 and R diagonal if it is a pivot the round takes
+      float iv0_own = 1.f, rj_own = 0.f;
+#pragma unroll
+      for (int m = 0; m < KM; ++m)
+        if (rho == m && m < taken) {
+          iv0_own = rv[m];
+          rj_own = rr[m];
+        }
+      if (col && (rho >= 0 || w0)) {
+        // This column's coefficients, its R entries in rows j.. (Rr) and, for
+        // the reflectors past it, S = y_k^T v (stored and consumed columns).
+        float gc[KM], Rr[KM];
+#pragma unroll
+        for (int q = 0; q < KM; ++q) gc[q] = Rr[q] = 0.f;
+        float phi[KM];
+#pragma unroll
+        for (int q = 0; q < KM; ++q) phi[q] = D[q];
+#pragma unroll
+        for (int i = 0; i < KM; ++i) {
+          if (i < taken) {
+            const float Ai = A[i];
+            float cur = Ai;
+#pragma unroll
+            for (int l = 0; l < i; ++l) {
+              phi[l] -= pt[l][i] * Ai;
+              cur -= gc[l] * pt[l][i];
+            }
+            float phv = phi[i];
+#pragma unroll
+            for (int l = 0; l < i; ++l) phv -= gm[i][l] * phi[l] + gc[l] * rc[i][l];
+            const float hv = cur + rv[i] * phv;
+            if (rho > i) {
+              const float f = rb[i] * hv;
+              Rr[i] = cur - f;
+              const float qf = f * rv[i];
+#pragma unroll
+              for (int l = 0; l < i; ++l) gc[l] -= qf * gm[i][l];
+              gc[i] = qf;
+            } else if (rho < i && w0 && part == 0) {
+              Ss[k * BK_TSTR + j + i] = hv * iv0_own;
+            }
+          }
+        }
+        if (rho >= 0) {
+          // a -= sum_l g_l y_l (a consumed pivot: its own coefficients, then
+          // scaled by 1/v0 into its reflector's vector)
+#pragma unroll
+          for (int l = 0; l < KM; ++l)
+            if (l < taken) {
+              const float *y = px[par][l];
+              const float gl = gc[l];
+#pragma unroll
+              for (int i = 0; i < NI; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  a[i][e] = fmaf(-gl, y[BK_LI * i + 4 * part + e], a[i][e]);
+            }
+          if (rho < taken) {
+            // (with the triangular-factor output, workgroup 0's R rows above
+            // the pivot's diagonal row keep their values)
+            const bool keep_r = w0 && want_r;
+#pragma unroll
+            for (int i = 0; i < NI; ++i)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (!keep_r || i >= NIM || BK_LI * i + 4 * part + e > k) a[i][e] *= iv0_own;
+          }
+          if (w0 && want_r) {
+            // R rows j..: R[j+s][k] = Rr[s] for the reflectors applied to this
+            // column, and the R diagonal for a consumed pivot
+            const int nl = rho < taken ? rho : taken;
+#pragma unroll
+            for (int s = 0; s < KM; ++s) {
+              const int row = j + s;
+              if (s < nl && part == ((row >> 2) & (BK_PARTS - 1)))
+                bk_reg_set<NIM>(a, (row / BK_LI) * 4 + (row & 3), Rr[s]);
+            }
+            if (rho < taken && part == ((k >> 2) & (BK_PARTS - 1)))
+              bk_reg_set<NIM>(a, (k / BK_LI) * 4 + (k & 3), rj_own);
+          }
+        }
+      }
+      if (w0 && t == 0) {
+#pragma unroll
+        for (int i = 0; i < KM; ++i)
+          if (i < taken) {
+            bs[j + i] = rb[i];
+            p.beta[bz * n + c + j + i] = rb[i];
+            p.dsign[bz * n + c + j + i] = (rr[i] < 0.f) ? -1.f : 1.f;
+          }
+      }
+      // (not after the last round: T's formation clears Ts right after the
+      // loop, with no barrier in between)
+      if (j + taken < nb) save_diag_rows();
+      j += taken;
     }
-    // (not after the last round: T's formation clears Ts right after the
-    // loop, with no barrier in between)
-    if (j + taken < nb) save_diag_rows();
-    j += taken;
   }
   // Write Y (zeros above its diagonal, ones on it) and the R entries of the
   // block's diagonal rows.  An aborted exchange poisons the block.
@@ -1596,6 +1820,8 @@ hipError_t factor_block(const QrCtx &x, int64_t ob, hipStream_t s) {
   const dim3 grid((unsigned)P, (unsigned)x.batch);
   if (small)
     hipLaunchKernelGGL((qr_block_kernel<BK_R_SMALL, BK_K_SMALL>), grid, dim3(BK_THREADS), 0, s, bp);
+  else if (P <= BK_MID_MAX_P)
+    hipLaunchKernelGGL((qr_block_kernel<BK_R, BK_K_MID>), grid, dim3(BK_THREADS), 0, s, bp);
   else
     hipLaunchKernelGGL((qr_block_kernel<BK_R, BK_K_BIG>), grid, dim3(BK_THREADS), 0, s, bp);
   return hipGetLastError();
@@ -1882,11 +2108,19 @@ int resident_cap(bool small, hipError_t *err) {
   std::lock_guard<std::mutex> g(mu);
   int &c = cap[dev][small ? 1 : 0];
   if (c == 0) {
-    int per_cu = 0, cus = 0;
-    *err = small ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                       &per_cu, qr_block_kernel<BK_R_SMALL, BK_K_SMALL>, BK_THREADS, 0)
-                 : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, qr_block_kernel<BK_R, BK_K_BIG>,
-                                                                BK_THREADS, 0);
+    int per_cu = 0, per_cu_mid = 0, cus = 0;
+    if (small) {
+      *err = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per_cu, qr_block_kernel<BK_R_SMALL, BK_K_SMALL>, BK_THREADS, 0);
+    } else {
+      // (the 32-row launches take one of two kernels: the smaller count)
+      *err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, qr_block_kernel<BK_R, BK_K_BIG>,
+                                                          BK_THREADS, 0);
+      if (*err == hipSuccess)
+        *err = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &per_cu_mid, qr_block_kernel<BK_R, BK_K_MID>, BK_THREADS, 0);
+      per_cu = std::min(per_cu, per_cu_mid);
+    }
     if (*err != hipSuccess) return 0;
     if ((*err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) !=
         hipSuccess)
