@@ -116,6 +116,33 @@ def test_qr_matches_oracle(n):
     assert np.array_equal(host(Ad), A)   # input untouched
 
 
+@pytest.mark.parametrize("n", [3300, 4500])
+def test_qr_matches_oracle_32_row_blocks(n):
+    """Orders whose first blocks take 32 rows per thread: eight-column rounds
+    up to 16 workgroups (n = 3300: two blocks of 13; n = 4500: 16 down to 13
+    after four blocks of 18 and 17 workgroups with four-column rounds), then
+    the 16-row kernel."""
+    import paper_2607_20548_amd as soap
+    import oracle
+    import torch
+    log(f"qr n={n}")
+    A = _well_conditioned(n, 3)
+    Ad = dev(A)
+    Qd = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    Rd = torch.empty((n, n), dtype=torch.float32, device="cuda")
+    wsb = soap.soap_qr_workspace_bytes(n)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    soap.soap_qr_f32(n, Ad, Qd, Rd, ws, wsb)
+    Q, R = host(Qd), host(Rd)
+    A64 = A.astype(np.float64)
+    Qo = oracle.householder_qr(A64)
+    assert column_signs_agree(Q, Qo)
+    assert rel(Q, Qo) <= 1e-4
+    assert np.linalg.norm(Q @ R - A64) / np.linalg.norm(A64) <= 1e-5
+    assert np.linalg.norm(Q.T @ Q - np.eye(n)) / np.sqrt(n) <= 1e-5
+    assert np.all(np.tril(R, -1) == 0) and np.all(np.diag(R) >= 0)
+
+
 @pytest.mark.parametrize("n", [255, 256, 257, 300, 640, 1000, 1500])
 def test_qr_q_only_matches_oracle(n):
     """Without an R output (the SOAP step's call): the same Q as with one, to
