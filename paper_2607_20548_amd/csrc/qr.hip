@@ -506,9 +506,10 @@ __global__ __launch_bounds__(256) void qr_inner_apply_kernel(ApplyParams p) {
 //     in the diagonal rows j..j+K-1, and every workgroup reads back the P
 //     partials of each dot of the columns it needs and sums them in one
 //     fixed order, so that all of them hold bit-identical totals;
-//   * from the totals of the pivot columns, one wave forms the round's
-//     reflectors (Gram recurrence below), and every thread applies them to its
-//     own column as one combination of the tails.
+//   * from the totals of the pivot columns, every thread (rounds of up to
+//     four columns) or wave 0 with one lane per pivot (more) forms the
+//     round's reflectors (Gram recurrence below), and every thread applies
+//     them to its own column as one combination of the tails.
 // Workgroup 0 holds the block's diagonal rows: its broadcasts are zero at and
 // above each pivot's diagonal row (so its dot products need no masks), and it
 // keeps S = strict upper part of Y^T Y (from the same dot products), from
@@ -744,7 +745,9 @@ __global__ __launch_bounds__(BK_THREADS) void qr_block_kernel(BlockParams p) {
   constexpr int RS = BK_PARTS * R;
   // Items per lane of a gather: the P partials of one dot over 8 / K' lanes
   // (K' = columns of the round rounded up to a power of two), at most H
-  // (registers).  Launches of the big kernel with more than 56 workgroups
+  // (registers): eight-column rounds hold one dot's P partials per lane
+  // (launched for at most BK_MID_MAX_P or BK_SMALL_MAX_P workgroups), and
+  // launches of the four-column 32-row kernel with more than 56 workgroups
   // (orders past 14336) take two columns per round.
   constexpr int KP2 = KM > 4 ? 8 : (KM > 2 ? 4 : KM);
   constexpr int H = R == BK_R ? (KM > 4 ? BK_MID_MAX_P : 28) : (BK_SMALL_MAX_P * KP2 + 7) / 8;
