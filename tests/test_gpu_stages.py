@@ -170,13 +170,14 @@ def test_qr_q_only_matches_oracle(n):
     assert np.linalg.norm(Q.T @ Q - np.eye(n)) / np.sqrt(n) <= 1e-5
 
 
-@pytest.mark.parametrize("n", [300, 640])
+@pytest.mark.parametrize("n", [300, 640, 3300])
 def test_qr_nearly_dependent_neighbour_columns(n):
     """Every third column is 1.5 x its left neighbour plus 5% of a fresh
     direction: the reflector of the left column removes most of it, so the
-    block factorization takes that column in a round of its own (no
-    two-column round), at every alignment.  Q against the oracle and the
-    residuals at the usual bar."""
+    block factorization ends a round right before that column, at every
+    alignment within the rounds (n = 3300: also in the 32-row kernel with
+    eight-column rounds).  Q against the oracle and the residuals at the
+    usual bar."""
     import paper_2607_20548_amd as soap
     import oracle
     import torch
