@@ -177,14 +177,31 @@ hipError_t launch_axpby_bf16(float *W, const uint16_t *X, int64_t count, float a
 // makes every later call whose status_bit is in `mask` start with its
 // matrices' abort flags raised (a test hook: every bounded wait then ends at
 // once and the kernels exit normally).
+//
+// With `split`, the batch is two factors' matrices of the same order (batch
+// = 2 half): Q is then a contiguous buffer of the whole batch that the call
+// uses as its own, and at the end entries [0, half) are copied to QA and
+// [half, 2 half) to QB; a failed entry is not copied and or-s bitA or bitB
+// (by its half) into *status (status_bit is not used; Rf must be null).
+struct QrSplitOut {
+  float *QA;
+  float *QB;
+  int64_t half;
+  unsigned bitA;
+  unsigned bitB;
+};
 size_t qr_workspace_bytes(int64_t batch, int64_t n);
 void qr_force_give_up(unsigned mask);
+// Whether a call over `batch` matrices of order n runs the resident block
+// factorization on the current device (else the slower panel path).
+hipError_t qr_block_path(int64_t batch, int64_t n, bool *out);
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
                                 hipStream_t st, unsigned *status, unsigned status_bit,
                                 hipEvent_t q_free = nullptr,
                                 hipEvent_t mid = nullptr, float mid_frac = 0.5f,
-                                const std::function<hipError_t()> &at_mid = {});
+                                const std::function<hipError_t()> &at_mid = {},
+                                const QrSplitOut *split = nullptr);
 // dst = src^T for one n x n row-major matrix.
 hipError_t launch_transpose(float *dst, const float *src, int64_t n, hipStream_t s);
 

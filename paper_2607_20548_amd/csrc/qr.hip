@@ -1579,6 +1579,34 @@ __global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *d
   }
 }
 
+// Q of entry bz of a call over two factors' matrices (contiguous, n x n each)
+// to its owner: Q_A + bz nn for bz < half, Q_B + (bz - half) nn after.  An
+// entry whose factorization failed is not copied (its destination keeps the
+// Q it held) and its half's bit is or-ed into *status.
+__global__ __launch_bounds__(256) void qr_scatter_q_kernel(const float *Qs, float *QA, float *QB,
+                                                           int64_t half, int64_t nn,
+                                                           const unsigned *skip, int64_t sSkip,
+                                                           unsigned *status, unsigned bitA,
+                                                           unsigned bitB) {
+  const int64_t bz = blockIdx.y;
+  if (skip && skip[bz * sSkip] != 0u) {
+    if (status && blockIdx.x == 0 && threadIdx.x == 0)
+      __hip_atomic_fetch_or(status, bz < half ? bitA : bitB, __ATOMIC_RELAXED,
+                            __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  const float *src = Qs + bz * nn;
+  float *dst = bz < half ? QA + bz * nn : QB + (bz - half) * nn;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  if ((nn & 3) == 0) {   // every entry then starts 16-byte aligned
+    const float4 *s4 = reinterpret_cast<const float4 *>(src);
+    float4 *d4 = reinterpret_cast<float4 *>(dst);
+    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn / 4; e += stride) d4[e] = s4[e];
+  } else {
+    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += stride) dst[e] = src[e];
+  }
+}
+
 // The first w columns of W = Y^T Q[c:, c:] for a group of w reflectors
 // starting at column c, while rows and columns c..c+w-1 of Q still hold
 // diag(d): W[i][j] = Y[j][i] d[c+j] = At[c+i][c+j] d[c+j] (i, j < w).
@@ -2137,27 +2165,39 @@ int resident_cap(bool small, hipError_t *err) {
 
 void qr_force_give_up(unsigned mask) { g_force_give_up.store(mask); }
 
+hipError_t qr_block_path(int64_t batch, int64_t n, bool *out) {
+  *out = qr_layout(batch, n).block;
+  if (!*out) return hipSuccess;
+  hipError_t err = hipSuccess;
+  const int cap_big = resident_cap(false, &err);
+  if (err != hipSuccess) return err;
+  const int64_t P0 = (n + BK_ROWS - 1) / BK_ROWS;
+  *out = P0 * batch <= std::min(BK_MAX_WG, cap_big);
+  return hipSuccess;
+}
+
 hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, int64_t n,
                                 void *ws, size_t ws_bytes, hipStream_t s, hipStream_t sp,
                                 hipStream_t st, unsigned *status, unsigned status_bit,
                                 hipEvent_t q_free, hipEvent_t mid, float mid_frac,
-                                const std::function<hipError_t()> &at_mid) {
+                                const std::function<hipError_t()> &at_mid,
+                                const QrSplitOut *split) {
   QrCtx x;
   x.L = qr_layout(batch, n);
   if (ws_bytes < x.L.total) return hipErrorInvalidValue;
+  if (split && (Rf || batch != 2 * split->half || !split->QA || !split->QB))
+    return hipErrorInvalidValue;
   x.cap_small = BK_MAX_WG;
   if (x.L.block) {   // resident blocks only where the device holds them all at once
+    SOAP_TRY(qr_block_path(batch, n, &x.L.block));
     hipError_t err = hipSuccess;
-    const int cap_big = resident_cap(false, &err);
-    if (err != hipSuccess) return err;
     const int cap_small = resident_cap(true, &err);
     if (err != hipSuccess) return err;
-    const int64_t P0 = (n + BK_ROWS - 1) / BK_ROWS;
-    x.L.block = P0 * batch <= std::min(BK_MAX_WG, cap_big);
     x.cap_small = std::min(BK_MAX_WG, cap_small);
   }
-  x.status = status;
-  x.status_bit = status_bit;
+  // (with two destinations the scatter of the Q's reports failures per half)
+  x.status = split ? nullptr : status;
+  x.status_bit = split ? 0u : status_bit;
   char *base = static_cast<char *>(ws);
   x.At = At; x.Q = Q; x.Rf = Rf; x.batch = batch; x.n = n; x.sA = n * n; x.ni = (int)n;
   x.Tb = reinterpret_cast<float *>(base + x.L.t_off);
@@ -2193,11 +2233,15 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     SOAP_TRY(hipGetLastError());
     x.skip = x.xch + BK_XFAILED;
     x.sSkip = xs;
-    if (g_force_give_up.load() & status_bit) {
-      hipLaunchKernelGGL(qr_raise_abort_kernel,
-                         dim3((unsigned)std::min<int64_t>((batch + 63) / 64, 1024)), dim3(64), 0,
-                         s, x.xch, xs, batch);
-      SOAP_TRY(hipGetLastError());
+    for (int h = 0; h < (split ? 2 : 1); ++h) {
+      const unsigned bit = split ? (h ? split->bitB : split->bitA) : status_bit;
+      const int64_t cnt = split ? split->half : batch;
+      if (g_force_give_up.load() & bit) {
+        hipLaunchKernelGGL(qr_raise_abort_kernel,
+                           dim3((unsigned)std::min<int64_t>((cnt + 63) / 64, 1024)), dim3(64), 0,
+                           s, x.xch + h * cnt * xs, xs, cnt);
+        SOAP_TRY(hipGetLastError());
+      }
     }
   }
 
@@ -2312,6 +2356,13 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     SOAP_TRY(q_update(x, 4 * q * NB, 4 * NB, x.TQ + q * 16 * NB * NB, 4 * NB, x.L.sTQ, s));
   for (int64_t o8 = no - 1; o8 >= 0; --o8)
     SOAP_TRY(q_update(x, 8 * o8 * NB, 8 * NB, x.TO + o8 * 64 * NB * NB, 8 * NB, x.L.sTO, s));
+  if (split) {
+    const unsigned gx = (unsigned)std::min<int64_t>((n * n / 4 + 255) / 256, 1024);
+    hipLaunchKernelGGL(qr_scatter_q_kernel, dim3(std::max(gx, 1u), (unsigned)batch), dim3(256), 0,
+                       s, Q, split->QA, split->QB, split->half, n * n, x.skip, x.sSkip, status,
+                       split->bitA, split->bitB);
+    SOAP_TRY(hipGetLastError());
+  }
   return hipSuccess;
 }
 

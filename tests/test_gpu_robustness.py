@@ -97,11 +97,13 @@ def test_forced_give_up_of_both_qrs_keeps_the_bases(kl):
             " ".join(f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}" for k, v in errs.items()))
 
 
+@pytest.mark.parametrize("m,n", [(300, 600), (320, 320)])
 @pytest.mark.parametrize("side", ["L", "R"])
-def test_forced_give_up_of_one_qr_keeps_only_that_basis(side):
+def test_forced_give_up_of_one_qr_keeps_only_that_basis(side, m, n):
+    """One side's QR gives up (320 x 320: both QRs are one call over two
+    matrices, and the give-up of one half keeps only that half's basis)."""
     import paper_2607_20548_amd as soap
     import oracle
-    m, n = 300, 600
     grads = _grads(m, n, 3, 7)
     W0 = (0.02 * np.random.default_rng(6).standard_normal((m, n))).astype(np.float32)
     gs = soap.SoapState(m, n)
@@ -193,6 +195,40 @@ def test_forced_give_up_batched_keeps_every_entry():
             else:
                 sts[b] = oracle.soap_step(sts[b], G[b].astype(np.float64), t, **HP)
             compare_state(sts[b], gs, f"entry {b} t={t}", b=b)
+            assert rel(host(W)[b], sts[b].W) <= 1e-4
+
+
+@pytest.mark.parametrize("side", ["L", "R"])
+def test_forced_give_up_batched_square_keeps_that_side(side):
+    """Three 320 x 320 matrices: both sides' QRs are one call over six
+    matrices; a forced give-up of one side keeps that side's basis in every
+    entry and refreshes the other side's."""
+    import paper_2607_20548_amd as soap
+    B, m = 3, 320
+    grads = _grads(m, m, 2, 9, batch=B)
+    W0 = (0.02 * np.random.default_rng(8).standard_normal((B, m, m))).astype(np.float32)
+    gs = soap.SoapState(m, m, batch=B)
+    W = dev(W0)
+    import oracle
+    sts = [oracle.init_state(W0[b].astype(np.float64)) for b in range(B)]
+    bit = soap.SOAP_STATUS_QR_L if side == "L" else soap.SOAP_STATUS_QR_R
+    for t, G in enumerate(grads, start=1):
+        forced = t == 2
+        Q_prev = (host(gs.Q_L), host(gs.Q_R))
+        soap.soap_test_force_qr_give_up(bit if forced else 0)
+        gs.step(W, dev(G), t, **HP)
+        soap.soap_test_force_qr_give_up(0)
+        assert gs.status() == ((soap.SOAP_ERR_QR_GAVE_UP, bit) if forced else (soap.SOAP_OK, 0))
+        if forced:
+            assert np.array_equal(host(gs.Q_L if side == "L" else gs.Q_R),
+                                  Q_prev[0] if side == "L" else Q_prev[1])
+        for b in range(B):
+            if forced:
+                sts[b], _ = _oracle_one_side_kept(sts[b], G[b].astype(np.float64), t,
+                                                  keep_left=side == "L")
+            else:
+                sts[b] = oracle.soap_step(sts[b], G[b].astype(np.float64), t, **HP)
+            compare_state(sts[b], gs, f"square {side} entry {b} t={t}", b=b)
             assert rel(host(W)[b], sts[b].W) <= 1e-4
 
 

@@ -57,6 +57,16 @@ def test_wide_shapes_several_reflector_groups(m, n):
                    (0.02 * rng.standard_normal((m, n))).astype(np.float32))
 
 
+@pytest.mark.parametrize("m,n", [(200, 200), (520, 520), (1100, 1100)])
+def test_square_shapes(m, n):
+    """Square weights: both factors' QRs run as one call over two matrices
+    when A_L, A_R (and T_G, T_M) lie back to back in the workspace (m^2 a
+    multiple of 64: 200, 520); 1100 takes two separate QRs."""
+    rng = np.random.default_rng([m, n, 26])
+    _run_open_loop(m, n, recipe_grads(m, n, 3, 26),
+                   (0.02 * rng.standard_normal((m, n))).astype(np.float32))
+
+
 @pytest.mark.parametrize("m,n", [(37, 70), (200, 257)])
 def test_ragged_shapes_gaussian_stress(m, n):
     """Full-rank Gaussian gradients: ill-conditioned factors, checked with the
@@ -136,6 +146,37 @@ def test_batched_matches_single_and_oracle():
             assert rel(host(gb.Q_R)[b], host(singles[b].Q_R)) <= 1e-6
             assert rel(Wbh[b], sts[b].W) <= TOL
             assert rel(host(gb.Q_L)[b], sts[b].QL) <= TOL
+            assert rel(host(gb.V)[b], sts[b].V) <= TOL
+
+
+def test_batched_square_matches_single_and_oracle():
+    """Three square matrices through soap_step_batched: one QR call over the
+    six factors; every entry's bases and weight follow the oracle and equal
+    the single-matrix steps' (one QR call over two factors each)."""
+    import paper_2607_20548_amd as soap
+    import oracle
+    B, m = 3, 200
+    rng = np.random.default_rng(27)
+    W0 = (0.02 * rng.standard_normal((B, m, m))).astype(np.float32)
+    grads = recipe_grads(m, m, 3, 27, batch=B)
+    gb = soap.SoapState(m, m, batch=B)
+    Wb = dev(W0)
+    singles = [soap.SoapState(m, m) for _ in range(B)]
+    Ws = [dev(W0[b]) for b in range(B)]
+    sts = [oracle.init_state(W0[b].astype(np.float64)) for b in range(B)]
+    for t, G in enumerate(grads, start=1):
+        gb.step(Wb, dev(G), t, **HP)
+        assert gb.status() == (soap.SOAP_OK, 0)
+        for b in range(B):
+            singles[b].step(Ws[b], dev(G[b]), t, **HP)
+            sts[b] = oracle.soap_step(sts[b], G[b].astype(np.float64), t, **HP)
+        Wbh, QLb, QRb = host(Wb), host(gb.Q_L), host(gb.Q_R)
+        for b in range(B):
+            assert rel(Wbh[b], host(Ws[b])) <= 1e-6
+            assert rel(QLb[b], host(singles[b].Q_L)) <= 1e-6
+            assert rel(QRb[b], host(singles[b].Q_R)) <= 1e-6
+            assert rel(Wbh[b], sts[b].W) <= TOL
+            assert rel(QLb[b], sts[b].QL) <= TOL and rel(QRb[b], sts[b].QR) <= TOL
             assert rel(host(gb.V)[b], sts[b].V) <= TOL
 
 
