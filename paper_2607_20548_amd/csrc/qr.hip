@@ -1580,11 +1580,13 @@ __global__ __launch_bounds__(256) void qr_init_q_kernel(float *Q, const float *d
 }
 
 // Q of entry bz of a call over two factors' matrices (contiguous, n x n each)
-// to its owner: Q_A + bz nn for bz < half, Q_B + (bz - half) nn after.  An
+// to its owner: Q_A + bz nn for bz < half, Q_B + (bz - half) nn after, with
+// column j scaled by dsign[bz n + j] (the signs that make diag(R) >= 0).  An
 // entry whose factorization failed is not copied (its destination keeps the
 // Q it held) and its half's bit is or-ed into *status.
 __global__ __launch_bounds__(256) void qr_scatter_q_kernel(const float *Qs, float *QA, float *QB,
-                                                           int64_t half, int64_t nn,
+                                                           int64_t half, int n,
+                                                           const float *dsign,
                                                            const unsigned *skip, int64_t sSkip,
                                                            unsigned *status, unsigned bitA,
                                                            unsigned bitB) {
@@ -1595,16 +1597,34 @@ __global__ __launch_bounds__(256) void qr_scatter_q_kernel(const float *Qs, floa
                             __HIP_MEMORY_SCOPE_AGENT);
     return;
   }
+  const int64_t nn = (int64_t)n * n;
   const float *src = Qs + bz * nn;
+  const float *d = dsign ? dsign + bz * n : nullptr;
   float *dst = bz < half ? QA + bz * nn : QB + (bz - half) * nn;
   const int64_t stride = (int64_t)gridDim.x * 256;
-  if ((nn & 3) == 0) {   // every entry then starts 16-byte aligned
+  if ((n & 3) == 0) {   // every entry starts 16-byte aligned; four columns of one row
     const float4 *s4 = reinterpret_cast<const float4 *>(src);
     float4 *d4 = reinterpret_cast<float4 *>(dst);
-    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn / 4; e += stride) d4[e] = s4[e];
+    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn / 4; e += stride) {
+      float4 v = s4[e];
+      if (d) {
+        const int j = (int)((4 * e) % n);
+        v.x *= d[j]; v.y *= d[j + 1]; v.z *= d[j + 2]; v.w *= d[j + 3];
+      }
+      d4[e] = v;
+    }
   } else {
-    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += stride) dst[e] = src[e];
+    for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += stride)
+      dst[e] = d ? src[e] * d[e % n] : src[e];
   }
+}
+
+// Q = I for every matrix of the batch (n x n, batch stride sA).
+__global__ __launch_bounds__(256) void qr_identity_kernel(float *Q, int n, int64_t sA) {
+  float *Qb = Q + (int64_t)blockIdx.y * sA;
+  const int64_t nn = (int64_t)n * n;
+  for (int64_t e = blockIdx.x * 256 + threadIdx.x; e < nn; e += (int64_t)gridDim.x * 256)
+    Qb[e] = (e / n == e % n) ? 1.f : 0.f;
 }
 
 // The first w columns of W = Y^T Q[c:, c:] for a group of w reflectors
@@ -1670,7 +1690,9 @@ struct QrLayout {
   bool block;          // outer blocks factored by qr_block_kernel (else the panel path)
   size_t t_off, w_off, w2_off, sk_off, part_off, wi_off, d_off, b_off, cnt_off, x_off, total;
   size_t tp_off, sx_off, skp_off, skp2_off, tq_off, sq_off, to_off, so_off, wn_off, skn_off;
+  size_t fv_off;
   int64_t sT, sWbuf, sSk, sPart, sWi;
+  int64_t sFv;         // the forward Q formation's V = Q Y and V T (n x 2 NB each)
   int64_t sWn, sSkn;   // the near update's own W, W2 (NB x NB each) and split-K partials
   int64_t np;          // pairs of full outer blocks
   int64_t nq;          // quads (pairs of full pairs)
@@ -1713,6 +1735,7 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.sSo = L.no * 32 * NB * NB;
   L.sPart = P * PART_STRIDE;
   L.sWi = (int64_t)MAX_B * NB;
+  L.sFv = (int64_t)4 * NB * n;
   size_t o = 0;
   L.t_off = o;    o = align256(o + sizeof(float) * batch * L.sT);
   L.w_off = o;    o = align256(o + sizeof(float) * batch * L.sWbuf);
@@ -1733,6 +1756,7 @@ QrLayout qr_layout(int64_t batch, int64_t n) {
   L.so_off = o;   o = align256(o + sizeof(float) * batch * L.sSo);
   L.wn_off = o;   o = align256(o + sizeof(float) * batch * L.sWn);
   L.skn_off = o;  o = align256(o + sizeof(float) * batch * L.sSkn);
+  L.fv_off = o;   o = align256(o + sizeof(float) * batch * L.sFv);
   // The resident-block path needs every workgroup of a launch resident at
   // once: at most BK_MAX_WG workgroups (two such launches, one per factor,
   // may run together on the 256 compute units).
@@ -1815,6 +1839,7 @@ struct QrCtx {
   float *TP, *Sx, *Skp, *TQ, *Sq, *TO, *So;
   float *Wn, *Skn;
   float *Skp2;     // split-K partials of the pair T's (the merges use Skp)
+  float *Fv;       // V and V T of the forward Q formation
 };
 
 hipError_t panel_phase(const QrCtx &x, int64_t ob, hipStream_t s);
@@ -2122,6 +2147,45 @@ hipError_t q_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_
   return launch_gemm(g3, s);
 }
 
+// Forward Q formation: Q[:, c:] -= ((Q[:, c:] Y) T) Y^T for the w
+// reflectors stored in At rows c..c+w-1 (explicit: zero before their pivot,
+// one on it), i.e. Q <- Q (I - Y T Y^T).  Applied group after group from
+// the first on, it accumulates Q = H_1 H_2 ... (the column signs follow at
+// the copy out).  Every row of Q takes part (2 n^3 flops in all, against
+// (4/3) n^3 backwards), but each group's update can run as soon as its T
+// exists, beside the factorization; capped to `max_wg` workgroups so that
+// whole compute units stay free for the block kernels.
+hipError_t q_forward_update(const QrCtx &x, int64_t c, int64_t w, const float *T, int64_t ldt,
+                            int64_t sT, int max_wg, hipStream_t s) {
+  const int64_t n = x.n, Kr = n - c;
+  float *V = x.Fv, *V2 = x.Fv + 2 * NB * n;
+  GemmDesc g1;  // V = Q[:, c:] Y:  op(B)[k][j] = Y[k][j] = At[c+j][c+k]
+  g1.trans_a = 0; g1.trans_b = 1; g1.M = n; g1.N = w; g1.K = Kr;
+  g1.A = x.Q + c; g1.lda = n; g1.sA = x.sA;
+  g1.B = x.At + c * n + c; g1.ldb = n; g1.sB = x.sA;
+  g1.C = V; g1.ldc = w; g1.sC = x.L.sFv; g1.batch = x.batch;
+  g1.skip = x.skip; g1.sSkip = x.sSkip; g1.max_wg = max_wg;
+  SOAP_TRY(launch_gemm(g1, s));
+  GemmDesc g2;  // V2 = V T
+  g2.M = n; g2.N = w; g2.K = w;
+  g2.A = V; g2.lda = w; g2.sA = x.L.sFv;
+  g2.B = T; g2.ldb = ldt; g2.sB = sT;
+  g2.C = V2; g2.ldc = w; g2.sC = x.L.sFv; g2.batch = x.batch;
+  g2.skip = x.skip; g2.sSkip = x.sSkip; g2.max_wg = max_wg;
+  SOAP_TRY(launch_gemm(g2, s));
+  GemmDesc g3;  // Q[:, c:] -= V2 Y^T:  B = Y^T = At rows c..c+w-1 from column c
+  g3.M = n; g3.N = Kr; g3.K = w;
+  g3.A = V2; g3.lda = w; g3.sA = x.L.sFv;
+  g3.B = x.At + c * n + c; g3.ldb = n; g3.sB = x.sA;
+  g3.C = x.Q + c; g3.ldc = n; g3.sC = x.sA;
+  g3.alpha = -1.f; g3.beta = 1.f; g3.batch = x.batch;
+  g3.skip = x.skip; g3.sSkip = x.sSkip; g3.max_wg = max_wg;
+  return launch_gemm(g3, s);
+}
+
+// Workgroups of a forward Q update running beside the factorization.
+constexpr int FWD_MAX_WG = 160;
+
 std::atomic<unsigned> g_force_give_up{0};
 
 // Workgroups of one block-kernel launch (R rows per thread) that the current
@@ -2220,7 +2284,12 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   x.So = reinterpret_cast<float *>(base + x.L.so_off);
   x.Wn = reinterpret_cast<float *>(base + x.L.wn_off);
   x.Skn = reinterpret_cast<float *>(base + x.L.skn_off);
+  x.Fv = reinterpret_cast<float *>(base + x.L.fv_off);
   const int64_t nob = x.L.nob, np = x.L.np;
+  // With two destinations Q is the call's own buffer, written as the
+  // factorization runs: formed forwards, group by group beside it (a failed
+  // matrix's partial Q is never copied out).
+  const bool fwd = split != nullptr;
 
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
   x.skip = nullptr;
@@ -2258,6 +2327,13 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   SOAP_TRY(t_events.get(&ev));
   SOAP_TRY(hipEventRecord(ev, s));
   SOAP_TRY(hipStreamWaitEvent(sp, ev, 0));
+  if (fwd) {   // Q = I on the stream of the forward updates
+    SOAP_TRY(hipStreamWaitEvent(st, ev, 0));
+    const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
+    hipLaunchKernelGGL(qr_identity_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, st, Q, x.ni,
+                       x.sA);
+    SOAP_TRY(hipGetLastError());
+  }
   SOAP_TRY(factor_block(x, 0, sp));
   hipEvent_t ev_f;                                // block ob factored (on sp)
   SOAP_TRY(t_events.get(&ev_f));
@@ -2296,7 +2372,13 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
                          x.At, x.sA, x.Rf, x.dsign, x.ni, (int)((ob - 1) * NB));
       SOAP_TRY(hipGetLastError());
       SOAP_TRY(pair_t(x, p, s));
-      if (p % 2 == 1 && p / 2 < x.L.nq) {                  // quad (p-1, p) complete
+      if (fwd) {                                           // Q <- Q (I - Y_p T_p Y_p^T)
+        SOAP_TRY(t_events.get(&ev));
+        SOAP_TRY(hipEventRecord(ev, s));
+        SOAP_TRY(hipStreamWaitEvent(st, ev, 0));
+        SOAP_TRY(q_forward_update(x, 2 * p * NB, 2 * NB, x.TP + p * 4 * NB * NB, 2 * NB, x.L.sTP,
+                                  FWD_MAX_WG, st));
+      } else if (p % 2 == 1 && p / 2 < x.L.nq) {           // quad (p-1, p) complete
         SOAP_TRY(t_events.get(&ev));
         SOAP_TRY(hipEventRecord(ev, s));
         SOAP_TRY(hipStreamWaitEvent(st, ev, 0));
@@ -2314,7 +2396,7 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
     if (mid) SOAP_TRY(hipEventRecord(mid, s));
     if (at_mid) SOAP_TRY(at_mid());
   }
-  if (np > 0) {                                                 // pair T's done
+  if (np > 0 || fwd) {                                          // pair T's (or Q) done
     SOAP_TRY(t_events.get(&ev));
     SOAP_TRY(hipEventRecord(ev, st));
     SOAP_TRY(hipStreamWaitEvent(s, ev, 0));
@@ -2326,41 +2408,49 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
                        x.dsign, x.ni, x.sA, (int)np);
     SOAP_TRY(hipGetLastError());
   }
-  if (np > 0) {   // R is no longer needed: clear it above the block rows of every column
-    const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
-    hipLaunchKernelGGL(qr_zero_above_blocks_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s,
-                       At, x.ni, x.sA);
-    SOAP_TRY(hipGetLastError());
-  }
+  if (fwd) {   // the blocks past the last full pair, forwards
+    for (int64_t ob = 2 * np; ob < nob; ++ob) {
+      const int64_t c = ob * NB;
+      SOAP_TRY(q_forward_update(x, c, std::min<int64_t>(n, c + NB) - c, x.Tb + ob * NB * NB, NB,
+                                x.L.sT, 0, s));
+    }
+  } else {
+    if (np > 0) {   // R is no longer needed: clear it above the block rows of every column
+      const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
+      hipLaunchKernelGGL(qr_zero_above_blocks_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s,
+                         At, x.ni, x.sA);
+      SOAP_TRY(hipGetLastError());
+    }
 
-  // Explicit Q (row-major), accumulated backwards from diag(d).
-  if (q_free) SOAP_TRY(hipStreamWaitEvent(s, q_free, 0));
-  {
-    const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
-    hipLaunchKernelGGL(qr_init_q_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, Q, x.dsign,
-                       x.ni, x.sA, x.skip, x.sSkip);
-    SOAP_TRY(hipGetLastError());
+    // Explicit Q (row-major), accumulated backwards from diag(d).
+    if (q_free) SOAP_TRY(hipStreamWaitEvent(s, q_free, 0));
+    {
+      const unsigned gx = (unsigned)std::min<int64_t>((n * n + 255) / 256, 2048);
+      hipLaunchKernelGGL(qr_init_q_kernel, dim3(gx, (unsigned)batch), dim3(256), 0, s, Q, x.dsign,
+                         x.ni, x.sA, x.skip, x.sSkip);
+      SOAP_TRY(hipGetLastError());
+    }
+    // Backwards: the blocks past the last full pair one by one, then the
+    // pairs, quads and octs past the last full group of the next size as
+    // rank-2NB, 4NB and 8NB updates (longer K per product: the update runs
+    // nearer the matrix cores' rate than with rank 256).
+    const int64_t nq = x.L.nq, no = x.L.no;
+    for (int64_t ob = nob - 1; ob >= 2 * np; --ob) {
+      const int64_t c = ob * NB;
+      SOAP_TRY(q_update(x, c, std::min<int64_t>(n, c + NB) - c, x.Tb + ob * NB * NB, NB, x.L.sT, s));
+    }
+    for (int64_t p = np - 1; p >= 2 * nq; --p)
+      SOAP_TRY(q_update(x, 2 * p * NB, 2 * NB, x.TP + p * 4 * NB * NB, 2 * NB, x.L.sTP, s));
+    for (int64_t q = nq - 1; q >= 2 * no; --q)
+      SOAP_TRY(q_update(x, 4 * q * NB, 4 * NB, x.TQ + q * 16 * NB * NB, 4 * NB, x.L.sTQ, s));
+    for (int64_t o8 = no - 1; o8 >= 0; --o8)
+      SOAP_TRY(q_update(x, 8 * o8 * NB, 8 * NB, x.TO + o8 * 64 * NB * NB, 8 * NB, x.L.sTO, s));
   }
-  // Backwards: the blocks past the last full pair one by one, then the
-  // pairs, quads and octs past the last full group of the next size as
-  // rank-2NB, 4NB and 8NB updates (longer K per product: the update runs
-  // nearer the matrix cores' rate than with rank 256).
-  const int64_t nq = x.L.nq, no = x.L.no;
-  for (int64_t ob = nob - 1; ob >= 2 * np; --ob) {
-    const int64_t c = ob * NB;
-    SOAP_TRY(q_update(x, c, std::min<int64_t>(n, c + NB) - c, x.Tb + ob * NB * NB, NB, x.L.sT, s));
-  }
-  for (int64_t p = np - 1; p >= 2 * nq; --p)
-    SOAP_TRY(q_update(x, 2 * p * NB, 2 * NB, x.TP + p * 4 * NB * NB, 2 * NB, x.L.sTP, s));
-  for (int64_t q = nq - 1; q >= 2 * no; --q)
-    SOAP_TRY(q_update(x, 4 * q * NB, 4 * NB, x.TQ + q * 16 * NB * NB, 4 * NB, x.L.sTQ, s));
-  for (int64_t o8 = no - 1; o8 >= 0; --o8)
-    SOAP_TRY(q_update(x, 8 * o8 * NB, 8 * NB, x.TO + o8 * 64 * NB * NB, 8 * NB, x.L.sTO, s));
   if (split) {
     const unsigned gx = (unsigned)std::min<int64_t>((n * n / 4 + 255) / 256, 1024);
     hipLaunchKernelGGL(qr_scatter_q_kernel, dim3(std::max(gx, 1u), (unsigned)batch), dim3(256), 0,
-                       s, Q, split->QA, split->QB, split->half, n * n, x.skip, x.sSkip, status,
-                       split->bitA, split->bitB);
+                       s, Q, split->QA, split->QB, split->half, x.ni, fwd ? x.dsign : nullptr,
+                       x.skip, x.sSkip, status, split->bitA, split->bitB);
     SOAP_TRY(hipGetLastError());
   }
   return hipSuccess;
