@@ -97,11 +97,12 @@ def test_forced_give_up_of_both_qrs_keeps_the_bases(kl):
             " ".join(f"{k}={v:.2e}" if isinstance(v, float) else f"{k}={v}" for k, v in errs.items()))
 
 
-@pytest.mark.parametrize("m,n", [(300, 600), (320, 320)])
+@pytest.mark.parametrize("m,n", [(300, 600), (320, 320), (1100, 300)])
 @pytest.mark.parametrize("side", ["L", "R"])
 def test_forced_give_up_of_one_qr_keeps_only_that_basis(side, m, n):
     """One side's QR gives up (320 x 320: both QRs are one call over two
-    matrices, and the give-up of one half keeps only that half's basis)."""
+    matrices, and the give-up of one half keeps only that half's basis;
+    1100 x 300: the larger factor on the L side)."""
     import paper_2607_20548_amd as soap
     import oracle
     grads = _grads(m, n, 3, 7)

@@ -38,7 +38,7 @@ def test_workload0_ten_steps_open_loop():
 
 
 @pytest.mark.parametrize("m,n", [(1, 1), (3, 5), (37, 70), (130, 129), (200, 257), (300, 600),
-                                 (600, 300)])
+                                 (600, 300), (1100, 200)])
 def test_ragged_shapes(m, n):
     """Shapes that are not multiples of the tiles, with gradients of the
     workloads' recipe (low-rank signal + 10% noise)."""
