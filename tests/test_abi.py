@@ -108,6 +108,7 @@ def test_timing_api_without_gpu(L):
     n = soap.soap_timing_num_stages()
     names = [soap.soap_timing_stage_name(i) for i in range(n)]
     assert "qr_R" in names and "power_R" in names and len(set(names)) == n
+    assert "qr_L_R" in names   # both square factors' QRs as one call
     soap.soap_timing_reset()
     assert soap.soap_timing_get(0) == (0.0, 0, 0.0)
 
