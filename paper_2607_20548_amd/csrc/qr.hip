@@ -2185,6 +2185,11 @@ hipError_t q_forward_update(const QrCtx &x, int64_t c, int64_t w, const float *T
 
 // Workgroups of a forward Q update running beside the factorization.
 constexpr int FWD_MAX_WG = 160;
+// Largest order whose paired QR forms Q forwards: the block chain leaves
+// the device mostly idle up to here (a square 2048 step 7.8 -> 7.3 ms, 4096
+// 25.3 -> 23.9 ms); at 8192 its far updates already fill it and the extra
+// flops slow the chain (123 -> 135 ms).
+constexpr int64_t FWD_MAX_N = 4096;
 
 std::atomic<unsigned> g_force_give_up{0};
 
@@ -2286,10 +2291,10 @@ hipError_t qr_factor_and_form_q(float *At, float *Q, float *Rf, int64_t batch, i
   x.Skn = reinterpret_cast<float *>(base + x.L.skn_off);
   x.Fv = reinterpret_cast<float *>(base + x.L.fv_off);
   const int64_t nob = x.L.nob, np = x.L.np;
-  // With two destinations Q is the call's own buffer, written as the
-  // factorization runs: formed forwards, group by group beside it (a failed
-  // matrix's partial Q is never copied out).
-  const bool fwd = split != nullptr;
+  // With two destinations Q is the call's own buffer and, up to order
+  // FWD_MAX_N, is written as the factorization runs: formed forwards, group
+  // by group beside it (a failed matrix's partial Q is never copied out).
+  const bool fwd = split != nullptr && n <= FWD_MAX_N;
 
   SOAP_TRY(launch_zero_u32(x.cnt, batch, s));
   x.skip = nullptr;

@@ -736,10 +736,10 @@ int step_impl(int64_t batch, float *param, const float *grad, float *L, float *R
   // A_R (adjacent in the workspace).  Two factorizations side by side contend
   // for the compute units and double the launches of the block chain; one
   // call carries both in each launch (4096 x 4096, Q formed backwards: 14.6
-  // ms for the pair against 13.2 ms for one alone).  Its Q's are formed
-  // forwards in T_G, T_M (adjacent, free until the rotation) while the
-  // factorization runs, and copied to Q_L, Q_R; the rotation Q_L^T G then
-  // follows on the caller's stream.
+  // ms for the pair against 13.2 ms for one alone).  Its Q's are formed in
+  // T_G, T_M (adjacent, free until the rotation; up to order 4096 forwards,
+  // while the factorization runs) and copied to Q_L, Q_R; the rotation
+  // Q_L^T G then follows on the caller's stream.
   bool pair = false;
   if (refresh && !kl && m == n && AR == AL + batch * nn && TM == TG + batch * nn &&
       soap::qr_workspace_bytes(2 * batch, n) <= ws_bytes - lay.qrl) {

@@ -57,11 +57,13 @@ def test_wide_shapes_several_reflector_groups(m, n):
                    (0.02 * rng.standard_normal((m, n))).astype(np.float32))
 
 
-@pytest.mark.parametrize("m,n", [(200, 200), (520, 520), (1100, 1100)])
+@pytest.mark.parametrize("m,n", [(200, 200), (520, 520), (1100, 1100), (4104, 4104)])
 def test_square_shapes(m, n):
     """Square weights: both factors' QRs run as one call over two matrices
     when A_L, A_R (and T_G, T_M) lie back to back in the workspace (m^2 a
-    multiple of 64: 200, 520); 1100 takes two separate QRs."""
+    multiple of 64: 200, 520 with Q formed forwards; 4104, past the forward
+    threshold, with Q formed backwards in the call's buffer); 1100 takes two
+    separate QRs."""
     rng = np.random.default_rng([m, n, 26])
     _run_open_loop(m, n, recipe_grads(m, n, 3, 26),
                    (0.02 * rng.standard_normal((m, n))).astype(np.float32))
