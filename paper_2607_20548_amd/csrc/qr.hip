@@ -2187,8 +2187,8 @@ hipError_t q_forward_update(const QrCtx &x, int64_t c, int64_t w, const float *T
 constexpr int FWD_MAX_WG = 160;
 // Largest order whose paired QR forms Q forwards: the block chain leaves
 // the device mostly idle up to here (a square 2048 step 7.8 -> 7.3 ms, 4096
-// 25.3 -> 23.9 ms); at 8192 its far updates already fill it and the extra
-// flops slow the chain (123 -> 135 ms).
+// 25.3 -> 23.9 ms); from 6144 on its far updates already fill it and the
+// extra flops slow the chain (6144: 60.8 -> 63.7 ms, 8192: 123 -> 135 ms).
 constexpr int64_t FWD_MAX_N = 4096;
 
 std::atomic<unsigned> g_force_give_up{0};
